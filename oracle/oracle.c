@@ -1,0 +1,695 @@
+/*
+ * Plain CPU oracle for batched TFHE programmable bootstrapping (PBS) over the
+ * Goldilocks prime p = 2^64 - 2^32 + 1.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg do.  It shares no code, header, table or constant
+ * generator with the HIP library: every definition here is written out from
+ * the mathematics, slowly and plainly, so that it can be read against the
+ * paper by eye.
+ *
+ * What the paper fixes (ROSETTA, Sec. 2.2 "TFHE Scheme", PBS paragraph and
+ * Fig. rlwe_primitives(a)): a LUT f is laid out as the coefficients of a test
+ * polynomial v(X) in Z_Q[X]/(X^N+1); blind rotation uses the encrypted
+ * message as the rotation amount so that f(m) lands in the constant term,
+ * which is then extracted into a fresh LWE ciphertext.  Sec. 2.2.3 defines
+ * LWE Extract.  Everything the paper leaves open (modulus, modulus-switch
+ * rounding, gadget decomposition, GGSW layout, CMux form, key switching) is
+ * fixed by the conventions written next to each function below; the same
+ * conventions are stated in the library header, since they decide the output
+ * bits.
+ *
+ * Field arithmetic deliberately uses unsigned __int128 and the C '%'
+ * operator: slow, but obviously correct.  The hot-path has no floating point;
+ * doubles appear only in the Gaussian noise sampler used by key generation
+ * and encryption (test data, not the PBS itself).
+ *
+ * Two product kinds, bit-identical by construction of exact arithmetic:
+ *   OR_SCHOOLBOOK (tier 1) - negacyclic product by its definition, O(N^2);
+ *   OR_NTT        (tier 2) - textbook iterative radix-2 NTT of the twisted
+ *                            input (evaluation at the odd powers of a 2N-th
+ *                            root of unity), O(N log N).
+ * Tier 2 is pinned to tier 1 by the tests, then used where tier 1 is too slow.
+ *
+ * Pins (tests/test_oracle_field.py, tests/test_oracle_pbs.py), each checking
+ * against something other than this file's own formulas:
+ *   field       2^64 = 2^32-1, 2^96 = -1, Fermat, ring axioms, 7 generates
+ *               Z_p^* (p-1 = 2^32*3*5*17*257*65537)
+ *   product     X * X^(N-1) = -1, monomial closed forms, and (a*b)(z) =
+ *               a(z) b(z) at every root z of X^N+1 (Horner, big integers)
+ *   transform   value at psi^(2k+1) by Horner; inverse; product = schoolbook
+ *   modswitch   exact rational rounding (fractions), boundary values
+ *   decompose   reconstruction bound, digit ranges, brute force over all
+ *               spellings for tiny (levels, beta)
+ *   randomness  published SplitMix64 vector; Box-Muller moments
+ *   extract     decrypt_S(extract(C)) = phase(C)_0 exactly
+ *   ext. prod.  noise-free GGSW(0): phase 0; GGSW(1): deterministic bound
+ *   key switch  phase kept within N 2^(s_ks-1) (+ noise term)
+ *   blind rot.  trivial input gives (0, X^-b~ v) exactly; the paper's
+ *               N = 4 example (LUT 6,7,3,5; m = 2 -> 3)
+ *   PBS         decrypt(PBS(Enc m)) = T[m] for every m (3-bit and 4-bit
+ *               spaces); tier 1 = tier 2 bit for bit
+ * The exact noise bits of a bootstrapped ciphertext are fixed by the
+ * conventions above (loop order, CMux form, rounding rules) and are checked
+ * only through these component pins and tier agreement.
+ */
+#include <math.h>
+#include <omp.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef uint64_t u64;
+typedef int64_t i64;
+typedef unsigned __int128 u128;
+typedef __int128 i128;
+
+#define OR_P 0xFFFFFFFF00000001ULL
+
+enum { OR_SCHOOLBOOK = 0, OR_NTT = 1 };
+
+/* Parameter set; the field order mirrors the library's, but this is an
+ * independent declaration. */
+typedef struct {
+  uint32_t n;            /* LWE dimension */
+  uint32_t k;            /* GLWE dimension (only k = 1 is used) */
+  uint32_t N;            /* ring degree, power of two */
+  uint32_t pbs_level;    /* l: gadget levels of the bootstrapping key */
+  uint32_t pbs_base_log; /* beta: log2 of the gadget base */
+  uint32_t ks_level;     /* l_ks */
+  uint32_t ks_base_log;  /* beta_ks */
+  uint32_t msg_bits;     /* message space M = 2^msg_bits (plus one padding bit) */
+} or_params;
+
+/* ------------------------------------------------------------------------- */
+/* Field Z_p                                                                 */
+/* ------------------------------------------------------------------------- */
+
+u64 or_add(u64 a, u64 b) { return (u64)(((u128)a + b) % OR_P); }
+u64 or_sub(u64 a, u64 b) { return (u64)(((u128)a + OR_P - b) % OR_P); }
+u64 or_neg(u64 a) { return (u64)(((u128)OR_P - a) % OR_P); }
+u64 or_mul(u64 a, u64 b) { return (u64)(((u128)a * b) % OR_P); }
+
+u64 or_pow(u64 a, u64 e) {
+  u64 r = 1, b = a % OR_P;
+  while (e) {
+    if (e & 1) r = or_mul(r, b);
+    b = or_mul(b, b);
+    e >>= 1;
+  }
+  return r;
+}
+
+u64 or_inv(u64 a) { return or_pow(a, OR_P - 2); } /* Fermat */
+
+/* A signed integer of small magnitude, as an element of Z_p. */
+static u64 or_from_i64(i64 x) {
+  i128 r = (i128)x % (i128)OR_P;
+  if (r < 0) r += OR_P;
+  return (u64)r;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Negacyclic ring Z_p[X]/(X^N + 1)                                          */
+/* ------------------------------------------------------------------------- */
+
+/* Tier 1: c = a * b mod (X^N + 1), by the definition X^N = -1. */
+void or_polymul_schoolbook(const u64 *a, const u64 *b, u64 *c, int N) {
+  u64 *acc = (u64 *)calloc((size_t)N, sizeof(u64));
+  for (int i = 0; i < N; ++i) {
+    if (a[i] == 0) continue;
+    for (int j = 0; j < N; ++j) {
+      u64 prod = or_mul(a[i], b[j]);
+      int e = i + j;
+      if (e < N)
+        acc[e] = or_add(acc[e], prod);
+      else
+        acc[e - N] = or_sub(acc[e - N], prod);
+    }
+  }
+  memcpy(c, acc, (size_t)N * sizeof(u64));
+  free(acc);
+}
+
+/* The canonical primitive 2N-th root of unity psi = 7^((p-1)/(2N)).
+ * 7 generates the multiplicative group of Z_p, so psi has order exactly 2N
+ * and psi^N = -1. */
+u64 or_root_2n(int N) { return or_pow(7, (OR_P - 1) / (u64)(2 * N)); }
+
+static int or_log2(int N) {
+  int L = 0;
+  while ((1 << L) < N) ++L;
+  return L;
+}
+
+static void or_bit_reverse(u64 *a, int N) {
+  int L = or_log2(N);
+  for (int i = 0; i < N; ++i) {
+    int r = 0;
+    for (int b = 0; b < L; ++b)
+      if (i & (1 << b)) r |= 1 << (L - 1 - b);
+    if (i < r) {
+      u64 t = a[i];
+      a[i] = a[r];
+      a[r] = t;
+    }
+  }
+}
+
+/* Cyclic DFT of length N with root w (iterative radix-2, bit-reversed input
+ * permutation, natural output): A_k = sum_j a_j w^(jk). */
+static void or_dft_cyclic(u64 *a, int N, u64 w) {
+  or_bit_reverse(a, N);
+  for (int len = 2; len <= N; len <<= 1) {
+    u64 wl = or_pow(w, (u64)(N / len));
+    for (int i = 0; i < N; i += len) {
+      u64 t = 1;
+      for (int j = 0; j < len / 2; ++j) {
+        u64 u = a[i + j];
+        u64 v = or_mul(a[i + j + len / 2], t);
+        a[i + j] = or_add(u, v);
+        a[i + j + len / 2] = or_sub(u, v);
+        t = or_mul(t, wl);
+      }
+    }
+  }
+}
+
+/* Tier 2 forward transform, natural order:
+ *   A_k = a(psi^(2k+1)) = sum_j a_j psi^(j(2k+1)),  k = 0..N-1,
+ * computed as a twist by psi^j followed by a cyclic DFT with root psi^2. */
+void or_ntt_forward(u64 *a, int N) {
+  u64 psi = or_root_2n(N), t = 1;
+  for (int j = 0; j < N; ++j) {
+    a[j] = or_mul(a[j], t);
+    t = or_mul(t, psi);
+  }
+  or_dft_cyclic(a, N, or_mul(psi, psi));
+}
+
+/* Inverse of or_ntt_forward. */
+void or_ntt_inverse(u64 *a, int N) {
+  u64 psi = or_root_2n(N);
+  u64 psi_inv = or_inv(psi);
+  or_dft_cyclic(a, N, or_mul(psi_inv, psi_inv));
+  u64 ninv = or_inv((u64)N), t = ninv;
+  for (int j = 0; j < N; ++j) {
+    a[j] = or_mul(a[j], t);
+    t = or_mul(t, psi_inv);
+  }
+}
+
+/* Tier 2 negacyclic product through the transform. */
+void or_polymul_ntt(const u64 *a, const u64 *b, u64 *c, int N) {
+  u64 *fa = (u64 *)malloc((size_t)N * sizeof(u64));
+  u64 *fb = (u64 *)malloc((size_t)N * sizeof(u64));
+  memcpy(fa, a, (size_t)N * sizeof(u64));
+  memcpy(fb, b, (size_t)N * sizeof(u64));
+  or_ntt_forward(fa, N);
+  or_ntt_forward(fb, N);
+  for (int i = 0; i < N; ++i) fa[i] = or_mul(fa[i], fb[i]);
+  or_ntt_inverse(fa, N);
+  memcpy(c, fa, (size_t)N * sizeof(u64));
+  free(fa);
+  free(fb);
+}
+
+static void or_polymul(const u64 *a, const u64 *b, u64 *c, int N, int kind) {
+  if (kind == OR_SCHOOLBOOK)
+    or_polymul_schoolbook(a, b, c, N);
+  else
+    or_polymul_ntt(a, b, c, N);
+}
+
+/* c = X^r * a in the negacyclic ring, 0 <= r < 2N (X^N = -1). */
+void or_poly_monomial_mul(const u64 *a, int r, u64 *c, int N) {
+  for (int j = 0; j < N; ++j) c[j] = 0;
+  for (int j = 0; j < N; ++j) {
+    int e = j + r; /* exponent in [0, 3N) */
+    int sign = 0;
+    while (e >= N) {
+      e -= N;
+      sign ^= 1;
+    }
+    c[e] = sign ? or_neg(a[j]) : a[j];
+  }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Modulus switch and gadget decomposition                                   */
+/* ------------------------------------------------------------------------- */
+
+/* Rounding from Z_p to Z_2N (the paper's "ModSwitch"):
+ *   round(2N a / p) = floor((2N a + (p-1)/2) / p)  mod 2N.
+ * p is odd, so 2N a / p is never exactly half-way between two integers. */
+uint32_t or_modswitch(u64 a, int N) {
+  u128 num = (u128)(2 * (u64)N) * a + (OR_P - 1) / 2;
+  return (uint32_t)((num / OR_P) % (u128)(2 * N));
+}
+
+/* Floor division of a signed 128-bit integer by a positive one. */
+static i128 or_floor_div(i128 a, i128 b) {
+  i128 q = a / b;
+  if ((a % b != 0) && (a < 0)) q -= 1;
+  return q;
+}
+
+/* Signed gadget decomposition of a in Z_p with `levels` digits of base
+ * B = 2^beta.  Convention:
+ *   a_c = a if a <= (p-1)/2, else a - p         (centred representative)
+ *   s   = 64 - levels*beta                      (discarded low bits)
+ *   r   = floor((a_c + 2^(s-1)) / 2^s)          (round half up)
+ *   for t = levels-1 down to 1:
+ *       d_t = ((r + B/2) mod B) - B/2  in [-B/2, B/2);  r = (r - d_t) / B
+ *   d_0 = r                                     (top digit, in [-B/2, B/2])
+ * so that sum_t d_t * 2^(64 - (t+1) beta) = r * 2^s and
+ * a_c - r 2^s lies in [-2^(s-1), 2^(s-1)).  Digit t pairs with gadget
+ * factor g_t = 2^(64 - (t+1) beta), t = 0 being the most significant. */
+void or_decompose(u64 a, int levels, int beta, i64 *digits) {
+  i128 ac = (a <= (OR_P - 1) / 2) ? (i128)a : (i128)a - (i128)OR_P;
+  int s = 64 - levels * beta;
+  i128 r = or_floor_div(ac + ((i128)1 << (s - 1)), (i128)1 << s);
+  i128 B = (i128)1 << beta;
+  for (int t = levels - 1; t >= 1; --t) {
+    i128 m = (r + B / 2) % B;
+    if (m < 0) m += B;
+    i128 d = m - B / 2;
+    digits[t] = (i64)d;
+    r = (r - d) / B;
+  }
+  digits[0] = (i64)r;
+}
+
+/* Gadget factor g_t = 2^(64 - (t+1) beta) as an element of Z_p. */
+static u64 or_gadget(int t, int beta) {
+  int e = 64 - (t + 1) * beta;
+  return or_pow(2, (u64)e);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Seeded randomness for key generation and encryption (test data only)      */
+/* ------------------------------------------------------------------------- */
+
+/* SplitMix64 (Steele, Lea and Flood, OOPSLA 2014) used as a counter-based
+ * generator: word(key, i) is output number i (0-based) of the SplitMix64
+ * sequence whose state starts at `key`, i.e. the mixing function applied to
+ * key + (i+1) * 0x9E3779B97F4A7C15. */
+u64 or_splitmix_word(u64 key, u64 idx) {
+  u64 z = key + (idx + 1) * 0x9E3779B97F4A7C15ULL;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+/* Independent sub-stream key for artefact `stream` under master `seed`. */
+static u64 or_stream_key(u64 seed, u64 stream) { return or_splitmix_word(seed, stream); }
+
+enum {
+  OR_STREAM_LWE_KEY = 1,
+  OR_STREAM_GLWE_KEY = 2,
+  OR_STREAM_BSK_MASK = 3,
+  OR_STREAM_BSK_NOISE = 4,
+  OR_STREAM_KSK_MASK = 5,
+  OR_STREAM_KSK_NOISE = 6,
+  OR_STREAM_ENC_MASK = 7,
+  OR_STREAM_ENC_NOISE = 8
+};
+
+/* Uniform element of Z_p from one word (the bias of 2^-32 is irrelevant for
+ * test data). */
+static u64 or_uniform(u64 key, u64 idx) {
+  u64 w = or_splitmix_word(key, idx);
+  return w >= OR_P ? w - OR_P : w;
+}
+
+/* Standard normal sample number idx by the Box-Muller transform on words
+ * 2 idx and 2 idx + 1:  U1 in (0,1], U2 in [0,1),
+ *   Z = sqrt(-2 ln U1) cos(2 pi U2). */
+double or_gauss(u64 key, u64 idx) {
+  u64 w1 = or_splitmix_word(key, 2 * idx);
+  u64 w2 = or_splitmix_word(key, 2 * idx + 1);
+  double u1 = (double)((w1 >> 11) + 1) * 0x1.0p-53;
+  double u2 = (double)(w2 >> 11) * 0x1.0p-53;
+  return sqrt(-2.0 * log(u1)) * cos(6.283185307179586 * u2);
+}
+
+/* Rounded Gaussian noise with standard deviation sigma * 2^64 (sigma given as
+ * a fraction of the modulus; p rounds to 2^64 in double), as an element of
+ * Z_p. */
+static u64 or_noise(u64 key, u64 idx, double sigma) {
+  double sd = ldexp(sigma, 64);
+  double x = floor(sd * or_gauss(key, idx) + 0.5);
+  return or_from_i64((i64)x);
+}
+
+/* Binary secret bit number idx. */
+static u64 or_key_bit(u64 key, u64 idx) { return or_splitmix_word(key, idx) >> 63; }
+
+/* ------------------------------------------------------------------------- */
+/* LWE and GLWE                                                              */
+/* ------------------------------------------------------------------------- */
+
+/* Scaling factor Delta = floor(p / 2M) for messages in Z_M with one padding
+ * bit. */
+static u64 or_delta(const or_params *P) { return OR_P / (2ULL << P->msg_bits); }
+
+/* LWE phase: b - <a, s>, ciphertext laid out as (a_0 .. a_{dim-1}, b). */
+static u64 or_lwe_phase1(const u64 *key, int dim, const u64 *ct) {
+  u64 acc = ct[dim];
+  for (int i = 0; i < dim; ++i) acc = or_sub(acc, or_mul(ct[i], key[i]));
+  return acc;
+}
+
+void or_lwe_phase(const u64 *key, int dim, const u64 *ct, size_t count, u64 *phase) {
+  for (size_t q = 0; q < count; ++q) phase[q] = or_lwe_phase1(key, dim, ct + q * (size_t)(dim + 1));
+}
+
+/* Decryption to Z_2M: m = round(2M phase / p) mod 2M. */
+void or_lwe_decrypt(const or_params *P, const u64 *key, int dim, const u64 *ct, size_t count,
+                    uint32_t *msgs) {
+  u64 twoM = 2ULL << P->msg_bits;
+  for (size_t q = 0; q < count; ++q) {
+    u64 ph = or_lwe_phase1(key, dim, ct + q * (size_t)(dim + 1));
+    u128 num = (u128)twoM * ph + (OR_P - 1) / 2;
+    msgs[q] = (uint32_t)((num / OR_P) % twoM);
+  }
+}
+
+/* Encryption of a plaintext already scaled into Z_p:
+ *   a_i uniform, e Gaussian(sigma), b = <a, s> + plain + e. */
+void or_lwe_encrypt_plain(u64 seed, double sigma, const u64 *key, int dim, const u64 *plain,
+                          size_t count, u64 *out) {
+  u64 km = or_stream_key(seed, OR_STREAM_ENC_MASK);
+  u64 kn = or_stream_key(seed, OR_STREAM_ENC_NOISE);
+  for (size_t q = 0; q < count; ++q) {
+    u64 *ct = out + q * (size_t)(dim + 1);
+    u64 b = 0;
+    for (int i = 0; i < dim; ++i) {
+      ct[i] = or_uniform(km, (u64)q * (u64)dim + (u64)i);
+      b = or_add(b, or_mul(ct[i], key[i]));
+    }
+    b = or_add(b, plain[q]);
+    b = or_add(b, or_noise(kn, (u64)q, sigma));
+    ct[dim] = b;
+  }
+}
+
+/* Encryption of messages m in Z_2M with scale Delta. */
+void or_lwe_encrypt(u64 seed, const or_params *P, double sigma, const u64 *key, int dim,
+                    const uint32_t *msgs, size_t count, u64 *out) {
+  u64 delta = or_delta(P);
+  u64 *plain = (u64 *)malloc(count * sizeof(u64) + 8);
+  for (size_t q = 0; q < count; ++q) plain[q] = or_mul(delta, (u64)msgs[q]);
+  or_lwe_encrypt_plain(seed, sigma, key, dim, plain, count, out);
+  free(plain);
+}
+
+/* GLWE phase (k = 1): B - A * S, ciphertext laid out as (A[0..N), B[0..N)). */
+void or_glwe_phase(int N, const u64 *S, const u64 *ct, u64 *phase, int kind) {
+  u64 *as = (u64 *)malloc((size_t)N * sizeof(u64));
+  or_polymul(ct, S, as, N, kind);
+  for (int j = 0; j < N; ++j) phase[j] = or_sub(ct[N + j], as[j]);
+  free(as);
+}
+
+/* Test polynomial for a table T[0..M) with entries in Z_2M.  With box = N/M
+ * and h = floor(box/2) (half a box of tolerance on either side):
+ *   v_j = Delta T[floor((j + h) / box)]   for j <  N - h,
+ *   v_j = -Delta T[0]                     for j >= N - h,
+ * the tail being the negacyclic image of the first half-box of entry 0. */
+void or_test_poly(const or_params *P, const uint32_t *table, u64 *v) {
+  int N = (int)P->N, M = 1 << P->msg_bits;
+  int box = N / M, h = box / 2;
+  u64 delta = or_delta(P);
+  for (int j = 0; j < N; ++j) {
+    if (j < N - h)
+      v[j] = or_mul(delta, table[(j + h) / box]);
+    else
+      v[j] = or_neg(or_mul(delta, table[0]));
+  }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Key generation                                                            */
+/* ------------------------------------------------------------------------- */
+
+/* Sizes in 64-bit words. */
+size_t or_bsk_words(const or_params *P) {
+  return (size_t)P->n * 2 * P->pbs_level * 2 * P->N;
+}
+size_t or_ksk_words(const or_params *P) {
+  return (size_t)P->N * P->ks_level * (P->n + 1);
+}
+
+/* Keys (binary, uniform from the seed), bootstrapping key and key-switching
+ * key.  Layouts:
+ *   lwe_key  [n], glwe_key [N]
+ *   bsk [i][u][t][c][x]: GGSW encryption of s_i under S.  Row (u, t) is a
+ *       GLWE encryption of zero, (A, A*S + E), with s_i * g_t added to the
+ *       constant coefficient of component u (u = 0: mask A, u = 1: body B).
+ *   ksk [j][t][0..n]: LWE encryption under s of S_j * g^ks_t, with
+ *       g^ks_t = 2^(64 - (t+1) beta_ks).
+ * Randomness: SplitMix64 sub-streams of `seed` (see or_splitmix_word):
+ *   lwe key bit i          : stream 1, word i, top bit
+ *   glwe key bit x         : stream 2, word x, top bit
+ *   bsk mask, row r, coef x: stream 3, word r N + x   (r = (2 i + u) l + t)
+ *   bsk noise              : stream 4, Gaussian number r N + x, sigma_glwe
+ *   ksk mask, row r, col c : stream 5, word r n + c   (r = j l_ks + t)
+ *   ksk noise              : stream 6, Gaussian number r, sigma_lwe */
+void or_keygen(u64 seed, const or_params *P, double sigma_lwe, double sigma_glwe, u64 *lwe_key,
+               u64 *glwe_key, u64 *bsk, u64 *ksk) {
+  int n = (int)P->n, N = (int)P->N, l = (int)P->pbs_level, lk = (int)P->ks_level;
+  u64 k1 = or_stream_key(seed, OR_STREAM_LWE_KEY), k2 = or_stream_key(seed, OR_STREAM_GLWE_KEY);
+  for (int i = 0; i < n; ++i) lwe_key[i] = or_key_bit(k1, (u64)i);
+  for (int x = 0; x < N; ++x) glwe_key[x] = or_key_bit(k2, (u64)x);
+
+  u64 kbm = or_stream_key(seed, OR_STREAM_BSK_MASK), kbn = or_stream_key(seed, OR_STREAM_BSK_NOISE);
+  int nrows = n * 2 * l;
+#pragma omp parallel
+  {
+    u64 *as = (u64 *)malloc((size_t)N * sizeof(u64));
+#pragma omp for schedule(static)
+    for (int r = 0; r < nrows; ++r) {
+      int i = r / (2 * l), u = (r / l) % 2, t = r % l;
+      u64 *A = bsk + (size_t)r * 2 * N, *B = A + N;
+      for (int x = 0; x < N; ++x) A[x] = or_uniform(kbm, (u64)r * (u64)N + (u64)x);
+      or_polymul_ntt(A, glwe_key, as, N);
+      for (int x = 0; x < N; ++x)
+        B[x] = or_add(as[x], or_noise(kbn, (u64)r * (u64)N + (u64)x, sigma_glwe));
+      if (lwe_key[i]) {
+        u64 g = or_gadget(t, (int)P->pbs_base_log);
+        if (u == 0)
+          A[0] = or_add(A[0], g);
+        else
+          B[0] = or_add(B[0], g);
+      }
+    }
+    free(as);
+  }
+
+  u64 kkm = or_stream_key(seed, OR_STREAM_KSK_MASK), kkn = or_stream_key(seed, OR_STREAM_KSK_NOISE);
+  int krows = N * lk;
+#pragma omp parallel for schedule(static)
+  for (int r = 0; r < krows; ++r) {
+    int j = r / lk, t = r % lk;
+    u64 *row = ksk + (size_t)r * (size_t)(n + 1);
+    u64 b = 0;
+    for (int c = 0; c < n; ++c) {
+      row[c] = or_uniform(kkm, (u64)r * (u64)n + (u64)c);
+      b = or_add(b, or_mul(row[c], lwe_key[c]));
+    }
+    if (glwe_key[j]) b = or_add(b, or_gadget(t, (int)P->ks_base_log));
+    b = or_add(b, or_noise(kkn, (u64)r, sigma_lwe));
+    row[n] = b;
+  }
+}
+
+/* ------------------------------------------------------------------------- */
+/* External product, blind rotation, extraction, key switching               */
+/* ------------------------------------------------------------------------- */
+
+/* External product GGSW (x) GLWE: for a GLWE ciphertext D = (D_A, D_B) and a
+ * GGSW ciphertext G laid out [u][t][c][x],
+ *   out_c = sum_{u, t} Dec_t(D_u) * G[u][t][c],
+ * Dec being or_decompose applied coefficient-wise and digits taken mod p. */
+void or_external_product(const or_params *P, const u64 *ggsw, const u64 *glwe_in, u64 *glwe_out,
+                         int kind) {
+  int N = (int)P->N, l = (int)P->pbs_level, beta = (int)P->pbs_base_log;
+  u64 *digit = (u64 *)malloc((size_t)l * N * sizeof(u64));
+  u64 *prod = (u64 *)malloc((size_t)N * sizeof(u64));
+  i64 *dg = (i64 *)malloc((size_t)l * sizeof(i64));
+  u64 *out = (u64 *)calloc((size_t)2 * N, sizeof(u64));
+  for (int u = 0; u < 2; ++u) {
+    const u64 *Du = glwe_in + (size_t)u * N;
+    for (int x = 0; x < N; ++x) {
+      or_decompose(Du[x], l, beta, dg);
+      for (int t = 0; t < l; ++t) digit[(size_t)t * N + x] = or_from_i64(dg[t]);
+    }
+    for (int t = 0; t < l; ++t)
+      for (int c = 0; c < 2; ++c) {
+        const u64 *row = ggsw + (((size_t)u * l + t) * 2 + c) * N;
+        or_polymul(digit + (size_t)t * N, row, prod, N, kind);
+        for (int x = 0; x < N; ++x) out[(size_t)c * N + x] = or_add(out[(size_t)c * N + x], prod[x]);
+      }
+  }
+  memcpy(glwe_out, out, (size_t)2 * N * sizeof(u64));
+  free(digit);
+  free(prod);
+  free(dg);
+  free(out);
+}
+
+/* Forward transform (or_ntt_forward) of every row of a bootstrapping key;
+ * same layout as the key. */
+void or_bsk_transform(const or_params *P, const u64 *bsk, u64 *fbsk, int nthreads) {
+  size_t rows = or_bsk_words(P) / P->N;
+  int N = (int)P->N;
+  int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#pragma omp parallel for num_threads(nt) schedule(static)
+  for (long r = 0; r < (long)rows; ++r) {
+    memcpy(fbsk + (size_t)r * N, bsk + (size_t)r * N, (size_t)N * sizeof(u64));
+    or_ntt_forward(fbsk + (size_t)r * N, N);
+  }
+}
+
+/* Blind rotation of the test polynomial v by the LWE ciphertext
+ * (a_0..a_{n-1}, b):
+ *   a~_i = modswitch(a_i), b~ = modswitch(b)
+ *   ACC  = (0, X^(-b~) v)
+ *   for i = 0 .. n-1 (ascending):
+ *       ACC = ACC + GGSW_i (x) (X^(a~_i) ACC - ACC)     (CMux form)
+ * so that the phase of ACC ends as X^(-(b~ - sum a~_i s_i)) v, up to noise.
+ * With kind == OR_NTT the external product is evaluated in the transform
+ * domain (each product of a digit polynomial with a key row becomes a
+ * pointwise product; linearity lets the sums over (u, t) be taken there).
+ * `fbsk`, if not NULL, holds the forward transform of every key row
+ * (or_bsk_transform); otherwise rows are transformed when used. */
+void or_blind_rotate(const or_params *P, const u64 *lwe, const u64 *bsk, const u64 *fbsk,
+                     const u64 *v, u64 *acc, int kind) {
+  int n = (int)P->n, N = (int)P->N, l = (int)P->pbs_level, beta = (int)P->pbs_base_log;
+  size_t ggsw_words = (size_t)2 * l * 2 * N;
+  u64 *rot = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+  u64 *diff = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+  u64 *prod = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+
+  uint32_t bt = or_modswitch(lwe[n], N);
+  for (int j = 0; j < N; ++j) acc[j] = 0;
+  or_poly_monomial_mul(v, (int)((2 * (uint32_t)N - bt) % (2 * (uint32_t)N)), acc + N, N);
+
+  u64 *fd = NULL, *fk = NULL, *fy = NULL;
+  i64 *dg = NULL;
+  if (kind == OR_NTT) {
+    fd = (u64 *)malloc((size_t)N * sizeof(u64));
+    fk = (u64 *)malloc((size_t)N * sizeof(u64));
+    fy = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+    dg = (i64 *)malloc((size_t)l * sizeof(i64));
+  }
+
+  for (int i = 0; i < n; ++i) {
+    uint32_t ai = or_modswitch(lwe[i], N);
+    for (int u = 0; u < 2; ++u) {
+      or_poly_monomial_mul(acc + (size_t)u * N, (int)ai, rot + (size_t)u * N, N);
+      for (int j = 0; j < N; ++j)
+        diff[(size_t)u * N + j] = or_sub(rot[(size_t)u * N + j], acc[(size_t)u * N + j]);
+    }
+    const u64 *G = bsk + (size_t)i * ggsw_words;
+    if (kind == OR_SCHOOLBOOK) {
+      or_external_product(P, G, diff, prod, OR_SCHOOLBOOK);
+    } else {
+      for (int j = 0; j < 2 * N; ++j) fy[j] = 0;
+      for (int u = 0; u < 2; ++u)
+        for (int t = 0; t < l; ++t) {
+          for (int x = 0; x < N; ++x) {
+            or_decompose(diff[(size_t)u * N + x], l, beta, dg);
+            fd[x] = or_from_i64(dg[t]);
+          }
+          or_ntt_forward(fd, N);
+          for (int c = 0; c < 2; ++c) {
+            size_t off = (((size_t)u * l + t) * 2 + c) * N;
+            if (fbsk) {
+              memcpy(fk, fbsk + (size_t)i * ggsw_words + off, (size_t)N * sizeof(u64));
+            } else {
+              memcpy(fk, G + off, (size_t)N * sizeof(u64));
+              or_ntt_forward(fk, N);
+            }
+            for (int x = 0; x < N; ++x)
+              fy[(size_t)c * N + x] = or_add(fy[(size_t)c * N + x], or_mul(fd[x], fk[x]));
+          }
+        }
+      for (int c = 0; c < 2; ++c) {
+        memcpy(prod + (size_t)c * N, fy + (size_t)c * N, (size_t)N * sizeof(u64));
+        or_ntt_inverse(prod + (size_t)c * N, N);
+      }
+    }
+    for (int j = 0; j < 2 * N; ++j) acc[j] = or_add(acc[j], prod[j]);
+  }
+  free(rot);
+  free(diff);
+  free(prod);
+  free(fd);
+  free(fk);
+  free(fy);
+  free(dg);
+}
+
+/* Sample extraction of the constant coefficient (Sec. 2.2.3, LWE Extract):
+ * with phase B - A*S, the constant coefficient of the phase equals
+ * b' - <a', S> for a'_0 = A_0, a'_j = -A_{N-j} (j >= 1), b' = B_0.
+ * Output layout (a'_0 .. a'_{N-1}, b'). */
+void or_sample_extract(int N, const u64 *acc, u64 *big) {
+  big[0] = acc[0];
+  for (int j = 1; j < N; ++j) big[j] = or_neg(acc[N - j]);
+  big[N] = acc[N];
+}
+
+/* Key switching from the extracted key S (dimension N) to s (dimension n):
+ *   out = (0, .., 0, b') - sum_{j < N} sum_{t < l_ks} d_{j,t} KSK[j][t],
+ * with d_{j,.} = Dec(a'_j; l_ks, beta_ks) taken mod p. */
+void or_keyswitch(const or_params *P, const u64 *big, const u64 *ksk, u64 *out) {
+  int n = (int)P->n, N = (int)P->N, lk = (int)P->ks_level, bk = (int)P->ks_base_log;
+  i64 *dg = (i64 *)malloc((size_t)lk * sizeof(i64));
+  for (int c = 0; c < n; ++c) out[c] = 0;
+  out[n] = big[N];
+  for (int j = 0; j < N; ++j) {
+    or_decompose(big[j], lk, bk, dg);
+    for (int t = 0; t < lk; ++t) {
+      u64 d = or_from_i64(dg[t]);
+      if (d == 0) continue;
+      const u64 *row = ksk + ((size_t)j * lk + t) * (size_t)(n + 1);
+      for (int c = 0; c <= n; ++c) out[c] = or_sub(out[c], or_mul(d, row[c]));
+    }
+  }
+  free(dg);
+}
+
+/* Full PBS of `count` ciphertexts: blind rotation, sample extraction, key
+ * switching.  Optional outputs: the GLWE accumulators [count][2N] and the
+ * extracted ciphertexts [count][N+1].  Ciphertexts are independent; they are
+ * spread over `nthreads` OpenMP threads (<= 0: the runtime default). */
+void or_pbs(const or_params *P, const u64 *lwe_in, const u64 *bsk, const u64 *ksk, const u64 *v,
+            u64 *lwe_out, u64 *big_out, u64 *acc_out, size_t count, int kind, int nthreads) {
+  int n = (int)P->n, N = (int)P->N;
+  int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+  u64 *fbsk = NULL;
+  if (kind == OR_NTT) {
+    fbsk = (u64 *)malloc(or_bsk_words(P) * sizeof(u64));
+    or_bsk_transform(P, bsk, fbsk, nt);
+  }
+#pragma omp parallel num_threads(nt)
+  {
+    u64 *acc = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+    u64 *big = (u64 *)malloc((size_t)(N + 1) * sizeof(u64));
+#pragma omp for schedule(dynamic, 1)
+    for (long q = 0; q < (long)count; ++q) {
+      or_blind_rotate(P, lwe_in + (size_t)q * (n + 1), bsk, fbsk, v, acc, kind);
+      or_sample_extract(N, acc, big);
+      if (acc_out) memcpy(acc_out + (size_t)q * 2 * N, acc, (size_t)2 * N * sizeof(u64));
+      if (big_out) memcpy(big_out + (size_t)q * (N + 1), big, (size_t)(N + 1) * sizeof(u64));
+      if (lwe_out) or_keyswitch(P, big, ksk, lwe_out + (size_t)q * (n + 1));
+    }
+    free(acc);
+    free(big);
+  }
+  free(fbsk);
+}
