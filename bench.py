@@ -1,0 +1,171 @@
+#!/usr/bin/env python3
+"""Throughput of batched TFHE programmable bootstrapping on one MI355X.
+
+One step = one PBS of the whole batch (modulus switch, blind rotation,
+sample extraction, key switching) with inputs and prepared keys resident in
+device memory.  Default workload: the LLaMA-3-8B FFN SiLU layer of one
+decoded token, n = 1024, N = 2048, l = 3 x 8 bits, batch 14336.
+
+Prints one JSON line.  The timed region is bracketed by device
+synchronisations; per-kernel durations come from HIP events recorded on the
+stream the kernels are launched on.  A step calls the two entry points that
+make up rosetta_pbs_batch (blind rotation + extraction into a workspace,
+then key switching) so that the blind-rotation kernel can be timed on its
+own for the roofline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X published / derived peaks ("Roofline")
+HBM_PEAK_GBS = 8000.0
+CU, CLOCK_HZ, LANES = 256, 2.4e9, 64
+# VALU issue slots (one wave64 instruction at full rate = 1 slot per lane
+# group) of one Goldilocks modular multiplication in the library's sequence:
+# 4 v_mad_u64_u32 at half rate (2 slots each) + 14 full-rate ops.
+MODMUL_SLOTS = 4 * 2 + 14
+MODMUL_PEAK_T = CU * CLOCK_HZ * LANES / MODMUL_SLOTS / 1e12   # Tmodmul/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, keys, cts, v, seconds_target: float):
+    """The oracle (tier 2, OpenMP over ciphertexts) on a bounded sample."""
+    from oracle import oracle as O
+    op = O.Params.make(**{k: x for k, x in w.params().items() if k != "k"})
+    cores = min(os.cpu_count() or 1, int(os.environ.get("OMP_NUM_THREADS", "16") or 16))
+    # calibrate on one ciphertext, then size the sample to ~seconds_target
+    t0 = time.perf_counter()
+    O.pbs(op, cts[:1], keys["bsk"], keys["ksk"], v, O.NTT, 1)
+    one = time.perf_counter() - t0
+    sample = max(cores, int(seconds_target * cores / max(one, 1e-3)) // cores * cores)
+    sample = min(sample, cts.shape[0])
+    t0 = time.perf_counter()
+    O.pbs(op, cts[:sample], keys["bsk"], keys["ksk"], v, O.NTT, cores)
+    dt = time.perf_counter() - t0
+    return {"value": sample / dt, "unit": "PBS/s", "cores": cores, "kind": "oracle",
+            "sample": f"{sample} of the {w.batch} ciphertexts of {w.name} (first {sample}), "
+                      f"tier-2 transform oracle, {cores} OpenMP threads, {dt:.1f} s wall; "
+                      f"includes its once-per-call key transform"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline sample (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); batched PBS shards "
+              "by ciphertext with no exchange, so a multi-GPU figure is not produced here",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_16915_amd import rosetta as R
+    from paper_2609_16915_amd import workloads as W
+
+    name = args.workload or W.HEADLINE
+    w = W.get(name)
+    p = R.Params.from_dict(w.params())
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+
+    log(f"[bench] {name}: keygen (library host helper)")
+    keys = R.keygen(w.key_seed, p, w.sigma_lwe, w.sigma_glwe)
+    msgs = w.messages()
+    cts = R.lwe_encrypt(w.enc_seed, p, w.sigma_lwe, keys["lwe_key"], msgs)
+    table = w.table()
+    v = R.lut_build(p, table)
+
+    bsk = R.bsk_prepare(R.to_device(keys["bsk"]), p)
+    ksk = R.ksk_prepare(R.to_device(keys["ksk"]), p)
+    d_in, d_v = R.to_device(cts), R.to_device(v)
+    d_out = R.empty((w.batch, w.n + 1))
+    ws = R.empty(R.pbs_workspace_bytes(p, w.batch) // 8)
+    big = ws.view(w.batch, w.N + 1)
+    torch.cuda.synchronize()
+
+    def step():
+        R.blind_rotate_extract(d_in, bsk, d_v, p, out=big)
+        R.keyswitch(big, ksk, p, out=d_out)
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e0, e1, e2 in ev:
+        e0.record(stream)
+        R.blind_rotate_extract(d_in, bsk, d_v, p, out=big)
+        e1.record(stream)
+        R.keyswitch(big, ksk, p, out=d_out)
+        e2.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    br_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
+    ks_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
+    ms_per_step = wall * 1e3 / args.steps
+    value = w.batch / (wall / args.steps)
+
+    # the same step through the single entry point gives the same bits
+    ref = R.pbs_batch(d_in, bsk, ksk, d_v, p)
+    torch.cuda.synchronize()
+    out = R.to_host(d_out)
+    same = bool(np.array_equal(out, R.to_host(ref)))
+    ok_rate = float(np.mean(R.lwe_decrypt(p, keys["lwe_key"], out) == table[msgs]))
+
+    modmul_per_launch = w.br_modmul_per_pbs() * w.batch
+    achieved_t = modmul_per_launch / (br_ms * 1e-3) / 1e12
+    roofline = {"bound": "alu", "kernel": "k_blind_rotate", "achieved": round(achieved_t, 4),
+                "peak": round(MODMUL_PEAK_T, 4), "unit": "Tmodmul/s",
+                "frac": round(achieved_t / MODMUL_PEAK_T, 4), "traffic": None,
+                "per_launch_modmul": modmul_per_launch, "launch_ms": round(br_ms, 3)}
+    hbm_bytes = (w.bsk_words() + w.ksk_words()) * 8 + w.batch * 2 * (w.n + 1) * 8 + w.N * 8
+
+    result = {
+        "metric": "PBS/s (bootstraps per second) at N=2048, batch 14336; roofline fraction "
+                  "of the blind-rotation kernel",
+        "value": round(value, 2), "unit": "PBS/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u64 mod p (Goldilocks)",
+        "data": "synthetic (seeded activations, random keys)",
+        "config": {"workload": name, "n": w.n, "N": w.N, "pbs_level": w.pbs_level,
+                   "pbs_base_log": w.pbs_base_log, "ks_level": w.ks_level,
+                   "ks_base_log": w.ks_base_log, "msg_bits": w.msg_bits, "batch": w.batch,
+                   "function": w.function},
+        "kernels_ms": {"blind_rotate_extract": round(br_ms, 3), "keyswitch": round(ks_ms, 3)},
+        "hbm_algorithmic_frac": round(hbm_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 6),
+        "checks": {"split_equals_pbs_batch": same, "decrypt_equals_table_rate": round(ok_rate, 5)},
+        "roofline": roofline,
+    }
+    if args.cpu_seconds > 0:
+        log("[bench] CPU oracle baseline")
+        result["cpu_baseline"] = cpu_baseline(w, keys, cts, v, args.cpu_seconds)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

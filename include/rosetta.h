@@ -1,0 +1,227 @@
+/*
+ * rosetta.h - batched TFHE programmable bootstrapping on AMD Instinct MI355X
+ * (gfx950), over the Goldilocks prime p = 2^64 - 2^32 + 1.
+ *
+ * The operation is the one the ROSETTA paper (arXiv 2609.16915) builds its
+ * nonlinear layers on, Sec. 2.2 "TFHE Scheme", PBS paragraph and
+ * Fig. rlwe_primitives(a): a lookup table f is written into the coefficients
+ * of a test polynomial v(X) in Z_p[X]/(X^N + 1); blind rotation turns an LWE
+ * encryption of m into a GLWE encryption of X^(-m) v(X), whose constant
+ * term f(m) is extracted (Sec. 2.2.3, LWE Extract) into a fresh LWE
+ * ciphertext.  A final key switch brings it back under the input key, so
+ * outputs can be bootstrapped again.
+ *
+ * CONVENTIONS (they decide every output bit; the paper leaves them open):
+ *  - Modulus q = Q = p for LWE and GLWE.  Values are canonical, in [0, p).
+ *  - LWE ciphertext of dimension d: (a_0, ..., a_{d-1}, b), phase b - <a, s>.
+ *  - GLWE ciphertext (k = 1): (A[0..N), B[0..N)), phase B - A*S.
+ *  - Messages m in Z_M, M = 2^msg_bits, with one padding bit: plaintext
+ *    Delta*m, Delta = floor(p / 2M).  Decryption rounds 2M*phase/p.
+ *  - Modulus switch: a~ = floor((2N a + (p-1)/2) / p) mod 2N.
+ *  - Blind rotation: ACC = (0, X^(-b~) v); for i = 0..n-1 ascending,
+ *    ACC += GGSW_i (x) (X^(a~_i) ACC - ACC)   (CMux form).
+ *  - Gadget decomposition of a in Z_p, l levels of base B = 2^beta: centred
+ *    representative a_c, r = floor((a_c + 2^(s-1)) / 2^s) with s = 64 - l beta,
+ *    balanced digits d_t in [-B/2, B/2) for t = l-1..1, top digit d_0 = the
+ *    remaining carry; digit t pairs with g_t = 2^(64 - (t+1) beta).
+ *  - Bootstrapping key (standard layout) [i < n][u < 2][t < l][c < 2][x < N]:
+ *    row (u, t) of GGSW_i is a GLWE encryption of 0 with s_i g_t added to the
+ *    constant coefficient of component u (0 = mask, 1 = body).
+ *  - Sample extraction: a'_0 = A_0, a'_j = -A_{N-j}, b' = B_0.
+ *  - Key switching: out = (0, .., 0, b') - sum_{j<N, t<l_ks} d_{j,t} KSK[j][t]
+ *    with d = Dec(a'_j; l_ks, beta_ks); key-switching key (standard layout)
+ *    [j < N][t < l_ks][0..n], row (j, t) an LWE encryption of S_j g^ks_t.
+ *  - Test polynomial for a table T[0..M) (entries in Z_2M), box = N/M,
+ *    h = floor(box/2): v_j = Delta T[floor((j+h)/box)] for j < N - h and
+ *    v_j = -Delta T[0] for j >= N - h.
+ *
+ * MEMORY AND STREAMS.  Device pointers are plain HIP device addresses; the
+ * caller owns every buffer.  `stream` is a hipStream_t passed as void*
+ * (NULL: the default stream).  Calls that take device pointers only enqueue
+ * work and return; results are ready once the stream is synchronised.  A
+ * device-side fault surfaces at that synchronisation, not in the status.
+ * Inputs not in [0, p) are a precondition violation: the output is then
+ * unspecified, but every memory access stays in bounds.
+ *
+ * ERRORS.  Every call returns a rosetta_status; nothing throws across the
+ * ABI.  Arguments are validated on the host before anything is enqueued; on
+ * error nothing is enqueued and rosetta_last_error() (thread-local) holds a
+ * message.  batch == 0 (count == 0) is a successful no-op once the
+ * parameters are valid; pointers are then not inspected.
+ *
+ * Supported parameters: k = 1; N in {256, 512, 1024, 2048, 4096};
+ * 1 <= n <= 2048; 1 <= l <= 4, beta <= 30, l*beta <= 62; 1 <= l_ks <= 8,
+ * beta_ks <= 30, l_ks*beta_ks <= 62, N * l_ks * 2^beta_ks < 2^32;
+ * 1 <= msg_bits <= 20, 2^msg_bits <= N.
+ */
+#ifndef ROSETTA_H
+#define ROSETTA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct rosetta_params {
+  uint32_t n;            /* LWE dimension */
+  uint32_t k;            /* GLWE dimension; must be 1 */
+  uint32_t N;            /* ring degree (power of two, 256..4096) */
+  uint32_t pbs_level;    /* l */
+  uint32_t pbs_base_log; /* beta */
+  uint32_t ks_level;     /* l_ks */
+  uint32_t ks_base_log;  /* beta_ks */
+  uint32_t msg_bits;     /* log2 M */
+} rosetta_params;
+
+typedef enum rosetta_status {
+  ROSETTA_OK = 0,
+  ROSETTA_ERR_NULL = 1,        /* a required pointer is NULL */
+  ROSETTA_ERR_PARAMS = 2,      /* inconsistent parameters */
+  ROSETTA_ERR_UNSUPPORTED = 3, /* valid but outside what the kernels support */
+  ROSETTA_ERR_ALIAS = 4,       /* partially overlapping input and output */
+  ROSETTA_ERR_NOMEM = 5,       /* device allocation failed */
+  ROSETTA_ERR_DEVICE = 6,      /* a HIP call failed */
+  ROSETTA_ERR_SIZE = 7         /* a caller-provided buffer is too small */
+} rosetta_status;
+
+/* Library version string. */
+const char *rosetta_version(void);
+
+/* Name of a status code. */
+const char *rosetta_status_string(int status);
+
+/* Message for the last error returned on the calling thread ("" if none). */
+const char *rosetta_last_error(void);
+
+/* Validate a parameter set (ROSETTA_OK, _PARAMS or _UNSUPPORTED). */
+rosetta_status rosetta_check_params(const rosetta_params *params);
+
+/* Sizes in 64-bit words.  The standard and the device (prepared) layouts of
+ * the bootstrapping key have the same size, n*2*l*2*N.  The prepared
+ * key-switching key holds the N*l_ks*(n+1) key words plus n+1 column sums. */
+size_t rosetta_bsk_words(const rosetta_params *params);
+size_t rosetta_ksk_words(const rosetta_params *params);
+size_t rosetta_ksk_device_words(const rosetta_params *params);
+
+/* a0: bootstrapping-key preparation (once per key, not part of a PBS).
+ * Transforms every GGSW row of `bsk_std_dev` (standard layout, device) into
+ * the library's transform-domain layout in `bsk_dev` (device, same size,
+ * must not overlap).  Rows are pre-scaled by N^-1 so that the inverse
+ * transforms in the blind-rotation loop need no scaling. */
+rosetta_status rosetta_bsk_prepare(const uint64_t *bsk_std_dev, uint64_t *bsk_dev,
+                                   const rosetta_params *params, void *stream);
+
+/* Key-switching-key preparation: copies the standard layout into `ksk_dev`
+ * (rosetta_ksk_device_words words, device, must not overlap) and appends the
+ * column sums used by the key-switch kernel. */
+rosetta_status rosetta_ksk_prepare(const uint64_t *ksk_std_dev, uint64_t *ksk_dev,
+                                   const rosetta_params *params, void *stream);
+
+/* THE HOT PATH: programmable bootstrapping of `batch` LWE ciphertexts.
+ *   lwe_in   [batch][n+1]  device, canonical
+ *   bsk_dev  prepared bootstrapping key (rosetta_bsk_prepare)
+ *   ksk_dev  prepared key-switching key (rosetta_ksk_prepare)
+ *   lut      [N]           device, the test polynomial (rosetta_lut_build)
+ *   lwe_out  [batch][n+1]  device; may be exactly lwe_in (in place) but must
+ *                          not partially overlap it (ROSETTA_ERR_ALIAS)
+ * Steps a1-a8: modulus switch and accumulator set-up, n CMux steps
+ * (rotate-subtract, decompose, forward transforms, transform-domain
+ * multiply-accumulate with GGSW_i, inverse transforms, accumulate), sample
+ * extraction, key switching.  Uses a library-owned device workspace of
+ * rosetta_pbs_workspace_bytes(params, batch) bytes, grown on demand and kept
+ * per device until rosetta_shutdown(); calls sharing that workspace on one
+ * device must therefore be serialised (one stream at a time), or use
+ * rosetta_pbs_batch_ws with distinct workspaces. */
+rosetta_status rosetta_pbs_batch(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                 const uint64_t *ksk_dev, const uint64_t *lut, uint64_t *lwe_out,
+                                 size_t batch, const rosetta_params *params, void *stream);
+
+/* Workspace size (bytes) for a PBS of `batch` ciphertexts. */
+size_t rosetta_pbs_workspace_bytes(const rosetta_params *params, size_t batch);
+
+/* rosetta_pbs_batch with a caller-provided device workspace of at least
+ * rosetta_pbs_workspace_bytes bytes (else ROSETTA_ERR_SIZE). */
+rosetta_status rosetta_pbs_batch_ws(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                    const uint64_t *ksk_dev, const uint64_t *lut,
+                                    uint64_t *lwe_out, size_t batch,
+                                    const rosetta_params *params, void *workspace,
+                                    size_t workspace_bytes, void *stream);
+
+/* Steps a1-a6 alone: blind rotation, returning the GLWE accumulators
+ * glwe_out [batch][2N] (device; must not overlap the inputs). */
+rosetta_status rosetta_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                    const uint64_t *lut, uint64_t *glwe_out, size_t batch,
+                                    const rosetta_params *params, void *stream);
+
+/* Steps a1-a7: blind rotation and sample extraction, returning LWE
+ * ciphertexts of dimension N under the GLWE key, big_out [batch][N+1]
+ * (device; must not overlap the inputs). */
+rosetta_status rosetta_blind_rotate_extract(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                            const uint64_t *lut, uint64_t *big_out,
+                                            size_t batch, const rosetta_params *params,
+                                            void *stream);
+
+/* Step a8: key switching of big_in [batch][N+1] to lwe_out [batch][n+1]
+ * (device; must not overlap). */
+rosetta_status rosetta_keyswitch(const uint64_t *big_in, const uint64_t *ksk_dev,
+                                 uint64_t *lwe_out, size_t batch, const rosetta_params *params,
+                                 void *stream);
+
+/* Negacyclic number-theoretic transform of `count` polynomials of degree N
+ * (device, [count][N], in and out may be the same buffer).  Forward output
+ * order: out[j] = a(psi^(2 rev(j) + 1)) with psi = 7^((p-1)/2N) and rev the
+ * log2(N)-bit reversal.  The inverse takes that order back to coefficients
+ * and includes the 1/N scaling. */
+rosetta_status rosetta_ntt_forward(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,
+                                   void *stream);
+rosetta_status rosetta_ntt_inverse(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,
+                                   void *stream);
+
+/* Negacyclic products c = a * b mod (X^N + 1) of `count` pairs through the
+ * transform (device, [count][N] each; c may alias a or b exactly). */
+rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *c, size_t count,
+                                uint32_t N, void *stream);
+
+/* ---- test helpers: host memory, deterministic from the seed ------------ */
+
+/* Binary keys and the two switching keys in standard layout (host arrays of
+ * n, N, rosetta_bsk_words and rosetta_ksk_words words).  Randomness is
+ * SplitMix64 used as a counter-based generator (Steele, Lea and Flood 2014):
+ * word(key, i) = mix(key + (i+1) * 0x9E3779B97F4A7C15); sub-stream keys
+ * word(seed, stream) with streams 1 (LWE key bits, top bit of word i),
+ * 2 (GLWE key bits), 3/4 (key mask words r*N+x / noise of row r, coefficient
+ * x, r = (2i+u)l+t), 5/6 (key-switching mask words r*n+c / noise r,
+ * r = j l_ks + t).  Uniform elements: w - p if w >= p.  Gaussian number g:
+ * Box-Muller on words 2g, 2g+1, rounded after scaling by sigma * 2^64
+ * (sigma is a fraction of the modulus).  The products A*S run on the host. */
+rosetta_status rosetta_keygen(uint64_t seed, const rosetta_params *params, double sigma_lwe,
+                              double sigma_glwe, uint64_t *lwe_key, uint64_t *glwe_key,
+                              uint64_t *bsk_std, uint64_t *ksk_std);
+
+/* Encryption of msgs[count] (values in Z_2M) under a binary key of length
+ * `dim` (host): masks from stream 7 word q*dim+c, noise from stream 8
+ * Gaussian q, of sub-stream keys of `seed`. */
+rosetta_status rosetta_lwe_encrypt(uint64_t seed, const rosetta_params *params, double sigma,
+                                   const uint64_t *key, uint32_t dim, const uint32_t *msgs,
+                                   size_t count, uint64_t *lwe_out);
+
+/* Decryption of `count` ciphertexts of dimension `dim` to Z_2M (host). */
+rosetta_status rosetta_lwe_decrypt(const rosetta_params *params, const uint64_t *key,
+                                   uint32_t dim, const uint64_t *lwe, size_t count,
+                                   uint32_t *msgs_out);
+
+/* Test polynomial [N] for a table of M entries in Z_2M (host). */
+rosetta_status rosetta_lut_build(const rosetta_params *params, const uint32_t *table,
+                                 uint64_t *test_poly);
+
+/* Release the library's device state on every device it touched (twiddle
+ * tables, workspaces).  The library re-initialises lazily afterwards. */
+rosetta_status rosetta_shutdown(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROSETTA_H */

@@ -1,0 +1,431 @@
+// C ABI of librosetta: host-side validation, per-device state (transform
+// tables, PBS workspace) and dispatch to the HIP kernels.  Nothing here
+// computes on the host except the twiddle tables; every step of the PBS runs
+// in kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "gl.hpp"
+#include "internal.hpp"
+#include "rosetta.h"
+
+using namespace rosetta;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+rosetta_status fail(rosetta_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+rosetta_status ok() {
+  g_last_error.clear();
+  return ROSETTA_OK;
+}
+
+rosetta_status hip_fail(hipError_t e, const char *what) {
+  if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation)
+    return fail(ROSETTA_ERR_NOMEM, "%s: %s", what, hipGetErrorString(e));
+  return fail(ROSETTA_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool is_pow2_in(uint32_t N, uint32_t lo, uint32_t hi) {
+  return N >= lo && N <= hi && (N & (N - 1)) == 0;
+}
+
+int ilog2u(uint32_t N) {
+  int l = 0;
+  while ((1u << l) < N) ++l;
+  return l;
+}
+
+rosetta_status check_params(const rosetta_params *p) {
+  if (!p) return fail(ROSETTA_ERR_NULL, "params is NULL");
+  if (p->k != 1) return fail(ROSETTA_ERR_UNSUPPORTED, "only k = 1 is supported (got %u)", p->k);
+  if (!is_pow2_in(p->N, 256, 4096))
+    return fail(ROSETTA_ERR_UNSUPPORTED, "N must be a power of two in [256, 4096] (got %u)",
+                p->N);
+  if (p->n < 1) return fail(ROSETTA_ERR_PARAMS, "n must be >= 1");
+  if (p->n > MAX_LWE_N)
+    return fail(ROSETTA_ERR_UNSUPPORTED, "n must be <= %u (got %u)", MAX_LWE_N, p->n);
+  if (p->pbs_level < 1 || p->pbs_base_log < 1)
+    return fail(ROSETTA_ERR_PARAMS, "pbs_level and pbs_base_log must be >= 1");
+  if (p->pbs_level > 4 || p->pbs_base_log > 30 || p->pbs_level * p->pbs_base_log > 62)
+    return fail(ROSETTA_ERR_UNSUPPORTED,
+                "need pbs_level <= 4, pbs_base_log <= 30 and l*beta <= 62");
+  if (p->ks_level < 1 || p->ks_base_log < 1)
+    return fail(ROSETTA_ERR_PARAMS, "ks_level and ks_base_log must be >= 1");
+  if (p->ks_level > 8 || p->ks_base_log > 30 || p->ks_level * p->ks_base_log > 62)
+    return fail(ROSETTA_ERR_UNSUPPORTED, "need ks_level <= 8, ks_base_log <= 30, l*beta <= 62");
+  const unsigned long long acc_bound =
+      (unsigned long long)p->N * p->ks_level << p->ks_base_log;
+  if (acc_bound >= (1ull << 32))
+    return fail(ROSETTA_ERR_UNSUPPORTED, "N * ks_level * 2^ks_base_log must be < 2^32");
+  if (p->msg_bits < 1 || p->msg_bits > 20 || (1u << p->msg_bits) > p->N)
+    return fail(ROSETTA_ERR_PARAMS, "need 1 <= msg_bits and 2^msg_bits <= N");
+  return ROSETTA_OK;
+}
+
+// [a, a + na) and [b, b + nb) overlap without being the same range start
+bool partial_overlap(const void *a, size_t na, const void *b, size_t nb) {
+  const char *x = (const char *)a, *y = (const char *)b;
+  if (x == y) return false;
+  return x < y + nb && y < x + na;
+}
+
+bool any_overlap(const void *a, size_t na, const void *b, size_t nb) {
+  const char *x = (const char *)a, *y = (const char *)b;
+  return x < y + nb && y < x + na;
+}
+
+// ---- per-device state ------------------------------------------------------
+
+struct DevTables {
+  uint64_t *zeta = nullptr;
+  uint64_t *zeta_inv = nullptr;
+  uint64_t ninv = 0;
+};
+
+struct DeviceState {
+  std::map<uint32_t, DevTables> tables;
+  void *workspace = nullptr;
+  size_t workspace_bytes = 0;
+};
+
+std::mutex g_mu;
+std::map<int, DeviceState> g_dev;
+
+uint32_t bitrev(uint32_t x, int bits) {
+  uint32_t r = 0;
+  for (int b = 0; b < bits; ++b)
+    if (x & (1u << b)) r |= 1u << (bits - 1 - b);
+  return r;
+}
+
+rosetta_status get_tables(uint32_t N, Tables &out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState &ds = g_dev[dev];
+  auto it = ds.tables.find(N);
+  if (it == ds.tables.end()) {
+    const int logn = ilog2u(N);
+    const u64 psi = gl_pow(7, (GL_P - 1) / (2 * (u64)N));
+    std::vector<u64> z(N), zi(N);
+    for (uint32_t m = 0; m < N; ++m) {
+      const uint32_t r = bitrev(m, logn);
+      z[m] = gl_pow(psi, r);
+      zi[m] = gl_pow(psi, (2 * (u64)N - r) % (2 * (u64)N));
+    }
+    DevTables t;
+    e = hipMalloc(&t.zeta, N * sizeof(u64));
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc(twiddles)");
+    e = hipMalloc(&t.zeta_inv, N * sizeof(u64));
+    if (e != hipSuccess) {
+      (void)hipFree(t.zeta);
+      return hip_fail(e, "hipMalloc(twiddles)");
+    }
+    e = hipMemcpy(t.zeta, z.data(), N * sizeof(u64), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy(t.zeta_inv, zi.data(), N * sizeof(u64), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      (void)hipFree(t.zeta);
+      (void)hipFree(t.zeta_inv);
+      return hip_fail(e, "hipMemcpy(twiddles)");
+    }
+    t.ninv = gl_inv(N);
+    it = ds.tables.emplace(N, t).first;
+  }
+  out.zeta = it->second.zeta;
+  out.zeta_inv = it->second.zeta_inv;
+  out.ninv = it->second.ninv;
+  return ROSETTA_OK;
+}
+
+rosetta_status get_workspace(size_t bytes, void **ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState &ds = g_dev[dev];
+  if (ds.workspace_bytes < bytes) {
+    if (ds.workspace) {
+      // earlier calls may still read the old buffer
+      e = hipDeviceSynchronize();
+      if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+      (void)hipFree(ds.workspace);
+      ds.workspace = nullptr;
+      ds.workspace_bytes = 0;
+    }
+    e = hipMalloc(&ds.workspace, bytes);
+    if (e != hipSuccess) {
+      ds.workspace = nullptr;
+      return hip_fail(e, "hipMalloc(workspace)");
+    }
+    ds.workspace_bytes = bytes;
+  }
+  *ptr = ds.workspace;
+  return ROSETTA_OK;
+}
+
+size_t lwe_words(const rosetta_params *p, size_t batch) { return batch * (size_t)(p->n + 1); }
+
+}  // namespace
+
+void rosetta::set_last_error(const char *msg) { g_last_error = msg; }
+
+extern "C" {
+
+const char *rosetta_version(void) { return "rosetta-pbs 0.1.0 (gfx950)"; }
+
+const char *rosetta_status_string(int st) {
+  switch (st) {
+    case ROSETTA_OK: return "ROSETTA_OK";
+    case ROSETTA_ERR_NULL: return "ROSETTA_ERR_NULL";
+    case ROSETTA_ERR_PARAMS: return "ROSETTA_ERR_PARAMS";
+    case ROSETTA_ERR_UNSUPPORTED: return "ROSETTA_ERR_UNSUPPORTED";
+    case ROSETTA_ERR_ALIAS: return "ROSETTA_ERR_ALIAS";
+    case ROSETTA_ERR_NOMEM: return "ROSETTA_ERR_NOMEM";
+    case ROSETTA_ERR_DEVICE: return "ROSETTA_ERR_DEVICE";
+    case ROSETTA_ERR_SIZE: return "ROSETTA_ERR_SIZE";
+    default: return "ROSETTA_ERR_UNKNOWN";
+  }
+}
+
+const char *rosetta_last_error(void) { return g_last_error.c_str(); }
+
+rosetta_status rosetta_check_params(const rosetta_params *params) {
+  rosetta_status st = check_params(params);
+  return st == ROSETTA_OK ? ok() : st;
+}
+
+size_t rosetta_bsk_words(const rosetta_params *p) {
+  return p ? (size_t)p->n * 2 * p->pbs_level * 2 * p->N : 0;
+}
+
+size_t rosetta_ksk_words(const rosetta_params *p) {
+  return p ? (size_t)p->N * p->ks_level * (p->n + 1) : 0;
+}
+
+size_t rosetta_ksk_device_words(const rosetta_params *p) {
+  return p ? rosetta_ksk_words(p) + (p->n + 1) : 0;
+}
+
+rosetta_status rosetta_bsk_prepare(const uint64_t *bsk_std_dev, uint64_t *bsk_dev,
+                                   const rosetta_params *params, void *stream) {
+  rosetta_status st = check_params(params);
+  if (st) return st;
+  if (!bsk_std_dev || !bsk_dev) return fail(ROSETTA_ERR_NULL, "bsk pointer is NULL");
+  const size_t bytes = rosetta_bsk_words(params) * 8;
+  if (any_overlap(bsk_std_dev, bytes, bsk_dev, bytes))
+    return fail(ROSETTA_ERR_ALIAS, "bsk_std_dev and bsk_dev overlap");
+  Tables tb;
+  if ((st = get_tables(params->N, tb))) return st;
+  hipError_t e = launch_bsk_prepare(bsk_std_dev, bsk_dev, *params, tb, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "bsk_prepare launch");
+}
+
+rosetta_status rosetta_ksk_prepare(const uint64_t *ksk_std_dev, uint64_t *ksk_dev,
+                                   const rosetta_params *params, void *stream) {
+  rosetta_status st = check_params(params);
+  if (st) return st;
+  if (!ksk_std_dev || !ksk_dev) return fail(ROSETTA_ERR_NULL, "ksk pointer is NULL");
+  if (any_overlap(ksk_std_dev, rosetta_ksk_words(params) * 8, ksk_dev,
+                  rosetta_ksk_device_words(params) * 8))
+    return fail(ROSETTA_ERR_ALIAS, "ksk_std_dev and ksk_dev overlap");
+  hipError_t e = launch_ksk_prepare(ksk_std_dev, ksk_dev, *params, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "ksk_prepare launch");
+}
+
+size_t rosetta_pbs_workspace_bytes(const rosetta_params *p, size_t batch) {
+  return p ? batch * (size_t)(p->N + 1) * sizeof(uint64_t) : 0;
+}
+
+static rosetta_status check_br_args(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                    const uint64_t *lut, const void *out, size_t out_bytes,
+                                    size_t batch, const rosetta_params *p) {
+  if (!lwe_in || !bsk_dev || !lut || !out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t in_bytes = lwe_words(p, batch) * 8;
+  if (any_overlap(out, out_bytes, lwe_in, in_bytes) ||
+      any_overlap(out, out_bytes, lut, (size_t)p->N * 8) ||
+      any_overlap(out, out_bytes, bsk_dev, rosetta_bsk_words(p) * 8))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps an input");
+  return ROSETTA_OK;
+}
+
+rosetta_status rosetta_pbs_batch_ws(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                    const uint64_t *ksk_dev, const uint64_t *lut,
+                                    uint64_t *lwe_out, size_t batch,
+                                    const rosetta_params *params, void *workspace,
+                                    size_t workspace_bytes, void *stream) {
+  rosetta_status st = check_params(params);
+  if (st) return st;
+  if (batch == 0) return ok();
+  if (!lwe_in || !bsk_dev || !ksk_dev || !lut || !lwe_out)
+    return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  if (!workspace) return fail(ROSETTA_ERR_NULL, "workspace is NULL");
+  const size_t need = rosetta_pbs_workspace_bytes(params, batch);
+  if (workspace_bytes < need)
+    return fail(ROSETTA_ERR_SIZE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
+  const size_t io = lwe_words(params, batch) * 8;
+  if (partial_overlap(lwe_in, io, lwe_out, io))
+    return fail(ROSETTA_ERR_ALIAS, "lwe_in and lwe_out partially overlap");
+  if (any_overlap(workspace, need, lwe_in, io) || any_overlap(workspace, need, lwe_out, io) ||
+      any_overlap(workspace, need, lut, (size_t)params->N * 8) ||
+      any_overlap(lwe_out, io, lut, (size_t)params->N * 8) ||
+      any_overlap(lwe_out, io, bsk_dev, rosetta_bsk_words(params) * 8) ||
+      any_overlap(lwe_out, io, ksk_dev, rosetta_ksk_device_words(params) * 8))
+    return fail(ROSETTA_ERR_ALIAS, "workspace or output overlaps another buffer");
+  Tables tb;
+  if ((st = get_tables(params->N, tb))) return st;
+  uint64_t *big = (uint64_t *)workspace;
+  hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, lut, big, batch, *params, tb, BR_EXTRACT,
+                                     (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "blind_rotate launch");
+  e = launch_keyswitch(big, ksk_dev, lwe_out, batch, *params, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "keyswitch launch");
+  return ok();
+}
+
+rosetta_status rosetta_pbs_batch(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                 const uint64_t *ksk_dev, const uint64_t *lut, uint64_t *lwe_out,
+                                 size_t batch, const rosetta_params *params, void *stream) {
+  rosetta_status st = check_params(params);
+  if (st) return st;
+  if (batch == 0) return ok();
+  if (!lwe_in || !bsk_dev || !ksk_dev || !lut || !lwe_out)
+    return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  void *ws = nullptr;
+  const size_t need = rosetta_pbs_workspace_bytes(params, batch);
+  if ((st = get_workspace(need, &ws))) return st;
+  return rosetta_pbs_batch_ws(lwe_in, bsk_dev, ksk_dev, lut, lwe_out, batch, params, ws, need,
+                              stream);
+}
+
+rosetta_status rosetta_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                    const uint64_t *lut, uint64_t *glwe_out, size_t batch,
+                                    const rosetta_params *params, void *stream) {
+  rosetta_status st = check_params(params);
+  if (st) return st;
+  if (batch == 0) return ok();
+  if ((st = check_br_args(lwe_in, bsk_dev, lut, glwe_out, batch * 2 * (size_t)params->N * 8,
+                          batch, params)))
+    return st;
+  Tables tb;
+  if ((st = get_tables(params->N, tb))) return st;
+  hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, lut, glwe_out, batch, *params, tb, BR_GLWE,
+                                     (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "blind_rotate launch");
+}
+
+rosetta_status rosetta_blind_rotate_extract(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                            const uint64_t *lut, uint64_t *big_out,
+                                            size_t batch, const rosetta_params *params,
+                                            void *stream) {
+  rosetta_status st = check_params(params);
+  if (st) return st;
+  if (batch == 0) return ok();
+  if ((st = check_br_args(lwe_in, bsk_dev, lut, big_out, batch * ((size_t)params->N + 1) * 8,
+                          batch, params)))
+    return st;
+  Tables tb;
+  if ((st = get_tables(params->N, tb))) return st;
+  hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, lut, big_out, batch, *params, tb,
+                                     BR_EXTRACT, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "blind_rotate launch");
+}
+
+rosetta_status rosetta_keyswitch(const uint64_t *big_in, const uint64_t *ksk_dev,
+                                 uint64_t *lwe_out, size_t batch, const rosetta_params *params,
+                                 void *stream) {
+  rosetta_status st = check_params(params);
+  if (st) return st;
+  if (batch == 0) return ok();
+  if (!big_in || !ksk_dev || !lwe_out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t out_bytes = lwe_words(params, batch) * 8;
+  if (any_overlap(lwe_out, out_bytes, big_in, batch * ((size_t)params->N + 1) * 8) ||
+      any_overlap(lwe_out, out_bytes, ksk_dev, rosetta_ksk_device_words(params) * 8))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps an input");
+  hipError_t e = launch_keyswitch(big_in, ksk_dev, lwe_out, batch, *params, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "keyswitch launch");
+}
+
+static rosetta_status check_ntt_args(const void *in, const void *out, size_t count, uint32_t N) {
+  if (!is_pow2_in(N, 256, 4096))
+    return fail(ROSETTA_ERR_UNSUPPORTED, "N must be a power of two in [256, 4096]");
+  if (count == 0) return ROSETTA_OK;
+  if (!in || !out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t bytes = count * (size_t)N * 8;
+  if (partial_overlap(in, bytes, out, bytes))
+    return fail(ROSETTA_ERR_ALIAS, "in and out partially overlap");
+  return ROSETTA_OK;
+}
+
+rosetta_status rosetta_ntt_forward(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,
+                                   void *stream) {
+  rosetta_status st = check_ntt_args(in, out, count, N);
+  if (st) return st;
+  if (count == 0) return ok();
+  Tables tb;
+  if ((st = get_tables(N, tb))) return st;
+  hipError_t e = launch_ntt(in, out, count, N, tb, false, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "ntt launch");
+}
+
+rosetta_status rosetta_ntt_inverse(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,
+                                   void *stream) {
+  rosetta_status st = check_ntt_args(in, out, count, N);
+  if (st) return st;
+  if (count == 0) return ok();
+  Tables tb;
+  if ((st = get_tables(N, tb))) return st;
+  hipError_t e = launch_ntt(in, out, count, N, tb, true, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "ntt launch");
+}
+
+rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *c, size_t count,
+                                uint32_t N, void *stream) {
+  rosetta_status st = check_ntt_args(a, c, count, N);
+  if (st) return st;
+  if ((st = check_ntt_args(b, c, count, N))) return st;
+  if (count == 0) return ok();
+  Tables tb;
+  if ((st = get_tables(N, tb))) return st;
+  hipError_t e = launch_poly_mul(a, b, c, count, N, tb, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "poly_mul launch");
+}
+
+rosetta_status rosetta_shutdown(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  for (auto &kv : g_dev) {
+    (void)hipSetDevice(kv.first);
+    (void)hipDeviceSynchronize();
+    for (auto &t : kv.second.tables) {
+      (void)hipFree(t.second.zeta);
+      (void)hipFree(t.second.zeta_inv);
+    }
+    if (kv.second.workspace) (void)hipFree(kv.second.workspace);
+  }
+  g_dev.clear();
+  (void)hipSetDevice(cur);
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,45 @@
+// Internal interface between the C ABI (abi.cpp) and the kernels
+// (kernels.hip).  Not installed; the public surface is include/rosetta.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "rosetta.h"
+
+namespace rosetta {
+
+// Largest LWE dimension the blind-rotation kernel accepts (its rounded
+// rotation amounts are staged in LDS).
+constexpr uint32_t MAX_LWE_N = 2048;
+
+// Per-device, per-N transform tables (device pointers) and N^-1.
+struct Tables {
+  const uint64_t *zeta;      // [N]: zeta[m] = psi^rev(m), m >= 1
+  const uint64_t *zeta_inv;  // [N]: psi^-rev(m)
+  uint64_t ninv;
+};
+
+enum BrMode { BR_GLWE = 0, BR_EXTRACT = 1 };
+
+// Record the calling thread's error message (read by rosetta_last_error).
+void set_last_error(const char *msg);
+
+hipError_t launch_bsk_prepare(const uint64_t *bsk_std, uint64_t *bsk_dev,
+                              const rosetta_params &p, const Tables &tb, hipStream_t st);
+hipError_t launch_ksk_prepare(const uint64_t *ksk_std, uint64_t *ksk_dev,
+                              const rosetta_params &p, hipStream_t st);
+hipError_t launch_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                               const uint64_t *lut, uint64_t *out, size_t batch,
+                               const rosetta_params &p, const Tables &tb, BrMode mode,
+                               hipStream_t st);
+hipError_t launch_keyswitch(const uint64_t *big, const uint64_t *ksk_dev, uint64_t *out,
+                            size_t batch, const rosetta_params &p, hipStream_t st);
+hipError_t launch_ntt(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,
+                      const Tables &tb, bool inverse, hipStream_t st);
+hipError_t launch_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *c, size_t count,
+                           uint32_t N, const Tables &tb, hipStream_t st);
+
+}  // namespace rosetta

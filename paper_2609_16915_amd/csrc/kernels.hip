@@ -1,0 +1,467 @@
+// HIP kernels for batched programmable bootstrapping on gfx950.
+//
+// One workgroup owns one ciphertext for the whole blind rotation: the GLWE
+// accumulator stays in registers (E coefficients of each component per
+// thread) for all n CMux steps, and every transform is done by the
+// workgroup in registers with LDS transposes (ntt.hpp).  Only the
+// bootstrapping key is streamed from memory; all workgroups walk the key in
+// the same order i = 0..n-1, so a GGSW row fetched by one workgroup is
+// served from L2 / the Infinity Cache to the others.
+#include <hip/hip_runtime.h>
+
+#include "gl.hpp"
+#include "internal.hpp"
+#include "ntt.hpp"
+
+namespace rosetta {
+
+// ---------------------------------------------------------------------------
+// Key preparation
+// ---------------------------------------------------------------------------
+
+// Row r of the standard key (N coefficients) -> transform domain, scaled by
+// N^-1, stored as [r][k][tid] so that thread tid of the blind rotation
+// reads its E words of the row with unit stride across the workgroup.
+template <class S>
+__global__ void __launch_bounds__(S::T)
+k_bsk_prepare(const u64 *__restrict__ std_key, u64 *__restrict__ dev_key,
+              const u64 *__restrict__ zeta, u64 ninv) {
+  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
+  LdsPair lds(lds_mem, S::LDS_WORDS);
+  const int tid = threadIdx.x;
+  const size_t row = blockIdx.x;
+  u64 x[S::E];
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) x[k] = std_key[row * S::N + tid + S::T * k];
+  ntt_forward<S>(x, lds, tid, as_global(zeta));
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) dev_key[row * S::N + k * S::T + tid] = gl_mul(x[k], ninv);
+}
+
+// Prepared key-switching key: the standard [N*l_ks][n+1] words followed by
+// h * (sum over rows of column c), h = 2^(beta_ks - 1), for the offset-digit
+// accumulation of k_keyswitch.
+__global__ void k_ksk_colsum(const u64 *__restrict__ ksk, u64 *__restrict__ out, size_t rows,
+                             int cols, u64 half) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= cols) return;
+  u64 s = 0;
+  for (size_t r = 0; r < rows; ++r) s = gl_add(s, ksk[r * cols + c]);
+  out[c] = gl_mul(s, half);
+}
+
+// ---------------------------------------------------------------------------
+// Stand-alone transforms
+// ---------------------------------------------------------------------------
+
+template <class S>
+__global__ void __launch_bounds__(S::T)
+k_ntt_forward(const u64 *in, u64 *out, const u64 *__restrict__ zeta) {
+  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
+  LdsPair lds(lds_mem, S::LDS_WORDS);
+  const int tid = threadIdx.x;
+  const size_t base = (size_t)blockIdx.x * S::N;
+  u64 x[S::E];
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) x[k] = in[base + tid + S::T * k];
+  ntt_forward<S>(x, lds, tid, as_global(zeta));
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) out[base + S::idx(S::PASSES - 1, tid, k)] = x[k];
+}
+
+template <class S>
+__global__ void __launch_bounds__(S::T)
+k_ntt_inverse(const u64 *in, u64 *out, const u64 *__restrict__ zeta_inv, u64 ninv) {
+  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
+  LdsPair lds(lds_mem, S::LDS_WORDS);
+  const int tid = threadIdx.x;
+  const size_t base = (size_t)blockIdx.x * S::N;
+  u64 x[S::E];
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) x[k] = in[base + S::idx(S::PASSES - 1, tid, k)];
+  ntt_inverse<S>(x, lds, tid, as_global(zeta_inv));
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) out[base + tid + S::T * k] = gl_mul(x[k], ninv);
+}
+
+template <class S>
+__global__ void __launch_bounds__(S::T)
+k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta,
+           const u64 *__restrict__ zeta_inv, u64 ninv) {
+  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
+  LdsPair lds(lds_mem, S::LDS_WORDS);
+  const int tid = threadIdx.x;
+  const size_t base = (size_t)blockIdx.x * S::N;
+  u64 x[S::E], y[S::E];
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) {
+    x[k] = a[base + tid + S::T * k];
+    y[k] = b[base + tid + S::T * k];
+  }
+  ntt_forward<S>(x, lds, tid, as_global(zeta));
+  ntt_forward<S>(y, lds, tid, as_global(zeta));
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) x[k] = gl_mul(x[k], y[k]);
+  ntt_inverse<S>(x, lds, tid, as_global(zeta_inv));
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) c[base + tid + S::T * k] = gl_mul(x[k], ninv);
+}
+
+// ---------------------------------------------------------------------------
+// Blind rotation (+ sample extraction)
+// ---------------------------------------------------------------------------
+
+#ifndef BR_WAVES_PER_EU
+#define BR_WAVES_PER_EU 2
+#endif
+
+// Coefficient j of X^r * v (negacyclic), 0 <= r < 2N.
+template <int N>
+__device__ __forceinline__ u64 rotated_coef(const u64 *v, int j, int r) {
+  const int rr = r & (N - 1);
+  const bool neg = (j < rr) != (r >= N);
+  const u64 x = v[(j - rr) & (N - 1)];
+  return neg ? gl_neg(x) : x;
+}
+
+// Digit t (0 = most significant) of the balanced base-2^beta expansion of
+// the rounded value r (see gl_digit); L is the number of levels.
+template <int L, typename RT>
+__device__ __forceinline__ RT digit_of(RT r, int beta, int t) {
+  const RT half = (RT)1 << (beta - 1);
+  const RT mask = ((RT)1 << beta) - 1;
+  RT d = 0;
+#pragma unroll
+  for (int u = L - 1; u >= 1; --u) {
+    const RT du = ((r + half) & mask) - half;
+    if (u == t) d = du;
+    r = (r - du) >> beta;
+  }
+  return t == 0 ? r : d;
+}
+
+// One workgroup per ciphertext.  Per CMux step i:
+//   a2  D_u = X^(a~_i) ACC_u - ACC_u           (rotation through LDS)
+//   a3  digits of D_u, level t                 (registers)
+//   a4  forward transform of each digit poly   (registers + LDS)
+//   a5  Y_c += digits^ . GGSW_i[u][t][c]^      (key streamed, pre-transformed)
+//   a6  ACC_c += inverse transform of Y_c
+// The transform-domain key rows are pre-scaled by N^-1 (k_bsk_prepare).
+// RT holds the rounded value before digit extraction: 32 bits suffice when
+// l * beta <= 30.
+template <class S, int L, typename RT>
+__global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(BR_WAVES_PER_EU)))
+k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
+               const u64 *__restrict__ lut, u64 *__restrict__ out, int n, int beta, int mode,
+               const u64 *__restrict__ zeta, const u64 *__restrict__ zeta_inv) {
+  constexpr int N = S::N, E = S::E, T = S::T;
+  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
+  __shared__ uint16_t rot[MAX_LWE_N + 1];
+  LdsPair lds(lds_mem, S::LDS_WORDS);
+  const int tid = threadIdx.x;
+  const size_t ct = blockIdx.x;
+
+  // a1: rounded rotation amounts of the whole ciphertext
+  const u64 *lwe = lwe_in + ct * (size_t)(n + 1);
+  for (int i = tid; i <= n; i += T) rot[i] = (uint16_t)gl_modswitch(lwe[i], S::LOGN);
+  __syncthreads();
+
+  u64 accA[E], accB[E];
+  {
+    const int r = (2 * N - (int)rot[n]) & (2 * N - 1);  // X^(-b~)
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      accA[k] = 0;
+      accB[k] = rotated_coef<N>(lut, tid + T * k, r);
+    }
+  }
+
+  const int s = 64 - L * beta;
+  constexpr size_t ggsw_words = (size_t)2 * L * 2 * N;
+  for (int i = 0; i < n; ++i) {
+    // Opaque copies of the table pointers: without them the compiler hoists
+    // every twiddle load out of the step loop and keeps the values live,
+    // which costs more occupancy than the reloads (cache hits) cost time.
+    const u64 *zf = zeta, *zi = zeta_inv;
+    asm volatile("" : "+s"(zf), "+s"(zi));
+    const int a = rot[i];
+    const int ar = a & (N - 1);
+    const bool flip = a >= N;
+    u64 Y0[E], Y1[E];
+#pragma unroll
+    for (int k = 0; k < E; ++k) Y0[k] = Y1[k] = 0;
+    gconst_u64 *G = as_global(bsk) + (size_t)i * ggsw_words + tid;
+
+#pragma unroll 1
+    for (int u = 0; u < 2; ++u) {
+      // a2: rotate-subtract, then round away the s low bits
+      RT R[E];
+      {
+        u64 cur[E];
+#pragma unroll
+        for (int k = 0; k < E; ++k) cur[k] = u ? accB[k] : accA[k];
+        u64 *buf = lds.next();
+#pragma unroll
+        for (int k = 0; k < E; ++k) buf[S::pad(tid) + S::pad(T * k)] = cur[k];
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < E; ++k) {
+          const int j = tid + T * k;
+          const bool neg = (j < ar) != flip;
+          const u64 v = buf[S::pad((j - ar) & (N - 1))];
+          const u64 d = gl_sub(neg ? gl_neg(v) : v, cur[k]);
+          R[k] = (RT)gl_round_top(d, s);
+        }
+      }
+#pragma unroll 1
+      for (int t = 0; t < L; ++t) {
+        // a3: digit polynomial of level t
+        u64 x[E];
+#pragma unroll
+        for (int k = 0; k < E; ++k) x[k] = gl_from_i64((i64)digit_of<L, RT>(R[k], beta, t));
+        // a4: forward transform
+        ntt_forward<S>(x, lds, tid, as_global(zf));
+        // a5: multiply-accumulate with the two rows of GGSW_i[u][t]
+        gconst_u64 *g = G + (size_t)((u * L + t) * 2) * N;
+#pragma unroll
+        for (int k = 0; k < E; ++k) {
+          Y0[k] = gl_add(Y0[k], gl_mul(x[k], g[k * T]));
+          Y1[k] = gl_add(Y1[k], gl_mul(x[k], g[N + k * T]));
+        }
+      }
+    }
+    // a6: back to coefficients, accumulate (one loop body for both
+    // components keeps a single copy of the inverse transform)
+#pragma unroll 1
+    for (int c = 0; c < 2; ++c) {
+      u64 y[E];
+#pragma unroll
+      for (int k = 0; k < E; ++k) y[k] = c ? Y1[k] : Y0[k];
+      ntt_inverse<S>(y, lds, tid, as_global(zi));
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        if (c)
+          accB[k] = gl_add(accB[k], y[k]);
+        else
+          accA[k] = gl_add(accA[k], y[k]);
+      }
+    }
+  }
+
+  if (mode == BR_GLWE) {
+    u64 *o = out + ct * (size_t)(2 * N);
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      o[tid + T * k] = accA[k];
+      o[N + tid + T * k] = accB[k];
+    }
+  } else {
+    // a7: sample extraction  a'_0 = A_0, a'_j = -A_{N-j}, b' = B_0
+    u64 *o = out + ct * (size_t)(N + 1);
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      const int j = tid + T * k;
+      o[(N - j) & (N - 1)] = j ? gl_neg(accA[k]) : accA[k];
+      if (j == 0) o[N] = accB[k];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Key switching
+// ---------------------------------------------------------------------------
+
+// out[b][c] = (c == n ? b'_b : 0) - sum_{j,t} d_{b,j,t} KSK[j][t][c].
+// A workgroup covers KS_BT ciphertexts x 256 output columns.  Digits are
+// produced in LDS per chunk of KS_JC input coefficients in offset form
+// d + h in [0, 2h] (h = 2^(beta_ks-1)); the offset is removed at the end
+// with the column sums stored after the key (k_ksk_colsum).  Sums of
+// offset digit x 32-bit half-word products stay below N l_ks 2^beta_ks
+// 2^32 < 2^64, so the two 64-bit accumulators per output never wrap.
+constexpr int KS_BT = 16;
+constexpr int KS_JC = 32;
+constexpr int KS_TPB = 256;
+
+template <int LKS>
+__global__ void __launch_bounds__(KS_TPB)
+k_keyswitch(const u64 *__restrict__ big, const u64 *__restrict__ ksk, u64 *__restrict__ out,
+            size_t batch, int n, int N, int beta) {
+  __shared__ u32 dig[KS_JC][LKS][KS_BT];
+  __shared__ u64 body[KS_BT];
+  const int tid = threadIdx.x;
+  const int c = blockIdx.y * KS_TPB + tid;
+  const size_t b0 = (size_t)blockIdx.x * KS_BT;
+  const int cols = n + 1;
+  const int s = 64 - LKS * beta;
+  const i64 h = (i64)1 << (beta - 1);
+  const i64 mask = ((i64)1 << beta) - 1;
+
+  u64 acc_lo[KS_BT], acc_hi[KS_BT];
+#pragma unroll
+  for (int b = 0; b < KS_BT; ++b) acc_lo[b] = acc_hi[b] = 0;
+  if (tid < KS_BT) body[tid] = (b0 + tid < batch) ? big[(b0 + tid) * (size_t)(N + 1) + N] : 0;
+
+  for (int j0 = 0; j0 < N; j0 += KS_JC) {
+    __syncthreads();
+    for (int e = tid; e < KS_BT * KS_JC; e += KS_TPB) {
+      const int bb = e / KS_JC, jj = e % KS_JC;
+      const size_t q = b0 + bb;
+      const u64 a = q < batch ? big[q * (size_t)(N + 1) + j0 + jj] : 0;
+      i64 r = gl_round_top(a, s);
+#pragma unroll
+      for (int t = LKS - 1; t >= 1; --t) {
+        const i64 d = ((r + h) & mask) - h;
+        r = (r - d) >> beta;
+        dig[jj][t][bb] = (u32)(d + h);
+      }
+      dig[jj][0][bb] = (u32)(r + h);
+    }
+    __syncthreads();
+    if (c < cols) {
+      const u64 *kp = ksk + (size_t)j0 * LKS * cols + c;
+#pragma unroll 4
+      for (int jj = 0; jj < KS_JC; ++jj) {
+#pragma unroll
+        for (int t = 0; t < LKS; ++t) {
+          const u64 w = kp[(size_t)(jj * LKS + t) * cols];
+          const u32 wl = (u32)w, wh = (u32)(w >> 32);
+#pragma unroll
+          for (int b = 0; b < KS_BT; ++b) {
+            const u32 d = dig[jj][t][b];
+            acc_lo[b] += (u64)d * wl;
+            acc_hi[b] += (u64)d * wh;
+          }
+        }
+      }
+    }
+  }
+  if (c < cols) {
+    const u64 hc = ksk[(size_t)N * LKS * cols + c];
+#pragma unroll
+    for (int b = 0; b < KS_BT; ++b) {
+      const size_t q = b0 + b;
+      if (q >= batch) break;
+      u64 lo = acc_lo[b] + (acc_hi[b] << 32);
+      const u64 hi = (acc_hi[b] >> 32) + (lo < acc_lo[b] ? 1 : 0);
+      const u64 sum = gl_reduce128(lo, hi);
+      u64 r = gl_sub(c == n ? body[b] : 0, sum);
+      out[q * (size_t)cols + c] = gl_add(r, hc);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+
+#define ROSETTA_DISPATCH_N(LOGN_VAR, ...)                  \
+  switch (LOGN_VAR) {                                      \
+    case 8: { using S = Ntt<8, 2>; __VA_ARGS__; } break;   \
+    case 9: { using S = Ntt<9, 3>; __VA_ARGS__; } break;   \
+    case 10: { using S = Ntt<10, 3>; __VA_ARGS__; } break; \
+    case 11: { using S = Ntt<11, 3>; __VA_ARGS__; } break; \
+    case 12: { using S = Ntt<12, 3>; __VA_ARGS__; } break; \
+    default: return hipErrorInvalidValue;                  \
+  }
+
+static int ilog2(uint32_t N) {
+  int l = 0;
+  while ((1u << l) < N) ++l;
+  return l;
+}
+
+hipError_t launch_bsk_prepare(const uint64_t *bsk_std, uint64_t *bsk_dev,
+                              const rosetta_params &p, const Tables &tb, hipStream_t st) {
+  const size_t rows = (size_t)p.n * 2 * p.pbs_level * 2;
+  ROSETTA_DISPATCH_N(ilog2(p.N), hipLaunchKernelGGL(k_bsk_prepare<S>, dim3(rows), dim3(S::T), 0,
+                                                    st, bsk_std, bsk_dev, tb.zeta, tb.ninv));
+  return hipGetLastError();
+}
+
+hipError_t launch_ksk_prepare(const uint64_t *ksk_std, uint64_t *ksk_dev,
+                              const rosetta_params &p, hipStream_t st) {
+  const size_t rows = (size_t)p.N * p.ks_level;
+  const int cols = (int)p.n + 1;
+  hipError_t e = hipMemcpyAsync(ksk_dev, ksk_std, rows * cols * sizeof(u64),
+                                hipMemcpyDeviceToDevice, st);
+  if (e != hipSuccess) return e;
+  const u64 half = 1ull << (p.ks_base_log - 1);
+  hipLaunchKernelGGL(k_ksk_colsum, dim3((cols + 255) / 256), dim3(256), 0, st, ksk_std,
+                     ksk_dev + rows * cols, rows, cols, half);
+  return hipGetLastError();
+}
+
+template <class S, int L>
+static void launch_br_levels(const uint64_t *lwe_in, const uint64_t *bsk_dev, const uint64_t *lut,
+                             uint64_t *out, size_t batch, const rosetta_params &p,
+                             const Tables &tb, int mode, hipStream_t st) {
+  const int n = (int)p.n, beta = (int)p.pbs_base_log;
+  if (L * beta <= 30)
+    hipLaunchKernelGGL((k_blind_rotate<S, L, int32_t>), dim3(batch), dim3(S::T), 0, st, lwe_in,
+                       bsk_dev, lut, out, n, beta, mode, tb.zeta, tb.zeta_inv);
+  else
+    hipLaunchKernelGGL((k_blind_rotate<S, L, int64_t>), dim3(batch), dim3(S::T), 0, st, lwe_in,
+                       bsk_dev, lut, out, n, beta, mode, tb.zeta, tb.zeta_inv);
+}
+
+hipError_t launch_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                               const uint64_t *lut, uint64_t *out, size_t batch,
+                               const rosetta_params &p, const Tables &tb, BrMode mode,
+                               hipStream_t st) {
+#define ROSETTA_BR_L(LV)                                                             \
+  case LV:                                                                           \
+    launch_br_levels<S, LV>(lwe_in, bsk_dev, lut, out, batch, p, tb, (int)mode, st); \
+    break;
+  ROSETTA_DISPATCH_N(ilog2(p.N), switch (p.pbs_level) {
+    ROSETTA_BR_L(1) ROSETTA_BR_L(2) ROSETTA_BR_L(3) ROSETTA_BR_L(4)
+    default: return hipErrorInvalidValue;
+  });
+#undef ROSETTA_BR_L
+  return hipGetLastError();
+}
+
+hipError_t launch_keyswitch(const uint64_t *big, const uint64_t *ksk_dev, uint64_t *out,
+                            size_t batch, const rosetta_params &p, hipStream_t st) {
+  const dim3 grid((unsigned)((batch + KS_BT - 1) / KS_BT), (p.n + 1 + KS_TPB - 1) / KS_TPB);
+  const int n = (int)p.n, N = (int)p.N, beta = (int)p.ks_base_log;
+#define ROSETTA_KS_CASE(LK)                                                                 \
+  case LK:                                                                                  \
+    hipLaunchKernelGGL(k_keyswitch<LK>, grid, dim3(KS_TPB), 0, st, big, ksk_dev, out, batch, \
+                       n, N, beta);                                                         \
+    break;
+  switch (p.ks_level) {
+    ROSETTA_KS_CASE(1)
+    ROSETTA_KS_CASE(2)
+    ROSETTA_KS_CASE(3)
+    ROSETTA_KS_CASE(4)
+    ROSETTA_KS_CASE(5)
+    ROSETTA_KS_CASE(6)
+    ROSETTA_KS_CASE(7)
+    ROSETTA_KS_CASE(8)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef ROSETTA_KS_CASE
+  return hipGetLastError();
+}
+
+hipError_t launch_ntt(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,
+                      const Tables &tb, bool inverse, hipStream_t st) {
+  if (inverse) {
+    ROSETTA_DISPATCH_N(ilog2(N), hipLaunchKernelGGL(k_ntt_inverse<S>, dim3(count), dim3(S::T), 0,
+                                                    st, in, out, tb.zeta_inv, tb.ninv));
+  } else {
+    ROSETTA_DISPATCH_N(ilog2(N), hipLaunchKernelGGL(k_ntt_forward<S>, dim3(count), dim3(S::T), 0,
+                                                    st, in, out, tb.zeta));
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *c, size_t count,
+                           uint32_t N, const Tables &tb, hipStream_t st) {
+  ROSETTA_DISPATCH_N(ilog2(N), hipLaunchKernelGGL(k_poly_mul<S>, dim3(count), dim3(S::T), 0, st,
+                                                  a, b, c, tb.zeta, tb.zeta_inv, tb.ninv));
+  return hipGetLastError();
+}
+
+}  // namespace rosetta

@@ -1,0 +1,321 @@
+"""Python binding of librosetta (batched TFHE PBS on MI355X).
+
+Argument marshalling only: every step of the PBS runs in the library's HIP
+kernels.  Device buffers are torch tensors on a ROCm device (dtype uint64, or
+int64 read as raw 64-bit words), passed by data_ptr() together with the
+current HIP stream; host helpers take and return numpy arrays.  There is no
+fallback: if the library is not built, or a call fails, an exception is
+raised.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "librosetta.so")
+P = 0xFFFFFFFF00000001
+
+STATUS = {0: "ROSETTA_OK", 1: "ROSETTA_ERR_NULL", 2: "ROSETTA_ERR_PARAMS",
+          3: "ROSETTA_ERR_UNSUPPORTED", 4: "ROSETTA_ERR_ALIAS", 5: "ROSETTA_ERR_NOMEM",
+          6: "ROSETTA_ERR_DEVICE", 7: "ROSETTA_ERR_SIZE"}
+
+
+class RosettaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class Params(C.Structure):
+    """rosetta_params (include/rosetta.h)."""
+
+    _fields_ = [(name, C.c_uint32) for name in
+                ("n", "k", "N", "pbs_level", "pbs_base_log", "ks_level", "ks_base_log",
+                 "msg_bits")]
+
+    @classmethod
+    def from_dict(cls, d: dict) -> "Params":
+        d = dict(d)
+        d.setdefault("k", 1)
+        return cls(**d)
+
+    @property
+    def M(self) -> int:
+        return 1 << self.msg_bits
+
+
+# Every symbol the header declares, with its ctypes signature.
+_u64p = C.c_void_p
+_pp = C.POINTER(Params)
+_ST = C.c_int
+SIGNATURES = {
+    "rosetta_version": (C.c_char_p, []),
+    "rosetta_status_string": (C.c_char_p, [C.c_int]),
+    "rosetta_last_error": (C.c_char_p, []),
+    "rosetta_check_params": (_ST, [_pp]),
+    "rosetta_bsk_words": (C.c_size_t, [_pp]),
+    "rosetta_ksk_words": (C.c_size_t, [_pp]),
+    "rosetta_ksk_device_words": (C.c_size_t, [_pp]),
+    "rosetta_bsk_prepare": (_ST, [_u64p, _u64p, _pp, C.c_void_p]),
+    "rosetta_ksk_prepare": (_ST, [_u64p, _u64p, _pp, C.c_void_p]),
+    "rosetta_pbs_batch": (_ST, [_u64p, _u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp,
+                                C.c_void_p]),
+    "rosetta_pbs_workspace_bytes": (C.c_size_t, [_pp, C.c_size_t]),
+    "rosetta_pbs_batch_ws": (_ST, [_u64p, _u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp,
+                                   C.c_void_p, C.c_size_t, C.c_void_p]),
+    "rosetta_blind_rotate": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp, C.c_void_p]),
+    "rosetta_blind_rotate_extract": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp,
+                                           C.c_void_p]),
+    "rosetta_keyswitch": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, _pp, C.c_void_p]),
+    "rosetta_ntt_forward": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
+    "rosetta_ntt_inverse": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
+    "rosetta_poly_mul": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
+    "rosetta_keygen": (_ST, [C.c_uint64, _pp, C.c_double, C.c_double, _u64p, _u64p, _u64p,
+                             _u64p]),
+    "rosetta_lwe_encrypt": (_ST, [C.c_uint64, _pp, C.c_double, _u64p, C.c_uint32, _u64p,
+                                  C.c_size_t, _u64p]),
+    "rosetta_lwe_decrypt": (_ST, [_pp, _u64p, C.c_uint32, _u64p, C.c_size_t, _u64p]),
+    "rosetta_lut_build": (_ST, [_pp, _u64p, _u64p]),
+    "rosetta_shutdown": (_ST, []),
+}
+
+_lib = None
+
+
+def lib():
+    """Load librosetta.so (built in-tree by paper_2609_16915_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run "
+                               "`python -m paper_2609_16915_amd.build` first")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise RosettaError(status, lib().rosetta_last_error().decode())
+
+
+def _params(p) -> Params:
+    return p if isinstance(p, Params) else Params.from_dict(p)
+
+
+# --------------------------------------------------------------------------
+# device buffers (torch)
+# --------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dev(t, name: str) -> int:
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a torch tensor on a ROCm device")
+    if t.element_size() != 8 or not t.is_contiguous():
+        raise TypeError(f"{name} must be contiguous with 64-bit elements")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def empty(words, device="cuda"):
+    torch = _torch()
+    return torch.empty(words, dtype=torch.uint64, device=device)
+
+
+def to_device(a: np.ndarray, device="cuda"):
+    torch = _torch()
+    a = np.ascontiguousarray(a, dtype=np.uint64)
+    return torch.from_numpy(a).to(device)
+
+
+def to_host(t) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint64)
+
+
+def bsk_words(params) -> int:
+    return lib().rosetta_bsk_words(C.byref(_params(params)))
+
+
+def ksk_words(params) -> int:
+    return lib().rosetta_ksk_words(C.byref(_params(params)))
+
+
+def ksk_device_words(params) -> int:
+    return lib().rosetta_ksk_device_words(C.byref(_params(params)))
+
+
+def check_params(params):
+    _check(lib().rosetta_check_params(C.byref(_params(params))))
+
+
+def bsk_prepare(bsk_std, params, out=None, stream=None):
+    p = _params(params)
+    if out is None:
+        out = empty(bsk_words(p), bsk_std.device)
+    _check(lib().rosetta_bsk_prepare(_dev(bsk_std, "bsk_std"), _dev(out, "bsk_dev"), C.byref(p),
+                                     _stream(stream)))
+    return out
+
+
+def ksk_prepare(ksk_std, params, out=None, stream=None):
+    p = _params(params)
+    if out is None:
+        out = empty(ksk_device_words(p), ksk_std.device)
+    _check(lib().rosetta_ksk_prepare(_dev(ksk_std, "ksk_std"), _dev(out, "ksk_dev"), C.byref(p),
+                                     _stream(stream)))
+    return out
+
+
+def pbs_batch(lwe_in, bsk_dev, ksk_dev, lut, params, out=None, stream=None):
+    p = _params(params)
+    batch = lwe_in.numel() // (p.n + 1)
+    if out is None:
+        out = empty((batch, p.n + 1), lwe_in.device)
+    _check(lib().rosetta_pbs_batch(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
+                                   _dev(ksk_dev, "ksk_dev"), _dev(lut, "lut"),
+                                   _dev(out, "lwe_out"), batch, C.byref(p), _stream(stream)))
+    return out
+
+
+def pbs_workspace_bytes(params, batch: int) -> int:
+    return lib().rosetta_pbs_workspace_bytes(C.byref(_params(params)), batch)
+
+
+def pbs_batch_ws(lwe_in, bsk_dev, ksk_dev, lut, params, workspace, out=None, stream=None):
+    p = _params(params)
+    batch = lwe_in.numel() // (p.n + 1)
+    if out is None:
+        out = empty((batch, p.n + 1), lwe_in.device)
+    _check(lib().rosetta_pbs_batch_ws(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
+                                      _dev(ksk_dev, "ksk_dev"), _dev(lut, "lut"),
+                                      _dev(out, "lwe_out"), batch, C.byref(p),
+                                      _dev(workspace, "workspace"),
+                                      workspace.numel() * workspace.element_size(),
+                                      _stream(stream)))
+    return out
+
+
+def blind_rotate(lwe_in, bsk_dev, lut, params, out=None, stream=None):
+    p = _params(params)
+    batch = lwe_in.numel() // (p.n + 1)
+    if out is None:
+        out = empty((batch, 2 * p.N), lwe_in.device)
+    _check(lib().rosetta_blind_rotate(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
+                                      _dev(lut, "lut"), _dev(out, "glwe_out"), batch, C.byref(p),
+                                      _stream(stream)))
+    return out
+
+
+def blind_rotate_extract(lwe_in, bsk_dev, lut, params, out=None, stream=None):
+    p = _params(params)
+    batch = lwe_in.numel() // (p.n + 1)
+    if out is None:
+        out = empty((batch, p.N + 1), lwe_in.device)
+    _check(lib().rosetta_blind_rotate_extract(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
+                                              _dev(lut, "lut"), _dev(out, "big_out"), batch,
+                                              C.byref(p), _stream(stream)))
+    return out
+
+
+def keyswitch(big_in, ksk_dev, params, out=None, stream=None):
+    p = _params(params)
+    batch = big_in.numel() // (p.N + 1)
+    if out is None:
+        out = empty((batch, p.n + 1), big_in.device)
+    _check(lib().rosetta_keyswitch(_dev(big_in, "big_in"), _dev(ksk_dev, "ksk_dev"),
+                                   _dev(out, "lwe_out"), batch, C.byref(p), _stream(stream)))
+    return out
+
+
+def ntt_forward(x, N: int, out=None, stream=None):
+    count = x.numel() // N
+    out = empty(x.shape, x.device) if out is None else out
+    _check(lib().rosetta_ntt_forward(_dev(x, "in"), _dev(out, "out"), count, N, _stream(stream)))
+    return out
+
+
+def ntt_inverse(x, N: int, out=None, stream=None):
+    count = x.numel() // N
+    out = empty(x.shape, x.device) if out is None else out
+    _check(lib().rosetta_ntt_inverse(_dev(x, "in"), _dev(out, "out"), count, N, _stream(stream)))
+    return out
+
+
+def poly_mul(a, b, N: int, out=None, stream=None):
+    count = a.numel() // N
+    out = empty(a.shape, a.device) if out is None else out
+    _check(lib().rosetta_poly_mul(_dev(a, "a"), _dev(b, "b"), _dev(out, "c"), count, N,
+                                  _stream(stream)))
+    return out
+
+
+def shutdown():
+    _check(lib().rosetta_shutdown())
+
+
+# --------------------------------------------------------------------------
+# host helpers (numpy)
+# --------------------------------------------------------------------------
+
+def _np_ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+def keygen(seed: int, params, sigma_lwe: float, sigma_glwe: float) -> dict:
+    p = _params(params)
+    keys = dict(lwe_key=np.zeros(p.n, np.uint64), glwe_key=np.zeros(p.N, np.uint64),
+                bsk=np.zeros(bsk_words(p), np.uint64), ksk=np.zeros(ksk_words(p), np.uint64))
+    _check(lib().rosetta_keygen(seed, C.byref(p), sigma_lwe, sigma_glwe,
+                                _np_ptr(keys["lwe_key"]), _np_ptr(keys["glwe_key"]),
+                                _np_ptr(keys["bsk"]), _np_ptr(keys["ksk"])))
+    return keys
+
+
+def lwe_encrypt(seed: int, params, sigma: float, key: np.ndarray, msgs) -> np.ndarray:
+    p = _params(params)
+    key = np.ascontiguousarray(key, np.uint64)
+    msgs = np.ascontiguousarray(msgs, np.uint32)
+    dim = key.shape[0]
+    out = np.zeros((msgs.shape[0], dim + 1), np.uint64)
+    _check(lib().rosetta_lwe_encrypt(seed, C.byref(p), sigma, _np_ptr(key), dim, _np_ptr(msgs),
+                                     msgs.shape[0], _np_ptr(out)))
+    return out
+
+
+def lwe_decrypt(params, key: np.ndarray, cts: np.ndarray) -> np.ndarray:
+    p = _params(params)
+    key = np.ascontiguousarray(key, np.uint64)
+    dim = key.shape[0]
+    cts = np.ascontiguousarray(cts, np.uint64).reshape(-1, dim + 1)
+    out = np.zeros(cts.shape[0], np.uint32)
+    _check(lib().rosetta_lwe_decrypt(C.byref(p), _np_ptr(key), dim, _np_ptr(cts), cts.shape[0],
+                                     _np_ptr(out)))
+    return out
+
+
+def lut_build(params, table) -> np.ndarray:
+    p = _params(params)
+    table = np.ascontiguousarray(table, np.uint32)
+    if table.shape[0] != p.M:
+        raise ValueError(f"table must have {p.M} entries")
+    v = np.zeros(p.N, np.uint64)
+    _check(lib().rosetta_lut_build(C.byref(p), _np_ptr(table), _np_ptr(v)))
+    return v

@@ -1,0 +1,207 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle,
+element by element, on the same seeded inputs.  Integer work, so the bar is
+bit-exact everywhere.
+
+Small cases cover several tiles and ragged tails; the full-size cases run the
+whole batch of each workload in the launch configuration the benchmark times
+and compare a seeded sample of ciphertexts (first, last and random picks)
+against the oracle computed one by one, plus decryption properties that hold
+at any size."""
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2609_16915_amd import rosetta as R
+from paper_2609_16915_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+P = 0xFFFFFFFF00000001
+
+
+def say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+@pytest.fixture(scope="session")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    R.lib()
+    return torch
+
+
+def bitrev(x, bits):
+    return int(format(x, f"0{bits}b")[::-1], 2)
+
+
+def oparams(O, w):
+    return O.Params.make(**{k: v for k, v in w.params().items() if k != "k"})
+
+
+_keys = {}
+
+
+def keyset(O, name):
+    """Oracle key material and prepared device keys for a workload."""
+    if name not in _keys:
+        w = W.get(name)
+        op = oparams(O, w)
+        say(f"[keys] oracle keygen {name} n={w.n} N={w.N}")
+        ks = O.KeySet(op, w.key_seed, w.sigma_lwe, w.sigma_glwe)
+        bsk_std = R.to_device(ks.bsk)
+        ksk_std = R.to_device(ks.ksk)
+        bsk = R.bsk_prepare(bsk_std, w.params())
+        ksk = R.ksk_prepare(ksk_std, w.params())
+        del bsk_std, ksk_std
+        _keys[name] = (w, op, ks, bsk, ksk)
+    return _keys[name]
+
+
+# ------------------------------------------------------------ transforms ---
+
+@pytest.mark.parametrize("N", [256, 512, 1024, 2048, 4096])
+def test_ntt_forward_inverse_vs_oracle(O, torch_dev, N):
+    rng = np.random.default_rng(N)
+    count = 5
+    a = rng.integers(0, P, size=(count, N), dtype=np.uint64)
+    fwd = R.to_host(R.ntt_forward(R.to_device(a), N))
+    L = N.bit_length() - 1
+    perm = np.array([bitrev(j, L) for j in range(N)])
+    for c in range(count):
+        ref = O.ntt_forward(a[c])                 # natural order, A_k = a(psi^(2k+1))
+        assert np.array_equal(fwd[c], ref[perm])  # library order: A_rev(j)
+    back = R.to_host(R.ntt_inverse(R.to_device(fwd), N))
+    assert np.array_equal(back, a)
+    # in place
+    t = R.to_device(a)
+    R.ntt_forward(t, N, out=t)
+    assert np.array_equal(R.to_host(t), fwd)
+
+
+@pytest.mark.parametrize("N", [256, 512, 2048, 4096])
+def test_poly_mul_vs_oracle(O, torch_dev, N):
+    rng = np.random.default_rng(100 + N)
+    count = 3
+    a = rng.integers(0, P, size=(count, N), dtype=np.uint64)
+    b = rng.integers(0, P, size=(count, N), dtype=np.uint64)
+    c = R.to_host(R.poly_mul(R.to_device(a), R.to_device(b), N))
+    kind = O.SCHOOLBOOK if N <= 512 else O.NTT
+    for i in range(count):
+        assert np.array_equal(c[i], O.polymul(a[i], b[i], kind))
+
+
+# ------------------------------------------------------- tiny, all stages ---
+
+@pytest.mark.parametrize("fn", ["identity", "square_mod"])
+def test_tiny_every_stage_bit_exact(O, torch_dev, fn):
+    w, op, ks, bsk, ksk = keyset(O, "tiny")
+    table = w.table(fn)
+    v = O.test_poly(op, table)
+    msgs = np.array(list(range(w.M)) * 3, dtype=np.uint32)[: 19]   # 19: ragged vs tiles of 16
+    cts = O.lwe_encrypt(op, w.enc_seed, w.sigma_lwe, ks.lwe_key, msgs)
+    o_out, o_big, o_acc = O.pbs(op, cts, ks.bsk, ks.ksk, v, O.SCHOOLBOOK, 0, True, True)
+    d_in, d_v = R.to_device(cts), R.to_device(v)
+    acc = R.to_host(R.blind_rotate(d_in, bsk, d_v, w.params()))
+    assert np.array_equal(acc, o_acc)                                    # a1-a6
+    big = R.blind_rotate_extract(d_in, bsk, d_v, w.params())
+    assert np.array_equal(R.to_host(big), o_big)                         # a7
+    assert np.array_equal(R.to_host(R.keyswitch(big, ksk, w.params())), o_out)   # a8
+    out = R.to_host(R.pbs_batch(d_in, bsk, ksk, d_v, w.params()))
+    assert np.array_equal(out, o_out)                                    # a1-a8
+    assert np.array_equal(O.lwe_decrypt(op, ks.lwe_key, out), table[msgs])
+
+
+def test_trivial_ciphertext_closed_form(O, torch_dev):
+    w, op, ks, bsk, ksk = keyset(O, "tiny")
+    N = w.N
+    v = O.test_poly(op, w.table("square_mod"))
+    bs = [0, 1, P - 1, P // 2, 12345678901234567]
+    cts = np.zeros((len(bs), w.n + 1), dtype=np.uint64)
+    cts[:, w.n] = bs
+    acc = R.to_host(R.blind_rotate(R.to_device(cts), bsk, R.to_device(v), w.params()))
+    for q, b in enumerate(bs):
+        bt = O.modswitch(b, N)
+        assert np.all(acc[q, :N] == 0)
+        assert np.array_equal(acc[q, N:], O.monomial_mul(v, (2 * N - bt) % (2 * N)))
+
+
+@pytest.mark.parametrize("batch", [1, 2, 15, 16, 17, 33])
+def test_ragged_batches_and_in_place(O, torch_dev, batch):
+    w, op, ks, bsk, ksk = keyset(O, "tiny")
+    v = O.test_poly(op, w.table("identity"))
+    msgs = (np.arange(batch) * 5 % w.M).astype(np.uint32)
+    cts = O.lwe_encrypt(op, 7 + batch, w.sigma_lwe, ks.lwe_key, msgs)
+    ref = O.pbs(op, cts, ks.bsk, ks.ksk, v, O.NTT)
+    t = R.to_device(cts)
+    R.pbs_batch(t, bsk, ksk, R.to_device(v), w.params(), out=t)         # in place
+    assert np.array_equal(R.to_host(t), ref)
+
+
+def test_caller_workspace_and_empty_batch(O, torch_dev):
+    w, op, ks, bsk, ksk = keyset(O, "tiny")
+    v = R.to_device(O.test_poly(op, w.table("identity")))
+    cts = O.lwe_encrypt(op, 3, w.sigma_lwe, ks.lwe_key, np.arange(8, dtype=np.uint32))
+    ref = O.pbs(op, cts, ks.bsk, ks.ksk, O.test_poly(op, w.table("identity")), O.NTT)
+    ws = R.empty(R.pbs_workspace_bytes(w.params(), 8) // 8)
+    out = R.pbs_batch_ws(R.to_device(cts), bsk, ksk, v, w.params(), ws)
+    assert np.array_equal(R.to_host(out), ref)
+    empty_in = R.empty((0, w.n + 1))
+    assert R.pbs_batch(empty_in, bsk, ksk, v, w.params()).shape[0] == 0
+
+
+def test_library_keys_give_same_result(O, torch_dev):
+    """Keys from the library's own generator are bit-identical to the
+    oracle's, so the PBS on them is too."""
+    w, op, ks, bsk, ksk = keyset(O, "tiny")
+    lk = R.keygen(w.key_seed, w.params(), w.sigma_lwe, w.sigma_glwe)
+    bsk2 = R.bsk_prepare(R.to_device(lk["bsk"]), w.params())
+    assert np.array_equal(R.to_host(bsk2), R.to_host(bsk))
+
+
+# ------------------------------------------------- workloads, full size ---
+
+FULL = ["gpt2_gelu", "tinyllama_silu", "llama3_8b_silu", "llama3_8b_softmax_exp",
+        "llama3_8b_softmax_recip"]
+# decryption of the key-switched output recovers T[m] except for the
+# noise-induced misses these parameter sets have (the two largest
+# parameter sets drift by a visible fraction of a box)
+MIN_DECRYPT_RATE = {"gpt2_gelu": 0.999, "tinyllama_silu": 0.999, "llama3_8b_silu": 0.85,
+                    "llama3_8b_softmax_exp": 0.40, "llama3_8b_softmax_recip": 0.40}
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_workload_sampled_parity(O, torch_dev, name):
+    torch = torch_dev
+    w, op, ks, bsk, ksk = keyset(O, name)
+    msgs = w.messages()
+    say(f"[{name}] encrypt batch {w.batch}")
+    cts = O.lwe_encrypt(op, w.enc_seed, w.sigma_lwe, ks.lwe_key, msgs)
+    table = w.table()
+    v = O.test_poly(op, table)
+    d_in, d_v = R.to_device(cts), R.to_device(v)
+    say(f"[{name}] GPU PBS of {w.batch}")
+    out = R.pbs_batch(d_in, bsk, ksk, d_v, w.params())
+    torch.cuda.synchronize()
+    out = R.to_host(out)
+    rng = np.random.default_rng(w.data_seed)
+    picks = sorted({0, w.batch - 1, *rng.choice(w.batch, size=min(6, w.batch), replace=False)})
+    say(f"[{name}] oracle on {len(picks)} sampled ciphertexts")
+    ref_out, ref_big = O.pbs(op, cts[picks], ks.bsk, ks.ksk, v, O.NTT, 0, want_big=True)
+    assert np.array_equal(out[picks], ref_out)
+    big = R.to_host(R.blind_rotate_extract(R.to_device(cts[picks]), bsk, d_v, w.params()))
+    assert np.array_equal(big, ref_big)
+    # properties over the whole batch
+    assert np.all(out < np.uint64(P))
+    rate = np.mean(O.lwe_decrypt(op, ks.lwe_key, out) == table[msgs])
+    say(f"[{name}] decrypt(PBS(Enc m)) = T[m] on {rate:.4%} of {w.batch}")
+    assert rate >= MIN_DECRYPT_RATE[name]
+
+
+def test_determinism(O, torch_dev):
+    w, op, ks, bsk, ksk = keyset(O, "gpt2_gelu")
+    cts = O.lwe_encrypt(op, 5, w.sigma_lwe, ks.lwe_key, w.messages(512, seed=9))
+    d_in, d_v = R.to_device(cts), R.to_device(O.test_poly(op, w.table()))
+    a = R.to_host(R.pbs_batch(d_in, bsk, ksk, d_v, w.params()))
+    b = R.to_host(R.pbs_batch(d_in, bsk, ksk, d_v, w.params()))
+    assert np.array_equal(a, b)
