@@ -69,6 +69,11 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 = skip)")
+    ap.add_argument("--batch", type=int, default=None,
+                    help="override the workload's batch (experiments only)")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="also run one plain device copy of this many MiB, outside the timed "
+                         "region, as the reference kernel for memory-traffic counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); batched PBS shards "
@@ -82,6 +87,9 @@ def main():
 
     name = args.workload or W.HEADLINE
     w = W.get(name)
+    if args.batch:
+        import dataclasses
+        w = dataclasses.replace(w, batch=args.batch)
     p = R.Params.from_dict(w.params())
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
@@ -104,6 +112,14 @@ def main():
     def step():
         R.blind_rotate_extract(d_in, bsk, d_v, p, out=big)
         R.keyswitch(big, ksk, p, out=d_out)
+
+    if args.calibrate_copy_mib:
+        words = args.calibrate_copy_mib * (1 << 20) // 8
+        src = torch.zeros(words, dtype=torch.int64, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):

@@ -96,7 +96,6 @@ bool any_overlap(const void *a, size_t na, const void *b, size_t nb) {
 
 struct DevTables {
   uint64_t *zeta = nullptr;
-  uint64_t *zeta_inv = nullptr;
   uint64_t ninv = 0;
 };
 
@@ -126,33 +125,20 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
   if (it == ds.tables.end()) {
     const int logn = ilog2u(N);
     const u64 psi = gl_pow(7, (GL_P - 1) / (2 * (u64)N));
-    std::vector<u64> z(N), zi(N);
-    for (uint32_t m = 0; m < N; ++m) {
-      const uint32_t r = bitrev(m, logn);
-      z[m] = gl_pow(psi, r);
-      zi[m] = gl_pow(psi, (2 * (u64)N - r) % (2 * (u64)N));
-    }
+    std::vector<u64> z(N);
+    for (uint32_t m = 0; m < N; ++m) z[m] = gl_pow(psi, bitrev(m, logn));
     DevTables t;
     e = hipMalloc(&t.zeta, N * sizeof(u64));
     if (e != hipSuccess) return hip_fail(e, "hipMalloc(twiddles)");
-    e = hipMalloc(&t.zeta_inv, N * sizeof(u64));
-    if (e != hipSuccess) {
-      (void)hipFree(t.zeta);
-      return hip_fail(e, "hipMalloc(twiddles)");
-    }
     e = hipMemcpy(t.zeta, z.data(), N * sizeof(u64), hipMemcpyHostToDevice);
-    if (e == hipSuccess)
-      e = hipMemcpy(t.zeta_inv, zi.data(), N * sizeof(u64), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       (void)hipFree(t.zeta);
-      (void)hipFree(t.zeta_inv);
       return hip_fail(e, "hipMemcpy(twiddles)");
     }
     t.ninv = gl_inv(N);
     it = ds.tables.emplace(N, t).first;
   }
   out.zeta = it->second.zeta;
-  out.zeta_inv = it->second.zeta_inv;
   out.ninv = it->second.ninv;
   return ROSETTA_OK;
 }
@@ -417,10 +403,7 @@ rosetta_status rosetta_shutdown(void) {
   for (auto &kv : g_dev) {
     (void)hipSetDevice(kv.first);
     (void)hipDeviceSynchronize();
-    for (auto &t : kv.second.tables) {
-      (void)hipFree(t.second.zeta);
-      (void)hipFree(t.second.zeta_inv);
-    }
+    for (auto &t : kv.second.tables) (void)hipFree(t.second.zeta);
     if (kv.second.workspace) (void)hipFree(kv.second.workspace);
   }
   g_dev.clear();

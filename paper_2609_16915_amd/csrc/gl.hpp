@@ -3,8 +3,8 @@
 // 2^64 = 2^32 - 1 (mod p), so a 128-bit value hi*2^64 + lo with
 // hi = h1*2^32 + h0 reduces to lo - h1 + h0*(2^32 - 1)  (since 2^96 = -1).
 // All functions take and return canonical values in [0, p).  The 64x64
-// product is built from four 32x32->64 multiply-adds (v_mad_u64_u32 on
-// CDNA), arranged so that no intermediate overflows 64 bits.
+// product is built from the low and high halves of four 32x32 products,
+// which gfx950 issues at full rate (v_mad_u64_u32 runs at half rate).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -20,47 +20,109 @@ typedef int64_t i64;
 constexpr u64 GL_P = 0xFFFFFFFF00000001ull;
 constexpr u64 GL_EPS = 0xFFFFFFFFull;  // 2^64 mod p
 
+__host__ __device__ __forceinline__ u64 gl_mk(u32 lo, u32 hi) { return ((u64)hi << 32) | lo; }
+
+// All arithmetic below is written on 32-bit limbs with explicit carry
+// chains (v_add_co / v_addc / v_sub_co / v_subb on CDNA) and branch-free
+// selects.  Two facts keep the corrections cheap:
+//   s - p == s + EPS (mod 2^64), so "wrapped past 2^64" and "s >= p" are
+//   both fixed by adding EPS;  and  d + p == d - EPS (mod 2^64).
+
+// (a + b) mod p for canonical a, b.
 __host__ __device__ __forceinline__ u64 gl_add(u64 a, u64 b) {
-  u64 s = a + b;
-  if (s < a) return s + GL_EPS;  // wrapped: a + b - 2^64 + (2^64 mod p), < p
-  return s >= GL_P ? s - GL_P : s;
+  u32 c1, c2;
+  const u32 s0 = __builtin_addc((u32)a, (u32)b, 0u, &c1);
+  const u32 s1 = __builtin_addc((u32)(a >> 32), (u32)(b >> 32), c1, &c1);
+  const u32 t0 = __builtin_addc(s0, 0xFFFFFFFFu, 0u, &c2);  // s + EPS, carry iff s >= p
+  const u32 t1 = __builtin_addc(s1, 0u, c2, &c2);
+  return (c1 | c2) ? gl_mk(t0, t1) : gl_mk(s0, s1);
 }
 
+// (a - b) mod p for canonical a, b.
 __host__ __device__ __forceinline__ u64 gl_sub(u64 a, u64 b) {
-  u64 d = a - b;
-  if (a < b) d -= GL_EPS;  // a - b + 2^64 - (2^64 - p)
-  return d;
+  u32 b1, b2;
+  const u32 d0 = __builtin_subc((u32)a, (u32)b, 0u, &b1);
+  const u32 d1 = __builtin_subc((u32)(a >> 32), (u32)(b >> 32), b1, &b1);
+  const u32 t0 = __builtin_subc(d0, 0xFFFFFFFFu, 0u, &b2);  // d - EPS = d + p
+  const u32 t1 = __builtin_subc(d1, 0u, b2, &b2);
+  return b1 ? gl_mk(t0, t1) : gl_mk(d0, d1);
 }
 
 __host__ __device__ __forceinline__ u64 gl_neg(u64 a) { return a ? GL_P - a : 0; }
 
-// Full 128-bit product a*b = hi*2^64 + lo.
-__host__ __device__ __forceinline__ void mul_wide(u64 a, u64 b, u64 &lo, u64 &hi) {
+// 128-bit product a*b as 32-bit limbs c0..c3 (c0 least significant): four
+// 32x32 products, low and high halves (v_mul_lo_u32 / v_mul_hi_u32, both
+// full rate on gfx950), summed with carries.
+__host__ __device__ __forceinline__ void gl_mul_limbs(u64 a, u64 b, u32 &c0, u32 &c1, u32 &c2,
+                                                      u32 &c3) {
   const u32 a0 = (u32)a, a1 = (u32)(a >> 32), b0 = (u32)b, b1 = (u32)(b >> 32);
-  const u64 p00 = (u64)a0 * b0;
-  const u64 t = (u64)a0 * b1 + (p00 >> 32);  // <= (2^32-1)^2 + 2^32-1 < 2^64
-  const u64 u = (u64)a1 * b0 + (u32)t;
-  u64 w = (u64)a1 * b1 + (t >> 32);
-  w += (u >> 32);  // a1 b1 + 2 (2^32-1) <= 2^64 - 1
-  lo = (p00 & 0xFFFFFFFFull) | (u << 32);
-  hi = w;
+  c0 = a0 * b0;
+  const u32 x = (u32)(((u64)a0 * b0) >> 32);
+  const u32 yl = a0 * b1, yh = (u32)(((u64)a0 * b1) >> 32);
+  const u32 zl = a1 * b0, zh = (u32)(((u64)a1 * b0) >> 32);
+  const u32 wl = a1 * b1, wh = (u32)(((u64)a1 * b1) >> 32);
+  u32 k1, k2, k3, k4;
+  c1 = __builtin_addc(x, yl, 0u, &k1);
+  c1 = __builtin_addc(c1, zl, 0u, &k2);
+  c2 = __builtin_addc(yh, zh, k1, &k3);
+  c2 = __builtin_addc(c2, wl, k2, &k4);
+  c3 = wh + k3 + k4;
+}
+
+// c0 + c1 2^32 + c2 2^64 + c3 2^96  mod p
+//   = (c1:c0) - c3 + c2 (2^32 - 1)          (2^64 = 2^32 - 1, 2^96 = -1)
+__host__ __device__ __forceinline__ u64 gl_reduce_limbs(u32 c0, u32 c1, u32 c2, u32 c3) {
+  u32 e1, e2;
+  u32 t0 = __builtin_subc(c0, c3, 0u, &e1);           // t = (c1:c0) - c3
+  u32 t1 = __builtin_subc(c1, 0u, e1, &e1);
+  const u32 adj = e1 ? 0xFFFFFFFFu : 0u;               // borrow: t + p = t - EPS
+  t0 = __builtin_subc(t0, adj, 0u, &e2);
+  t1 = __builtin_subc(t1, 0u, e2, &e2);
+  u32 bb;
+  const u32 v0 = __builtin_subc(0u, c2, 0u, &bb);      // v = c2 * EPS = (c2 << 32) - c2
+  const u32 v1 = c2 - bb;
+  u32 ca, cb;
+  const u32 r0 = __builtin_addc(t0, v0, 0u, &ca);      // r = t + v
+  const u32 r1 = __builtin_addc(t1, v1, ca, &ca);
+  const u32 s0 = __builtin_addc(r0, 0xFFFFFFFFu, 0u, &cb);
+  const u32 s1 = __builtin_addc(r1, 0u, cb, &cb);
+  return (ca | cb) ? gl_mk(s0, s1) : gl_mk(r0, r1);
 }
 
 // (hi*2^64 + lo) mod p for any 128-bit value.
 __host__ __device__ __forceinline__ u64 gl_reduce128(u64 lo, u64 hi) {
-  const u32 h0 = (u32)hi, h1 = (u32)(hi >> 32);
-  u64 t0 = lo - h1;
-  if (lo < h1) t0 -= GL_EPS;                      // borrow: add p
-  const u64 t1 = ((u64)h0 << 32) - (u64)h0;       // h0 * (2^32 - 1) < p
-  u64 r = t0 + t1;
-  if (r < t1) r += GL_EPS;                        // wrapped
-  return r >= GL_P ? r - GL_P : r;
+  return gl_reduce_limbs((u32)lo, (u32)(lo >> 32), (u32)hi, (u32)(hi >> 32));
 }
 
 __host__ __device__ __forceinline__ u64 gl_mul(u64 a, u64 b) {
-  u64 lo, hi;
-  mul_wide(a, b, lo, hi);
-  return gl_reduce128(lo, hi);
+  u32 c0, c1, c2, c3;
+  gl_mul_limbs(a, b, c0, c1, c2, c3);
+  return gl_reduce_limbs(c0, c1, c2, c3);
+}
+
+// x * 2^E mod p for a compile-time 0 <= E < 96 (2^96 = -1 covers the rest):
+// the product is a shifted copy of x's limbs, reduced like any product.
+template <int E>
+__host__ __device__ __forceinline__ u64 gl_mul_pow2(u64 x) {
+  static_assert(E >= 0 && E < 96, "exponent out of range");
+  const u32 x0 = (u32)x, x1 = (u32)(x >> 32);
+  if constexpr (E == 0) {
+    return x;
+  } else if constexpr (E < 32) {
+    return gl_reduce_limbs(x0 << E, (x1 << E) | (x0 >> (32 - E)), x1 >> (32 - E), 0u);
+  } else if constexpr (E == 32) {
+    return gl_reduce_limbs(0u, x0, x1, 0u);
+  } else if constexpr (E < 64) {
+    constexpr int f = E - 32;
+    return gl_reduce_limbs(0u, x0 << f, (x1 << f) | (x0 >> (32 - f)), x1 >> (32 - f));
+  } else if constexpr (E == 64) {
+    return gl_reduce_limbs(0u, 0u, x0, x1);
+  } else {
+    constexpr int f = E - 64;
+    const u32 c4 = x1 >> (32 - f);  // weight 2^128 = -2^32 (mod p)
+    return gl_sub(gl_reduce_limbs(0u, 0u, x0 << f, (x1 << f) | (x0 >> (32 - f))),
+                  (u64)c4 << 32);
+  }
 }
 
 __host__ __device__ inline u64 gl_pow(u64 a, u64 e) {

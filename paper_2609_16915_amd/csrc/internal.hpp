@@ -17,8 +17,7 @@ constexpr uint32_t MAX_LWE_N = 2048;
 
 // Per-device, per-N transform tables (device pointers) and N^-1.
 struct Tables {
-  const uint64_t *zeta;      // [N]: zeta[m] = psi^rev(m), m >= 1
-  const uint64_t *zeta_inv;  // [N]: psi^-rev(m)
+  const uint64_t *zeta;  // [N]: zeta[m] = psi^rev(m), m >= 1 (zeta[0] = 1)
   uint64_t ninv;
 };
 

@@ -19,6 +19,15 @@ namespace rosetta {
 // Key preparation
 // ---------------------------------------------------------------------------
 
+// Dynamic LDS of the transform kernels: the N-word twiddle table, then two
+// N-word transpose buffers.
+extern __shared__ __align__(16) u64 lds_dyn[];
+
+template <class S>
+constexpr size_t ntt_lds_bytes() {
+  return (size_t)3 * S::N * sizeof(u64);
+}
+
 // Row r of the standard key (N coefficients) -> transform domain, scaled by
 // N^-1, stored as [r][k][tid] so that thread tid of the blind rotation
 // reads its E words of the row with unit stride across the workgroup.
@@ -26,14 +35,16 @@ template <class S>
 __global__ void __launch_bounds__(S::T)
 k_bsk_prepare(const u64 *__restrict__ std_key, u64 *__restrict__ dev_key,
               const u64 *__restrict__ zeta, u64 ninv) {
-  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
-  LdsPair lds(lds_mem, S::LDS_WORDS);
+  u64 *tw = lds_dyn;
+  LdsPair lds(lds_dyn + S::N, S::N);
   const int tid = threadIdx.x;
   const size_t row = blockIdx.x;
+  load_twiddles<S>(tw, zeta, tid);
   u64 x[S::E];
 #pragma unroll
   for (int k = 0; k < S::E; ++k) x[k] = std_key[row * S::N + tid + S::T * k];
-  ntt_forward<S>(x, lds, tid, as_global(zeta));
+  __syncthreads();
+  ntt_forward<S>(x, lds, tid, tw);
 #pragma unroll
   for (int k = 0; k < S::E; ++k) dev_key[row * S::N + k * S::T + tid] = gl_mul(x[k], ninv);
 }
@@ -57,52 +68,57 @@ __global__ void k_ksk_colsum(const u64 *__restrict__ ksk, u64 *__restrict__ out,
 template <class S>
 __global__ void __launch_bounds__(S::T)
 k_ntt_forward(const u64 *in, u64 *out, const u64 *__restrict__ zeta) {
-  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
-  LdsPair lds(lds_mem, S::LDS_WORDS);
+  u64 *tw = lds_dyn;
+  LdsPair lds(lds_dyn + S::N, S::N);
   const int tid = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * S::N;
+  load_twiddles<S>(tw, zeta, tid);
   u64 x[S::E];
 #pragma unroll
   for (int k = 0; k < S::E; ++k) x[k] = in[base + tid + S::T * k];
-  ntt_forward<S>(x, lds, tid, as_global(zeta));
+  __syncthreads();
+  ntt_forward<S>(x, lds, tid, tw);
 #pragma unroll
   for (int k = 0; k < S::E; ++k) out[base + S::idx(S::PASSES - 1, tid, k)] = x[k];
 }
 
 template <class S>
 __global__ void __launch_bounds__(S::T)
-k_ntt_inverse(const u64 *in, u64 *out, const u64 *__restrict__ zeta_inv, u64 ninv) {
-  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
-  LdsPair lds(lds_mem, S::LDS_WORDS);
+k_ntt_inverse(const u64 *in, u64 *out, const u64 *__restrict__ zeta, u64 ninv) {
+  u64 *tw = lds_dyn;
+  LdsPair lds(lds_dyn + S::N, S::N);
   const int tid = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * S::N;
+  load_twiddles<S>(tw, zeta, tid);
   u64 x[S::E];
 #pragma unroll
   for (int k = 0; k < S::E; ++k) x[k] = in[base + S::idx(S::PASSES - 1, tid, k)];
-  ntt_inverse<S>(x, lds, tid, as_global(zeta_inv));
+  __syncthreads();
+  ntt_inverse<S>(x, lds, tid, tw);
 #pragma unroll
   for (int k = 0; k < S::E; ++k) out[base + tid + S::T * k] = gl_mul(x[k], ninv);
 }
 
 template <class S>
 __global__ void __launch_bounds__(S::T)
-k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta,
-           const u64 *__restrict__ zeta_inv, u64 ninv) {
-  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
-  LdsPair lds(lds_mem, S::LDS_WORDS);
+k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta, u64 ninv) {
+  u64 *tw = lds_dyn;
+  LdsPair lds(lds_dyn + S::N, S::N);
   const int tid = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * S::N;
+  load_twiddles<S>(tw, zeta, tid);
   u64 x[S::E], y[S::E];
 #pragma unroll
   for (int k = 0; k < S::E; ++k) {
     x[k] = a[base + tid + S::T * k];
     y[k] = b[base + tid + S::T * k];
   }
-  ntt_forward<S>(x, lds, tid, as_global(zeta));
-  ntt_forward<S>(y, lds, tid, as_global(zeta));
+  __syncthreads();
+  ntt_forward<S>(x, lds, tid, tw);
+  ntt_forward<S>(y, lds, tid, tw);
 #pragma unroll
   for (int k = 0; k < S::E; ++k) x[k] = gl_mul(x[k], y[k]);
-  ntt_inverse<S>(x, lds, tid, as_global(zeta_inv));
+  ntt_inverse<S>(x, lds, tid, tw);
 #pragma unroll
   for (int k = 0; k < S::E; ++k) c[base + tid + S::T * k] = gl_mul(x[k], ninv);
 }
@@ -111,9 +127,18 @@ k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta,
 // Blind rotation (+ sample extraction)
 // ---------------------------------------------------------------------------
 
+// Waves per SIMD the blind-rotation kernel is compiled for.  Up to N = 2048
+// three workgroups fit a CU's LDS, so the kernel targets 3 waves per SIMD
+// (<= 168 registers; the few spills touch only the accumulator, read twice
+// per step).  At N = 4096 one 512-thread workgroup fills the LDS and runs
+// 2 waves per SIMD, so it keeps 256 registers.
 #ifndef BR_WAVES_PER_EU
-#define BR_WAVES_PER_EU 2
+#define BR_WAVES_PER_EU 3
 #endif
+template <class S>
+constexpr int br_waves_per_eu() {
+  return S::LOGN >= 12 ? 2 : BR_WAVES_PER_EU;
+}
 
 // Coefficient j of X^r * v (negacyclic), 0 <= r < 2N.
 template <int N>
@@ -148,22 +173,33 @@ __device__ __forceinline__ RT digit_of(RT r, int beta, int t) {
 //   a6  ACC_c += inverse transform of Y_c
 // The transform-domain key rows are pre-scaled by N^-1 (k_bsk_prepare).
 // RT holds the rounded value before digit extraction: 32 bits suffice when
-// l * beta <= 30.
-template <class S, int L, typename RT>
-__global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(BR_WAVES_PER_EU)))
+// l * beta <= 30.  With PF the two key rows of a digit polynomial are loaded
+// into registers before its forward transform, so their latency overlaps
+// the transform.
+//
+// Dynamic LDS: twiddles [N], two transpose buffers [N] each, then the n+1
+// rounded rotation amounts (u16).
+template <class S>
+size_t br_lds_bytes(int n) {
+  return ntt_lds_bytes<S>() + (((size_t)(n + 1) * 2 + 15) & ~(size_t)15);
+}
+
+template <class S, int L, typename RT, bool PF>
+__global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(br_waves_per_eu<S>())))
 k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
                const u64 *__restrict__ lut, u64 *__restrict__ out, int n, int beta, int mode,
-               const u64 *__restrict__ zeta, const u64 *__restrict__ zeta_inv) {
+               const u64 *__restrict__ zeta) {
   constexpr int N = S::N, E = S::E, T = S::T;
-  __shared__ u64 lds_mem[2 * S::LDS_WORDS];
-  __shared__ uint16_t rot[MAX_LWE_N + 1];
-  LdsPair lds(lds_mem, S::LDS_WORDS);
+  u64 *tw = lds_dyn;
+  LdsPair lds(lds_dyn + N, N);
+  uint16_t *rot = (uint16_t *)(lds_dyn + 3 * N);
   const int tid = threadIdx.x;
   const size_t ct = blockIdx.x;
 
-  // a1: rounded rotation amounts of the whole ciphertext
+  // a1: rounded rotation amounts of the whole ciphertext; twiddles
   const u64 *lwe = lwe_in + ct * (size_t)(n + 1);
   for (int i = tid; i <= n; i += T) rot[i] = (uint16_t)gl_modswitch(lwe[i], S::LOGN);
+  load_twiddles<S>(tw, zeta, tid);
   __syncthreads();
 
   u64 accA[E], accB[E];
@@ -179,11 +215,6 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
   const int s = 64 - L * beta;
   constexpr size_t ggsw_words = (size_t)2 * L * 2 * N;
   for (int i = 0; i < n; ++i) {
-    // Opaque copies of the table pointers: without them the compiler hoists
-    // every twiddle load out of the step loop and keeps the values live,
-    // which costs more occupancy than the reloads (cache hits) cost time.
-    const u64 *zf = zeta, *zi = zeta_inv;
-    asm volatile("" : "+s"(zf), "+s"(zi));
     const int a = rot[i];
     const int ar = a & (N - 1);
     const bool flip = a >= N;
@@ -194,7 +225,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
 
 #pragma unroll 1
     for (int u = 0; u < 2; ++u) {
-      // a2: rotate-subtract, then round away the s low bits
+      // a2: rotate-subtract (natural layout), then round away the s low bits
       RT R[E];
       {
         u64 cur[E];
@@ -202,31 +233,53 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
         for (int k = 0; k < E; ++k) cur[k] = u ? accB[k] : accA[k];
         u64 *buf = lds.next();
 #pragma unroll
-        for (int k = 0; k < E; ++k) buf[S::pad(tid) + S::pad(T * k)] = cur[k];
+        for (int k = 0; k < E; ++k) buf[tid + T * k] = cur[k];
         __syncthreads();
 #pragma unroll
         for (int k = 0; k < E; ++k) {
           const int j = tid + T * k;
           const bool neg = (j < ar) != flip;
-          const u64 v = buf[S::pad((j - ar) & (N - 1))];
+          const u64 v = buf[(j - ar) & (N - 1)];
           const u64 d = gl_sub(neg ? gl_neg(v) : v, cur[k]);
           R[k] = (RT)gl_round_top(d, s);
         }
       }
 #pragma unroll 1
       for (int t = 0; t < L; ++t) {
-        // a3: digit polynomial of level t
-        u64 x[E];
-#pragma unroll
-        for (int k = 0; k < E; ++k) x[k] = gl_from_i64((i64)digit_of<L, RT>(R[k], beta, t));
-        // a4: forward transform
-        ntt_forward<S>(x, lds, tid, as_global(zf));
-        // a5: multiply-accumulate with the two rows of GGSW_i[u][t]
         gconst_u64 *g = G + (size_t)((u * L + t) * 2) * N;
+        u64 g0[E], g1[E];
+        if constexpr (PF) {
+#pragma unroll
+          for (int k = 0; k < E; ++k) {
+            g0[k] = g[k * T];
+            g1[k] = g[N + k * T];
+          }
+        }
+        // a3: digit polynomial of level t;  a4: forward transform (its first
+        // stage in integer arithmetic while the digits are small)
+        u64 x[E];
+        if (beta <= 14) {
+          RT d[E];
+#pragma unroll
+          for (int k = 0; k < E; ++k) d[k] = digit_of<L, RT>(R[k], beta, t);
+          ntt_forward_small<S, RT>(d, x, lds, tid, tw);
+        } else {
+#pragma unroll
+          for (int k = 0; k < E; ++k) x[k] = gl_from_i64((i64)digit_of<L, RT>(R[k], beta, t));
+          ntt_forward<S>(x, lds, tid, tw);
+        }
+        // a5: multiply-accumulate with the two rows of GGSW_i[u][t]
+        if constexpr (!PF) {
+#pragma unroll
+          for (int k = 0; k < E; ++k) {
+            g0[k] = g[k * T];
+            g1[k] = g[N + k * T];
+          }
+        }
 #pragma unroll
         for (int k = 0; k < E; ++k) {
-          Y0[k] = gl_add(Y0[k], gl_mul(x[k], g[k * T]));
-          Y1[k] = gl_add(Y1[k], gl_mul(x[k], g[N + k * T]));
+          Y0[k] = gl_add(Y0[k], gl_mul(x[k], g0[k]));
+          Y1[k] = gl_add(Y1[k], gl_mul(x[k], g1[k]));
         }
       }
     }
@@ -237,7 +290,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
       u64 y[E];
 #pragma unroll
       for (int k = 0; k < E; ++k) y[k] = c ? Y1[k] : Y0[k];
-      ntt_inverse<S>(y, lds, tid, as_global(zi));
+      ntt_inverse<S>(y, lds, tid, tw);
 #pragma unroll
       for (int k = 0; k < E; ++k) {
         if (c)
@@ -370,11 +423,28 @@ static int ilog2(uint32_t N) {
   return l;
 }
 
+// Allow a kernel more than the default 64 KiB of dynamic LDS (gfx950 has
+// 160 KiB per workgroup).
+template <typename K>
+static hipError_t allow_lds(K kernel, size_t bytes) {
+  if (bytes <= 65536) return hipSuccess;
+  return hipFuncSetAttribute((const void *)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)bytes);
+}
+
+#define ROSETTA_LAUNCH(KERNEL, GRID, BLOCK, LDS, ST, ...)                         \
+  do {                                                                           \
+    hipError_t e_ = allow_lds(KERNEL, LDS);                                      \
+    if (e_ != hipSuccess) return e_;                                             \
+    hipLaunchKernelGGL(KERNEL, GRID, BLOCK, LDS, ST, __VA_ARGS__);               \
+  } while (0)
+
 hipError_t launch_bsk_prepare(const uint64_t *bsk_std, uint64_t *bsk_dev,
                               const rosetta_params &p, const Tables &tb, hipStream_t st) {
   const size_t rows = (size_t)p.n * 2 * p.pbs_level * 2;
-  ROSETTA_DISPATCH_N(ilog2(p.N), hipLaunchKernelGGL(k_bsk_prepare<S>, dim3(rows), dim3(S::T), 0,
-                                                    st, bsk_std, bsk_dev, tb.zeta, tb.ninv));
+  ROSETTA_DISPATCH_N(ilog2(p.N), ROSETTA_LAUNCH(k_bsk_prepare<S>, dim3(rows), dim3(S::T),
+                                                ntt_lds_bytes<S>(), st, bsk_std, bsk_dev,
+                                                tb.zeta, tb.ninv));
   return hipGetLastError();
 }
 
@@ -391,32 +461,41 @@ hipError_t launch_ksk_prepare(const uint64_t *ksk_std, uint64_t *ksk_dev,
   return hipGetLastError();
 }
 
+#ifndef BR_PREFETCH
+#define BR_PREFETCH 0
+#endif
+
 template <class S, int L>
-static void launch_br_levels(const uint64_t *lwe_in, const uint64_t *bsk_dev, const uint64_t *lut,
-                             uint64_t *out, size_t batch, const rosetta_params &p,
-                             const Tables &tb, int mode, hipStream_t st) {
+static hipError_t launch_br_levels(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                   const uint64_t *lut, uint64_t *out, size_t batch,
+                                   const rosetta_params &p, const Tables &tb, int mode,
+                                   hipStream_t st) {
   const int n = (int)p.n, beta = (int)p.pbs_base_log;
+  const size_t lds = br_lds_bytes<S>(n);
   if (L * beta <= 30)
-    hipLaunchKernelGGL((k_blind_rotate<S, L, int32_t>), dim3(batch), dim3(S::T), 0, st, lwe_in,
-                       bsk_dev, lut, out, n, beta, mode, tb.zeta, tb.zeta_inv);
+    ROSETTA_LAUNCH((k_blind_rotate<S, L, int32_t, BR_PREFETCH>), dim3(batch), dim3(S::T), lds,
+                   st, lwe_in, bsk_dev, lut, out, n, beta, mode, tb.zeta);
   else
-    hipLaunchKernelGGL((k_blind_rotate<S, L, int64_t>), dim3(batch), dim3(S::T), 0, st, lwe_in,
-                       bsk_dev, lut, out, n, beta, mode, tb.zeta, tb.zeta_inv);
+    ROSETTA_LAUNCH((k_blind_rotate<S, L, int64_t, BR_PREFETCH>), dim3(batch), dim3(S::T), lds,
+                   st, lwe_in, bsk_dev, lut, out, n, beta, mode, tb.zeta);
+  return hipSuccess;
 }
 
 hipError_t launch_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
                                const uint64_t *lut, uint64_t *out, size_t batch,
                                const rosetta_params &p, const Tables &tb, BrMode mode,
                                hipStream_t st) {
-#define ROSETTA_BR_L(LV)                                                             \
-  case LV:                                                                           \
-    launch_br_levels<S, LV>(lwe_in, bsk_dev, lut, out, batch, p, tb, (int)mode, st); \
+  hipError_t e = hipSuccess;
+#define ROSETTA_BR_L(LV)                                                                  \
+  case LV:                                                                                \
+    e = launch_br_levels<S, LV>(lwe_in, bsk_dev, lut, out, batch, p, tb, (int)mode, st); \
     break;
   ROSETTA_DISPATCH_N(ilog2(p.N), switch (p.pbs_level) {
     ROSETTA_BR_L(1) ROSETTA_BR_L(2) ROSETTA_BR_L(3) ROSETTA_BR_L(4)
     default: return hipErrorInvalidValue;
   });
 #undef ROSETTA_BR_L
+  if (e != hipSuccess) return e;
   return hipGetLastError();
 }
 
@@ -448,19 +527,21 @@ hipError_t launch_keyswitch(const uint64_t *big, const uint64_t *ksk_dev, uint64
 hipError_t launch_ntt(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,
                       const Tables &tb, bool inverse, hipStream_t st) {
   if (inverse) {
-    ROSETTA_DISPATCH_N(ilog2(N), hipLaunchKernelGGL(k_ntt_inverse<S>, dim3(count), dim3(S::T), 0,
-                                                    st, in, out, tb.zeta_inv, tb.ninv));
+    ROSETTA_DISPATCH_N(ilog2(N), ROSETTA_LAUNCH(k_ntt_inverse<S>, dim3(count), dim3(S::T),
+                                                ntt_lds_bytes<S>(), st, in, out, tb.zeta,
+                                                tb.ninv));
   } else {
-    ROSETTA_DISPATCH_N(ilog2(N), hipLaunchKernelGGL(k_ntt_forward<S>, dim3(count), dim3(S::T), 0,
-                                                    st, in, out, tb.zeta));
+    ROSETTA_DISPATCH_N(ilog2(N), ROSETTA_LAUNCH(k_ntt_forward<S>, dim3(count), dim3(S::T),
+                                                ntt_lds_bytes<S>(), st, in, out, tb.zeta));
   }
   return hipGetLastError();
 }
 
 hipError_t launch_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *c, size_t count,
                            uint32_t N, const Tables &tb, hipStream_t st) {
-  ROSETTA_DISPATCH_N(ilog2(N), hipLaunchKernelGGL(k_poly_mul<S>, dim3(count), dim3(S::T), 0, st,
-                                                  a, b, c, tb.zeta, tb.zeta_inv, tb.ninv));
+  ROSETTA_DISPATCH_N(ilog2(N), ROSETTA_LAUNCH(k_poly_mul<S>, dim3(count), dim3(S::T),
+                                              ntt_lds_bytes<S>(), st, a, b, c, tb.zeta,
+                                              tb.ninv));
   return hipGetLastError();
 }
 

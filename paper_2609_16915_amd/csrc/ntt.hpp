@@ -6,8 +6,11 @@
 // b = j >> (LOGN - s) and multiplies the upper element by
 // zeta[2^s + b] = psi^rev(2^s + b)  (psi a primitive 2N-th root of unity,
 // rev the LOGN-bit reversal), so the result at in-place index j is
-// a(psi^(2 rev(j) + 1)).  The inverse runs the Gentleman-Sande mirror with
-// the inverse twiddles and leaves the factor N for the caller.
+// a(psi^(2 rev(j) + 1)).  The inverse runs the Gentleman-Sande mirror and
+// leaves the factor N for the caller.  It needs psi^-rev(m); within stage s
+// that equals -zeta[3*2^s - 1 - m], so a single table serves both
+// directions and the sign is absorbed by computing (v - u) * zeta instead of
+// (u - v) * zeta^-1.
 //
 // Stages are grouped into passes of LE stages.  During pass q a thread holds
 // the E elements whose index bits [lo_q, lo_q + LE) vary, lo_q =
@@ -18,16 +21,33 @@
 // between two buffers so that one barrier per transpose suffices.  Pass 0
 // is the natural layout j = tid + T*k.
 //
-// Addresses are written as a per-thread base plus a compile-time offset per
-// element, so that LDS accesses use the instructions' immediate offsets and
-// twiddle loads need one address register per stage.
+// LDS word addresses of the transposes go through a linear XOR swizzle
+// (bit b < 5 of the address is flipped by the parity of j & SWZ_MASK[b],
+// masks holding only bits above b).  It was chosen so that in every pass
+// layout of every supported (N, E) the 32 lanes of each half wave touch 32
+// distinct banks of 8-byte words, and the 16 lanes of each quarter wave 16
+// distinct ones.  Being linear over GF(2), the address of element k is the
+// thread's swizzled base XOR a compile-time constant.  The twiddle table
+// itself lives in LDS: the key streams through the vector memory path, so
+// keeping twiddle reads off it keeps their latency off the in-order
+// vector-memory counter.
 #pragma once
+
+#include <type_traits>
 
 #include "gl.hpp"
 
 namespace rosetta {
 
 typedef const u64 __attribute__((address_space(1))) gconst_u64;
+
+constexpr unsigned SWZ_MASK[5] = {0x7b0, 0x574, 0x538, 0xa60, 0x3e0};
+
+__host__ __device__ constexpr int swz(int j) {
+  int a = j;
+  for (int b = 0; b < 5; ++b) a ^= (__builtin_popcount((unsigned)j & SWZ_MASK[b]) & 1) << b;
+  return a;
+}
 
 template <int LOGN_, int LE_>
 struct Ntt {
@@ -37,9 +57,6 @@ struct Ntt {
   static constexpr int E = 1 << LE;
   static constexpr int T = N / E;
   static constexpr int PASSES = (LOGN + LE - 1) / LE;
-  // one padding word every 32 elements breaks power-of-two strides
-  static constexpr int PAD_SHIFT = 5;
-  static constexpr int LDS_WORDS = N + (N >> PAD_SHIFT);
 
   __host__ __device__ static constexpr int lo(int q) {
     return (LOGN - (q + 1) * LE) > 0 ? (LOGN - (q + 1) * LE) : 0;
@@ -48,33 +65,119 @@ struct Ntt {
   __host__ __device__ static constexpr int stage_end(int q) {
     return (q + 1) * LE < LOGN ? (q + 1) * LE : LOGN;
   }
-  __host__ __device__ static constexpr int pad(int j) { return j + (j >> PAD_SHIFT); }
   // index held by element k of thread tid during pass q
   __host__ __device__ static constexpr int idx(int q, int tid, int k) {
     return (tid & ((1 << lo(q)) - 1)) + (k << lo(q)) + ((tid >> lo(q)) << (lo(q) + LE));
   }
-  // padded LDS word of element k = per-thread base + constant offset.  The
-  // thread part and the k part of the index occupy disjoint bits, so the
-  // padding (j >> 5) splits the same way.
-  __host__ __device__ static constexpr int lds_base(int q, int tid) {
-    return pad(idx(q, tid, 0));
-  }
-  __host__ __device__ static constexpr int lds_off(int q, int k) { return pad(k << lo(q)); }
 };
 
-// Forward stages of pass Q.  For stage s (shift sh = LOGN - s) the twiddle
-// of the pair led by element k is
-//   zeta[2^s + ((tid >> lo) << (lo + LE - sh)) + ((k >> (sh - lo)) ...)],
-// i.e. a per-thread base for the stage plus a compile-time offset.
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// zeta[m] for m < 8 is a 16th root of unity, and with psi = 7^((p-1)/2N)
+// it equals 2^((156 * rev3(m)) mod 192) for every N, 7^((p-1)/16) being
+// 2^156.  Pass 0 (stages 0..LE-1 <= 2) uses only these, so its twiddle
+// products are shifts (gl_mul_pow2) and need no table.
+__host__ __device__ constexpr int rev3(int m) {
+  return ((m & 1) << 2) | (m & 2) | ((m >> 2) & 1);
+}
+__host__ __device__ constexpr int zeta_log2(int m) { return (156 * rev3(m)) % 192; }
+
+// |zeta[M]| * x for M < 8; zeta[M] is negative when its exponent is >= 96.
+template <int M>
+__device__ __forceinline__ u64 mul_small_root(u64 x) {
+  constexpr int e = zeta_log2(M);
+  return gl_mul_pow2<(e >= 96 ? e - 96 : e)>(x);
+}
+template <int M>
+__host__ __device__ constexpr bool small_root_negative() {
+  return zeta_log2(M) >= 96;
+}
+
+// Pass 0 of the forward transform (all twiddles compile-time powers of
+// two), starting at stage FIRST.
+template <class S, int FIRST>
+__device__ __forceinline__ void ntt_fwd_pass0(u64 (&x)[S::E]) {
+  constexpr int lo = S::lo(0);
+  static_for<FIRST, S::stage_end(0)>([&](auto sc) {
+    constexpr int s = decltype(sc)::value;
+    constexpr int sh = S::LOGN - s;
+    constexpr int b = sh - 1 - lo;
+    static_for<0, S::E>([&](auto kc) {
+      constexpr int k = decltype(kc)::value;
+      if constexpr (!(k & (1 << b))) {
+        constexpr int k2 = k | (1 << b);
+        constexpr int m = (1 << s) + (k >> (sh - lo));
+        const u64 t = mul_small_root<m>(x[k2]);
+        const u64 u = x[k];
+        if constexpr (small_root_negative<m>()) {  // w = -|w|
+          x[k] = gl_sub(u, t);
+          x[k2] = gl_add(u, t);
+        } else {
+          x[k] = gl_add(u, t);
+          x[k2] = gl_sub(u, t);
+        }
+      }
+    });
+  });
+}
+
+// Pass 0 of the inverse transform: (u, v) -> (u + v, (v - u) zeta[2^(s+1)-1-b]).
+template <class S>
+__device__ __forceinline__ void ntt_inv_pass0(u64 (&x)[S::E]) {
+  constexpr int lo = S::lo(0);
+  static_for<0, S::stage_end(0)>([&](auto rc) {
+    constexpr int s = S::stage_end(0) - 1 - decltype(rc)::value;
+    constexpr int sh = S::LOGN - s;
+    constexpr int b = sh - 1 - lo;
+    static_for<0, S::E>([&](auto kc) {
+      constexpr int k = decltype(kc)::value;
+      if constexpr (!(k & (1 << b))) {
+        constexpr int k2 = k | (1 << b);
+        constexpr int m = (2 << s) - 1 - (k >> (sh - lo));
+        const u64 u = x[k], v = x[k2];
+        x[k] = gl_add(u, v);
+        if constexpr (small_root_negative<m>())  // (v - u)(-|w|) = (u - v)|w|
+          x[k2] = mul_small_root<m>(gl_sub(u, v));
+        else
+          x[k2] = mul_small_root<m>(gl_sub(v, u));
+      }
+    });
+  });
+}
+
+// Stage 0 of the forward transform on small signed inputs (|d| < 2^14),
+// in exact 64-bit integer arithmetic: zeta[1] = 2^48, so
+// d_k +- 2^48 d_k2 fits in 63 bits and needs only a sign fix.
+template <class S, typename RT>
+__device__ __forceinline__ void ntt_fwd_stage0_small(const RT (&d)[S::E], u64 (&x)[S::E]) {
+  static_assert(zeta_log2(1) == 48, "zeta[1] must be 2^48");
+  constexpr int half = S::E / 2;
+#pragma unroll
+  for (int k = 0; k < half; ++k) {
+    const i64 lo = (i64)d[k];
+    const i64 hi = (i64)d[k + half] * ((i64)1 << 48);
+    x[k] = gl_from_i64(lo + hi);
+    x[k + half] = gl_from_i64(lo - hi);
+  }
+}
+
+// Forward stages of pass Q; `tw` is the LDS twiddle table.
 template <class S, int Q>
-__device__ __forceinline__ void ntt_fwd_pass(u64 (&x)[S::E], int tid, gconst_u64 *zeta) {
+__device__ __forceinline__ void ntt_fwd_pass(u64 (&x)[S::E], int tid, const u64 *tw) {
   constexpr int lo = S::lo(Q);
-  const int hb = tid >> lo;
+  const int jt = S::idx(Q, tid, 0);
 #pragma unroll
   for (int s = S::stage_begin(Q); s < S::stage_end(Q); ++s) {
     const int sh = S::LOGN - s;
     const int b = sh - 1 - lo;  // k-bit split by this stage
-    gconst_u64 *zs = zeta + (1 << s) + (hb << (lo + S::LE - sh));
+    const u64 *zs = tw + (1 << s) + (jt >> sh);
 #pragma unroll
     for (int k = 0; k < S::E; ++k) {
       if (k & (1 << b)) continue;
@@ -87,38 +190,40 @@ __device__ __forceinline__ void ntt_fwd_pass(u64 (&x)[S::E], int tid, gconst_u64
   }
 }
 
-// Inverse (Gentleman-Sande) stages of pass Q, in reverse stage order.
+// Inverse (Gentleman-Sande) stages of pass Q, in reverse stage order:
+// (u, v) -> (u + v, (v - u) * zeta[2^(s+1) - 1 - b]).
 template <class S, int Q>
-__device__ __forceinline__ void ntt_inv_pass(u64 (&x)[S::E], int tid, gconst_u64 *zeta_inv) {
+__device__ __forceinline__ void ntt_inv_pass(u64 (&x)[S::E], int tid, const u64 *tw) {
   constexpr int lo = S::lo(Q);
-  const int hb = tid >> lo;
+  const int jt = S::idx(Q, tid, 0);
 #pragma unroll
   for (int s = S::stage_end(Q) - 1; s >= S::stage_begin(Q); --s) {
     const int sh = S::LOGN - s;
     const int b = sh - 1 - lo;
-    gconst_u64 *zs = zeta_inv + (1 << s) + (hb << (lo + S::LE - sh));
+    const u64 *zs = tw + (2 << s) - 1 - (jt >> sh);
 #pragma unroll
     for (int k = 0; k < S::E; ++k) {
       if (k & (1 << b)) continue;
       const int k2 = k | (1 << b);
-      const u64 w = zs[k >> (sh - lo)];
+      const u64 w = zs[-(k >> (sh - lo))];
       const u64 u = x[k], v = x[k2];
       x[k] = gl_add(u, v);
-      x[k2] = gl_mul(gl_sub(u, v), w);
+      x[k2] = gl_mul(gl_sub(v, u), w);
     }
   }
 }
 
-// Move from the layout of pass QW to that of pass QR through one LDS buffer.
+// Move from the layout of pass QW to that of pass QR through one LDS buffer
+// (swizzled word addresses).
 template <class S, int QW, int QR>
 __device__ __forceinline__ void ntt_exchange(u64 (&x)[S::E], u64 *lds, int tid) {
-  u64 *w = lds + S::lds_base(QW, tid);
+  const int wb = swz(S::idx(QW, tid, 0));
 #pragma unroll
-  for (int k = 0; k < S::E; ++k) w[S::lds_off(QW, k)] = x[k];
+  for (int k = 0; k < S::E; ++k) lds[wb ^ swz(k << S::lo(QW))] = x[k];
   __syncthreads();
-  const u64 *r = lds + S::lds_base(QR, tid);
+  const int rb = swz(S::idx(QR, tid, 0));
 #pragma unroll
-  for (int k = 0; k < S::E; ++k) x[k] = r[S::lds_off(QR, k)];
+  for (int k = 0; k < S::E; ++k) x[k] = lds[rb ^ swz(k << S::lo(QR))];
 }
 
 // Two LDS buffers of `words` words each, used alternately.
@@ -136,21 +241,27 @@ struct LdsPair {
 
 template <class S, int Q>
 __device__ __forceinline__ void ntt_fwd_from(u64 (&x)[S::E], LdsPair &lds, int tid,
-                                             gconst_u64 *zeta) {
-  ntt_fwd_pass<S, Q>(x, tid, zeta);
+                                             const u64 *tw) {
+  if constexpr (Q == 0)
+    ntt_fwd_pass0<S, 0>(x);
+  else
+    ntt_fwd_pass<S, Q>(x, tid, tw);
   if constexpr (Q + 1 < S::PASSES) {
     ntt_exchange<S, Q, Q + 1>(x, lds.next(), tid);
-    ntt_fwd_from<S, Q + 1>(x, lds, tid, zeta);
+    ntt_fwd_from<S, Q + 1>(x, lds, tid, tw);
   }
 }
 
 template <class S, int Q>
 __device__ __forceinline__ void ntt_inv_from(u64 (&x)[S::E], LdsPair &lds, int tid,
-                                             gconst_u64 *zeta_inv) {
-  ntt_inv_pass<S, Q>(x, tid, zeta_inv);
+                                             const u64 *tw) {
+  if constexpr (Q == 0)
+    ntt_inv_pass0<S>(x);
+  else
+    ntt_inv_pass<S, Q>(x, tid, tw);
   if constexpr (Q > 0) {
     ntt_exchange<S, Q, Q - 1>(x, lds.next(), tid);
-    ntt_inv_from<S, Q - 1>(x, lds, tid, zeta_inv);
+    ntt_inv_from<S, Q - 1>(x, lds, tid, tw);
   }
 }
 
@@ -158,15 +269,36 @@ __device__ __forceinline__ void ntt_inv_from(u64 (&x)[S::E], LdsPair &lds, int t
 // pass out.
 template <class S>
 __device__ __forceinline__ void ntt_forward(u64 (&x)[S::E], LdsPair &lds, int tid,
-                                            gconst_u64 *zeta) {
-  ntt_fwd_from<S, 0>(x, lds, tid, zeta);
+                                            const u64 *tw) {
+  ntt_fwd_from<S, 0>(x, lds, tid, tw);
+}
+
+// Forward transform of a polynomial with small signed coefficients d
+// (|d| < 2^14): stage 0 in integer arithmetic, then as ntt_forward.
+template <class S, typename RT>
+__device__ __forceinline__ void ntt_forward_small(const RT (&d)[S::E], u64 (&x)[S::E],
+                                                  LdsPair &lds, int tid, const u64 *tw) {
+  ntt_fwd_stage0_small<S, RT>(d, x);
+  ntt_fwd_pass0<S, 1>(x);
+  if constexpr (S::PASSES > 1) {
+    ntt_exchange<S, 0, 1>(x, lds.next(), tid);
+    ntt_fwd_from<S, 1>(x, lds, tid, tw);
+  }
 }
 
 // Last-pass layout in, natural layout out, result scaled by N.
 template <class S>
 __device__ __forceinline__ void ntt_inverse(u64 (&x)[S::E], LdsPair &lds, int tid,
-                                            gconst_u64 *zeta_inv) {
-  ntt_inv_from<S, S::PASSES - 1>(x, lds, tid, zeta_inv);
+                                            const u64 *tw) {
+  ntt_inv_from<S, S::PASSES - 1>(x, lds, tid, tw);
+}
+
+// Copy the N-word twiddle table into LDS (all threads of the workgroup).
+template <class S>
+__device__ __forceinline__ void load_twiddles(u64 *tw_lds, const u64 *__restrict__ zeta,
+                                              int tid) {
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) tw_lds[tid + S::T * k] = zeta[tid + S::T * k];
 }
 
 // Global-address-space view of a device pointer.
