@@ -27,14 +27,44 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-# MI355X published / derived peaks ("Roofline")
+# MI355X peaks.  The VALU issues 64 lanes of a full-rate 32-bit instruction
+# per clock per CU (4 SIMDs x 16 lanes): 256 CUs x 64 x 2.4 GHz = 39.3e12
+# lane-ops/s.  The library's Goldilocks multiplication (gl_mul) is 28
+# full-rate VALU instructions on gfx950 (8 v_mul_lo/hi_u32 and 20
+# add/sub-with-carry and select), which bounds its rate at 39.3e12 / 28 =
+# 1.40e12 modmul/s; the 8 multiply instructions alone bound any 64x64-bit
+# modular product at 39.3e12 / 8 = 4.9e12 modmul/s.
 HBM_PEAK_GBS = 8000.0
 CU, CLOCK_HZ, LANES = 256, 2.4e9, 64
-# VALU issue slots (one wave64 instruction at full rate = 1 slot per lane
-# group) of one Goldilocks modular multiplication in the library's sequence:
-# 4 v_mad_u64_u32 at half rate (2 slots each) + 14 full-rate ops.
-MODMUL_SLOTS = 4 * 2 + 14
-MODMUL_PEAK_T = CU * CLOCK_HZ * LANES / MODMUL_SLOTS / 1e12   # Tmodmul/s
+MODMUL_VALU_OPS = 28
+MODMUL_PEAK_T = CU * CLOCK_HZ * LANES / MODMUL_VALU_OPS / 1e12   # Tmodmul/s
+MULTIPLIER_BOUND_T = CU * CLOCK_HZ * LANES / 8 / 1e12
+PMC_PROFILE = os.path.join(ROOT, "profiles", "k_blind_rotate_llama3_8b_silu_pmc.md")
+KERNEL_SOURCES = ["gl.hpp", "ntt.hpp", "kernels.hip"]
+
+
+def measured_traffic(workload: str, batch: int):
+    """Calibrated HBM bytes per blind-rotation launch from the committed
+    counter profile, or None unless that profile describes the current
+    kernel sources and this workload."""
+    import hashlib
+    import re
+    from paper_2609_16915_amd import workloads as W
+    if workload != W.HEADLINE or batch != W.get(W.HEADLINE).batch:
+        return None
+    try:
+        text = open(PMC_PROFILE).read()
+    except OSError:
+        return None
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_16915_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    m_sha = re.search(r"kernel_source_sha256: ([0-9a-f]{64})", text)
+    m_tb = re.search(r"traffic_bytes_per_launch: ([0-9.eE+]+)", text)
+    if not m_sha or not m_tb or m_sha.group(1) != h.hexdigest():
+        return None
+    return float(m_tb.group(1))
 
 
 def log(*a):
@@ -117,7 +147,8 @@ def main():
         words = args.calibrate_copy_mib * (1 << 20) // 8
         src = torch.zeros(words, dtype=torch.int64, device="cuda")
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.cuda.synchronize()
+        torch.add(src, 1, out=dst)  # elementwise: reads and writes `words` * 8 bytes
         torch.cuda.synchronize()
         del src, dst
 
@@ -155,8 +186,11 @@ def main():
     achieved_t = modmul_per_launch / (br_ms * 1e-3) / 1e12
     roofline = {"bound": "alu", "kernel": "k_blind_rotate", "achieved": round(achieved_t, 4),
                 "peak": round(MODMUL_PEAK_T, 4), "unit": "Tmodmul/s",
-                "frac": round(achieved_t / MODMUL_PEAK_T, 4), "traffic": None,
-                "per_launch_modmul": modmul_per_launch, "launch_ms": round(br_ms, 3)}
+                "frac": round(achieved_t / MODMUL_PEAK_T, 4),
+                "traffic": measured_traffic(name, w.batch),
+                "per_launch_modmul": modmul_per_launch, "launch_ms": round(br_ms, 3),
+                "multiplier_bound": round(MULTIPLIER_BOUND_T, 4),
+                "frac_of_multiplier_bound": round(achieved_t / MULTIPLIER_BOUND_T, 4)}
     hbm_bytes = (w.bsk_words() + w.ksk_words()) * 8 + w.batch * 2 * (w.n + 1) * 8 + w.N * 8
 
     result = {
