@@ -127,10 +127,24 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
     const u64 psi = gl_pow(7, (GL_P - 1) / (2 * (u64)N));
     std::vector<u64> z(N);
     for (uint32_t m = 0; m < N; ++m) z[m] = gl_pow(psi, bitrev(m, logn));
+    // radix-8 powers for the passes after the first that span three stages
+    // (passes of 3 stages when N > 256; the first pass uses no table)
+    if (logn >= 9) {
+      for (int q = 1; 3 * q + 3 <= logn; ++q) {
+        const int s0 = 3 * q;
+        for (uint32_t b = 0; b < (1u << s0); ++b) {
+          const u64 qq = z[4 * ((1u << s0) + b)];
+          z.push_back(gl_pow(qq, 3));
+          z.push_back(gl_pow(qq, 5));
+          z.push_back(gl_pow(qq, 6));
+          z.push_back(gl_pow(qq, 7));
+        }
+      }
+    }
     DevTables t;
-    e = hipMalloc(&t.zeta, N * sizeof(u64));
+    e = hipMalloc(&t.zeta, z.size() * sizeof(u64));
     if (e != hipSuccess) return hip_fail(e, "hipMalloc(twiddles)");
-    e = hipMemcpy(t.zeta, z.data(), N * sizeof(u64), hipMemcpyHostToDevice);
+    e = hipMemcpy(t.zeta, z.data(), z.size() * sizeof(u64), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       (void)hipFree(t.zeta);
       return hip_fail(e, "hipMemcpy(twiddles)");

@@ -125,6 +125,18 @@ __host__ __device__ __forceinline__ u64 gl_mul_pow2(u64 x) {
   }
 }
 
+// (a * b + c) mod p with one reduction: the 128-bit product plus a value
+// below p stays below p^2 + p < 2^128.
+__host__ __device__ __forceinline__ u64 gl_mul_add(u64 a, u64 b, u64 c) {
+  u32 c0, c1, c2, c3, k;
+  gl_mul_limbs(a, b, c0, c1, c2, c3);
+  c0 = __builtin_addc(c0, (u32)c, 0u, &k);
+  c1 = __builtin_addc(c1, (u32)(c >> 32), k, &k);
+  c2 = __builtin_addc(c2, 0u, k, &k);
+  c3 = c3 + k;
+  return gl_reduce_limbs(c0, c1, c2, c3);
+}
+
 __host__ __device__ inline u64 gl_pow(u64 a, u64 e) {
   u64 r = 1;
   while (e) {

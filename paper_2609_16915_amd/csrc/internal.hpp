@@ -17,7 +17,10 @@ constexpr uint32_t MAX_LWE_N = 2048;
 
 // Per-device, per-N transform tables (device pointers) and N^-1.
 struct Tables {
-  const uint64_t *zeta;  // [N]: zeta[m] = psi^rev(m), m >= 1 (zeta[0] = 1)
+  // zeta[m] = psi^rev(m) for m < N (zeta[0] = 1), followed by the radix-8
+  // powers q^3, q^5, q^6, q^7 (q = zeta[4m]) of every block m of each
+  // twisted pass (see ntt.hpp)
+  const uint64_t *zeta;
   uint64_t ninv;
 };
 

@@ -19,13 +19,13 @@ namespace rosetta {
 // Key preparation
 // ---------------------------------------------------------------------------
 
-// Dynamic LDS of the transform kernels: the N-word twiddle table, then two
-// N-word transpose buffers.
+// Dynamic LDS of the transform kernels: the twiddle area (TW_WORDS words:
+// zeta[N] then the radix-8 powers), then two N-word transpose buffers.
 extern __shared__ __align__(16) u64 lds_dyn[];
 
 template <class S>
 constexpr size_t ntt_lds_bytes() {
-  return (size_t)3 * S::N * sizeof(u64);
+  return (size_t)(S::TW_WORDS + 2 * S::N) * sizeof(u64);
 }
 
 // Row r of the standard key (N coefficients) -> transform domain, scaled by
@@ -36,7 +36,7 @@ __global__ void __launch_bounds__(S::T)
 k_bsk_prepare(const u64 *__restrict__ std_key, u64 *__restrict__ dev_key,
               const u64 *__restrict__ zeta, u64 ninv) {
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::N, S::N);
+  LdsPair lds(lds_dyn + S::TW_WORDS, S::N);
   const int tid = threadIdx.x;
   const size_t row = blockIdx.x;
   load_twiddles<S>(tw, zeta, tid);
@@ -69,7 +69,7 @@ template <class S>
 __global__ void __launch_bounds__(S::T)
 k_ntt_forward(const u64 *in, u64 *out, const u64 *__restrict__ zeta) {
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::N, S::N);
+  LdsPair lds(lds_dyn + S::TW_WORDS, S::N);
   const int tid = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * S::N;
   load_twiddles<S>(tw, zeta, tid);
@@ -86,7 +86,7 @@ template <class S>
 __global__ void __launch_bounds__(S::T)
 k_ntt_inverse(const u64 *in, u64 *out, const u64 *__restrict__ zeta, u64 ninv) {
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::N, S::N);
+  LdsPair lds(lds_dyn + S::TW_WORDS, S::N);
   const int tid = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * S::N;
   load_twiddles<S>(tw, zeta, tid);
@@ -103,7 +103,7 @@ template <class S>
 __global__ void __launch_bounds__(S::T)
 k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta, u64 ninv) {
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::N, S::N);
+  LdsPair lds(lds_dyn + S::TW_WORDS, S::N);
   const int tid = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * S::N;
   load_twiddles<S>(tw, zeta, tid);
@@ -177,8 +177,8 @@ __device__ __forceinline__ RT digit_of(RT r, int beta, int t) {
 // into registers before its forward transform, so their latency overlaps
 // the transform.
 //
-// Dynamic LDS: twiddles [N], two transpose buffers [N] each, then the n+1
-// rounded rotation amounts (u16).
+// Dynamic LDS: twiddle area [TW_WORDS], two transpose buffers [N] each,
+// then the n+1 rounded rotation amounts (u16).
 template <class S>
 size_t br_lds_bytes(int n) {
   return ntt_lds_bytes<S>() + (((size_t)(n + 1) * 2 + 15) & ~(size_t)15);
@@ -191,8 +191,8 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
                const u64 *__restrict__ zeta) {
   constexpr int N = S::N, E = S::E, T = S::T;
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + N, N);
-  uint16_t *rot = (uint16_t *)(lds_dyn + 3 * N);
+  LdsPair lds(lds_dyn + S::TW_WORDS, N);
+  uint16_t *rot = (uint16_t *)(lds_dyn + S::TW_WORDS + 2 * N);
   const int tid = threadIdx.x;
   const size_t ct = blockIdx.x;
 
@@ -278,8 +278,8 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
         }
 #pragma unroll
         for (int k = 0; k < E; ++k) {
-          Y0[k] = gl_add(Y0[k], gl_mul(x[k], g0[k]));
-          Y1[k] = gl_add(Y1[k], gl_mul(x[k], g1[k]));
+          Y0[k] = gl_mul_add(x[k], g0[k], Y0[k]);
+          Y1[k] = gl_mul_add(x[k], g1[k], Y1[k]);
         }
       }
     }

@@ -69,6 +69,21 @@ struct Ntt {
   __host__ __device__ static constexpr int idx(int q, int tid, int k) {
     return (tid & ((1 << lo(q)) - 1)) + (k << lo(q)) + ((tid >> lo(q)) << (lo(q) + LE));
   }
+  // Passes after the first that span three stages run in twisted radix-8
+  // form and need, per block of their first stage, the powers q^3, q^5,
+  // q^6, q^7 of q = zeta[4 m] (q, q^2, q^4 are zeta[4m], zeta[2m], zeta[m]).
+  __host__ __device__ static constexpr bool twisted(int q) {
+    return q >= 1 && LE == 3 && stage_end(q) - stage_begin(q) == 3;
+  }
+  __host__ __device__ static constexpr int tw8_base(int q) {
+    int b = 0;
+    for (int r = 1; r < q; ++r)
+      if (twisted(r)) b += 4 << stage_begin(r);
+    return b;
+  }
+  static constexpr int TW8_WORDS = tw8_base(PASSES);
+  // words of the LDS twiddle area: zeta[N] then the radix-8 powers
+  static constexpr int TW_WORDS = N + TW8_WORDS;
 };
 
 // Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
@@ -168,6 +183,117 @@ __device__ __forceinline__ void ntt_fwd_stage0_small(const RT (&d)[S::E], u64 (&
   }
 }
 
+// Twisted radix-8 form of a three-stage pass (Q >= 1).  The thread's eight
+// elements are the coefficients x_k of one block polynomial sum x_k Z^k
+// taken modulo Z^8 - zeta[m]^2 (m the block at the pass's first stage).  The
+// three merged-twist stages evaluate it at q w^e, q = zeta[4m] (q^4 =
+// zeta[m]) and w = psi^(N/4) a primitive 8th root, i.e. they equal
+//   y_k = q^k x_k   followed by an 8-point transform of y
+// whose twiddles are the 8th roots i = w^2 = 2^48, w = -2^24 and
+// w^3 = -2^72: shifts, not multiplications.  7 products + 5 shifts replace
+// 12 products.  The inverse undoes it: psi^-rev(4m) = w^-1 zeta[4 m_r] with
+// m_r = 3*2^s - 1 - m (the block reflected within its stage), and the
+// factor w^-k is absorbed by feeding the inverse 8-point transform its
+// inputs rotated by one frequency (slots 7,6,4,5,0,1,2,3), after which the
+// untwist multiplies by powers of zeta[4 m_r].
+template <class S, int Q>
+__device__ __forceinline__ void ntt_fwd_pass_twisted(u64 (&x)[S::E], int tid, const u64 *tw) {
+  constexpr int lo = S::lo(Q), s0 = S::stage_begin(Q);
+  const int b = tid >> lo;  // block at stage s0
+  const int m = (1 << s0) + b;
+  const u64 *t8 = tw + S::N + S::tw8_base(Q) + 4 * b;
+  x[1] = gl_mul(x[1], tw[4 * m]);
+  x[2] = gl_mul(x[2], tw[2 * m]);
+  x[3] = gl_mul(x[3], t8[0]);
+  x[4] = gl_mul(x[4], tw[m]);
+  x[5] = gl_mul(x[5], t8[1]);
+  x[6] = gl_mul(x[6], t8[2]);
+  x[7] = gl_mul(x[7], t8[3]);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const u64 u = x[k], v = x[k + 4];
+    x[k] = gl_add(u, v);
+    x[k + 4] = gl_sub(u, v);
+  }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    u64 u = x[k], v = x[k + 2];
+    x[k] = gl_add(u, v);
+    x[k + 2] = gl_sub(u, v);
+    u = x[k + 4];
+    v = gl_mul_pow2<48>(x[k + 6]);  // i
+    x[k + 4] = gl_add(u, v);
+    x[k + 6] = gl_sub(u, v);
+  }
+  {
+    u64 u = x[0], v = x[1];
+    x[0] = gl_add(u, v);
+    x[1] = gl_sub(u, v);
+    u = x[2];
+    v = gl_mul_pow2<48>(x[3]);  // i
+    x[2] = gl_add(u, v);
+    x[3] = gl_sub(u, v);
+    u = x[4];
+    v = gl_mul_pow2<24>(x[5]);  // w = -2^24
+    x[4] = gl_sub(u, v);
+    x[5] = gl_add(u, v);
+    u = x[6];
+    v = gl_mul_pow2<72>(x[7]);  // w^3 = -2^72
+    x[6] = gl_sub(u, v);
+    x[7] = gl_add(u, v);
+  }
+}
+
+template <class S, int Q>
+__device__ __forceinline__ void ntt_inv_pass_twisted(u64 (&x)[S::E], int tid, const u64 *tw) {
+  constexpr int lo = S::lo(Q), s0 = S::stage_begin(Q);
+  const int br = (1 << s0) - 1 - (tid >> lo);  // reflected block
+  const int mr = (1 << s0) + br;
+  const u64 *t8 = tw + S::N + S::tw8_base(Q) + 4 * br;
+  u64 z[8] = {x[7], x[6], x[4], x[5], x[0], x[1], x[2], x[3]};
+  {
+    u64 u = z[0], v = z[1];
+    z[0] = gl_add(u, v);
+    z[1] = gl_sub(u, v);
+    u = z[2];
+    v = z[3];
+    z[2] = gl_add(u, v);
+    z[3] = gl_mul_pow2<48>(gl_sub(v, u));  // i^-1 = -2^48
+    u = z[4];
+    v = z[5];
+    z[4] = gl_add(u, v);
+    z[5] = gl_mul_pow2<72>(gl_sub(u, v));  // w^-1 = 2^72
+    u = z[6];
+    v = z[7];
+    z[6] = gl_add(u, v);
+    z[7] = gl_mul_pow2<24>(gl_sub(u, v));  // w^-3 = 2^24
+  }
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    u64 u = z[k], v = z[k + 2];
+    z[k] = gl_add(u, v);
+    z[k + 2] = gl_sub(u, v);
+    u = z[k + 4];
+    v = z[k + 6];
+    z[k + 4] = gl_add(u, v);
+    z[k + 6] = gl_mul_pow2<48>(gl_sub(v, u));  // i^-1
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const u64 u = z[k], v = z[k + 4];
+    z[k] = gl_add(u, v);
+    z[k + 4] = gl_sub(u, v);
+  }
+  x[0] = z[0];
+  x[1] = gl_mul(z[1], tw[4 * mr]);
+  x[2] = gl_mul(z[2], tw[2 * mr]);
+  x[3] = gl_mul(z[3], t8[0]);
+  x[4] = gl_mul(z[4], tw[mr]);
+  x[5] = gl_mul(z[5], t8[1]);
+  x[6] = gl_mul(z[6], t8[2]);
+  x[7] = gl_mul(z[7], t8[3]);
+}
+
 // Forward stages of pass Q; `tw` is the LDS twiddle table.
 template <class S, int Q>
 __device__ __forceinline__ void ntt_fwd_pass(u64 (&x)[S::E], int tid, const u64 *tw) {
@@ -244,6 +370,8 @@ __device__ __forceinline__ void ntt_fwd_from(u64 (&x)[S::E], LdsPair &lds, int t
                                              const u64 *tw) {
   if constexpr (Q == 0)
     ntt_fwd_pass0<S, 0>(x);
+  else if constexpr (S::twisted(Q))
+    ntt_fwd_pass_twisted<S, Q>(x, tid, tw);
   else
     ntt_fwd_pass<S, Q>(x, tid, tw);
   if constexpr (Q + 1 < S::PASSES) {
@@ -257,6 +385,8 @@ __device__ __forceinline__ void ntt_inv_from(u64 (&x)[S::E], LdsPair &lds, int t
                                              const u64 *tw) {
   if constexpr (Q == 0)
     ntt_inv_pass0<S>(x);
+  else if constexpr (S::twisted(Q))
+    ntt_inv_pass_twisted<S, Q>(x, tid, tw);
   else
     ntt_inv_pass<S, Q>(x, tid, tw);
   if constexpr (Q > 0) {
@@ -293,12 +423,12 @@ __device__ __forceinline__ void ntt_inverse(u64 (&x)[S::E], LdsPair &lds, int ti
   ntt_inv_from<S, S::PASSES - 1>(x, lds, tid, tw);
 }
 
-// Copy the N-word twiddle table into LDS (all threads of the workgroup).
+// Copy the twiddle area (zeta[N] and the radix-8 powers, TW_WORDS words)
+// into LDS (all threads of the workgroup).
 template <class S>
 __device__ __forceinline__ void load_twiddles(u64 *tw_lds, const u64 *__restrict__ zeta,
                                               int tid) {
-#pragma unroll
-  for (int k = 0; k < S::E; ++k) tw_lds[tid + S::T * k] = zeta[tid + S::T * k];
+  for (int i = tid; i < S::TW_WORDS; i += S::T) tw_lds[i] = zeta[i];
 }
 
 // Global-address-space view of a device pointer.
