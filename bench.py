@@ -94,8 +94,8 @@ def cpu_baseline(w, keys, cts, v, seconds_target: float):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 = skip)")
@@ -172,6 +172,7 @@ def main():
     wall = time.perf_counter() - t0
     br_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
     ks_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
+    step_ms = [a.elapsed_time(c) for a, _, c in ev]
     ms_per_step = wall * 1e3 / args.steps
     value = w.batch / (wall / args.steps)
 
@@ -197,7 +198,10 @@ def main():
         "metric": "PBS/s (bootstraps per second) at N=2048, batch 14336; roofline fraction "
                   "of the blind-rotation kernel",
         "value": round(value, 2), "unit": "PBS/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3),
+        "ms_per_step_events": {"median": round(float(np.median(step_ms)), 3),
+                               "min": round(float(np.min(step_ms)), 3)},
+        "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "u64 mod p (Goldilocks)",
         "data": "synthetic (seeded activations, random keys)",
         "config": {"workload": name, "n": w.n, "N": w.N, "pbs_level": w.pbs_level,
