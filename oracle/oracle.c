@@ -565,17 +565,26 @@ void or_bsk_transform(const or_params *P, const u64 *bsk, u64 *fbsk, int nthread
  * pointwise product; linearity lets the sums over (u, t) be taken there).
  * `fbsk`, if not NULL, holds the forward transform of every key row
  * (or_bsk_transform); otherwise rows are transformed when used. */
+static void or_br_loop(const or_params *P, const u64 *lwe, const u64 *bsk, const u64 *fbsk,
+                       u64 *acc, int kind);
+
 void or_blind_rotate(const or_params *P, const u64 *lwe, const u64 *bsk, const u64 *fbsk,
                      const u64 *v, u64 *acc, int kind) {
+  int n = (int)P->n, N = (int)P->N;
+  uint32_t bt = or_modswitch(lwe[n], N);
+  for (int j = 0; j < N; ++j) acc[j] = 0;
+  or_poly_monomial_mul(v, (int)((2 * (uint32_t)N - bt) % (2 * (uint32_t)N)), acc + N, N);
+  or_br_loop(P, lwe, bsk, fbsk, acc, kind);
+}
+
+/* The CMux loop shared by both blind rotations (accumulator already set). */
+static void or_br_loop(const or_params *P, const u64 *lwe, const u64 *bsk, const u64 *fbsk,
+                       u64 *acc, int kind) {
   int n = (int)P->n, N = (int)P->N, l = (int)P->pbs_level, beta = (int)P->pbs_base_log;
   size_t ggsw_words = (size_t)2 * l * 2 * N;
   u64 *rot = (u64 *)malloc((size_t)2 * N * sizeof(u64));
   u64 *diff = (u64 *)malloc((size_t)2 * N * sizeof(u64));
   u64 *prod = (u64 *)malloc((size_t)2 * N * sizeof(u64));
-
-  uint32_t bt = or_modswitch(lwe[n], N);
-  for (int j = 0; j < N; ++j) acc[j] = 0;
-  or_poly_monomial_mul(v, (int)((2 * (uint32_t)N - bt) % (2 * (uint32_t)N)), acc + N, N);
 
   u64 *fd = NULL, *fk = NULL, *fy = NULL;
   i64 *dg = NULL;
@@ -692,4 +701,228 @@ void or_pbs(const or_params *P, const u64 *lwe_in, const u64 *bsk, const u64 *ks
     free(big);
   }
   free(fbsk);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Lookup-protocol primitives: blind rotation of a ciphertext test           */
+/* polynomial, Galois automorphisms, GLWE key switching and the RLWE trace   */
+/* (Sec. 3.2 "Cryptographic Lookup Protocol", Steps 2-3 and Algorithm 1;     */
+/* Sec. 2.2.3 "RLWE Trace Computation").                                     */
+/* ------------------------------------------------------------------------- */
+
+enum {
+  OR_STREAM_AUTK_MASK = 9,
+  OR_STREAM_AUTK_NOISE = 10,
+  OR_STREAM_GLWE_ENC_MASK = 11,
+  OR_STREAM_GLWE_ENC_NOISE = 12
+};
+
+/* Blind rotation whose accumulator starts from a GLWE ciphertext instead of
+ * a trivial one: ACC = X^(-b~) (TP_A, TP_B), both components rotated, then the
+ * same CMux loop as or_blind_rotate.  The phase ends as
+ * X^(-(b~ - sum a~_i s_i)) phase(TP) up to noise: the coefficient of phase(TP)
+ * at the selected position moves to the constant term (the "BlindRot" of
+ * Sec. 3.2, Step 3, and the selection of Step 2). */
+void or_blind_rotate_glwe(const or_params *P, const u64 *lwe, const u64 *bsk, const u64 *fbsk,
+                          const u64 *tp, u64 *acc, int kind) {
+  int n = (int)P->n, N = (int)P->N;
+  uint32_t bt = or_modswitch(lwe[n], N);
+  int r0 = (int)((2 * (uint32_t)N - bt) % (2 * (uint32_t)N));
+  or_poly_monomial_mul(tp, r0, acc, N);
+  or_poly_monomial_mul(tp + N, r0, acc + N, N);
+  or_br_loop(P, lwe, bsk, fbsk, acc, kind);
+}
+
+/* Galois automorphism tau_d: a(X) -> a(X^d) in Z_p[X]/(X^N + 1), d odd.
+ * The monomial X^j goes to X^(j d mod 2N), and an exponent e >= N stands
+ * for -X^(e - N) since X^N = -1. */
+void or_automorphism(const u64 *a, int d, u64 *out, int N) {
+  for (int j = 0; j < N; ++j) out[j] = 0;
+  for (int j = 0; j < N; ++j) {
+    u64 e = ((u64)j * (u64)d) % (2 * (u64)N);
+    if (e < (u64)N)
+      out[e] = or_add(out[e], a[j]);
+    else
+      out[e - N] = or_sub(out[e - N], a[j]);
+  }
+}
+
+/* GLWE key switching (k = 1) with a key K for S' -> S, rows K[t] =
+ * (A_t, B_t), B_t = A_t S + E_t + S' g_t, laid out [t][c][x]:
+ *   out = (0, B') - sum_t Dec_t(A') * K[t]
+ * for an input (A', B') under S', with Dec the decomposition of
+ * or_decompose (levels, beta) applied coefficient-wise and digits taken mod p.
+ * Phase: B' - sum_t Dec_t(A') (S' g_t + E_t) = B' - A' S' + small, the same
+ * sign convention as or_keyswitch. */
+void or_glwe_keyswitch(int N, int levels, int beta, const u64 *ct, const u64 *ksk, u64 *out,
+                       int kind) {
+  u64 *digit = (u64 *)malloc((size_t)levels * N * sizeof(u64));
+  u64 *prod = (u64 *)malloc((size_t)N * sizeof(u64));
+  u64 *res = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+  i64 *dg = (i64 *)malloc((size_t)levels * sizeof(i64));
+  for (int x = 0; x < N; ++x) {
+    or_decompose(ct[x], levels, beta, dg);
+    for (int t = 0; t < levels; ++t) digit[(size_t)t * N + x] = or_from_i64(dg[t]);
+  }
+  for (int x = 0; x < N; ++x) {
+    res[x] = 0;
+    res[N + x] = ct[N + x];
+  }
+  for (int t = 0; t < levels; ++t)
+    for (int c = 0; c < 2; ++c) {
+      or_polymul(digit + (size_t)t * N, ksk + ((size_t)t * 2 + c) * N, prod, N, kind);
+      for (int x = 0; x < N; ++x) res[(size_t)c * N + x] = or_sub(res[(size_t)c * N + x], prod[x]);
+    }
+  memcpy(out, res, (size_t)2 * N * sizeof(u64));
+  free(digit);
+  free(prod);
+  free(res);
+  free(dg);
+}
+
+/* Number of trace rounds, log2 N. */
+static int or_trace_rounds(int N) { return or_log2(N); }
+
+size_t or_autk_words(int N, int levels) {
+  return (size_t)or_trace_rounds(N) * levels * 2 * N;
+}
+
+/* Automorphism (trace) keys: for k = 1 .. log2 N, with d_k = 2^k + 1, the
+ * rows autk[k-1][t] = GLWE_S(tau_dk(S) g_t) (t < levels, g_t = 2^(64-(t+1)
+ * beta)), laid out [k-1][t][c][x].  Randomness: row r = (k-1) levels + t,
+ *   mask coefficient x : stream 9, word r N + x
+ *   noise coefficient x: stream 10, Gaussian number r N + x (sigma). */
+void or_autk_keygen(u64 seed, int N, int levels, int beta, double sigma, const u64 *glwe_key,
+                    u64 *autk) {
+  int rounds = or_trace_rounds(N);
+  u64 km = or_stream_key(seed, OR_STREAM_AUTK_MASK);
+  u64 kn = or_stream_key(seed, OR_STREAM_AUTK_NOISE);
+  int nrows = rounds * levels;
+#pragma omp parallel
+  {
+    u64 *as = (u64 *)malloc((size_t)N * sizeof(u64));
+    u64 *ts = (u64 *)malloc((size_t)N * sizeof(u64));
+#pragma omp for schedule(static)
+    for (int r = 0; r < nrows; ++r) {
+      int k = r / levels + 1, t = r % levels;
+      int d = (1 << k) + 1;
+      u64 *A = autk + (size_t)r * 2 * N, *B = A + N;
+      for (int x = 0; x < N; ++x) A[x] = or_uniform(km, (u64)r * (u64)N + (u64)x);
+      or_polymul_ntt(A, glwe_key, as, N);
+      or_automorphism(glwe_key, d, ts, N);
+      u64 g = or_gadget(t, beta);
+      for (int x = 0; x < N; ++x) {
+        u64 b = or_add(as[x], or_noise(kn, (u64)r * (u64)N + (u64)x, sigma));
+        B[x] = or_add(b, or_mul(ts[x], g));
+      }
+    }
+    free(as);
+    free(ts);
+  }
+}
+
+/* RLWE trace (Sec. 2.2.3): keeps the constant coefficient of the phase and
+ * cancels the others.  The sum of tau_d(a) over all d in (Z/2N)^* is
+ * N a_0; it is taken as a tower of log2 N doublings
+ *   c <- c + tau_d(c),  d = N + 1, N/2 + 1, ..., 3  (d = 2^k + 1, k = log2 N .. 1),
+ * each tau_d(c) brought back under S by GLWE key switching with autk[k-1].
+ * The factor N^-1 mod p is applied first, so that the phase of the result is
+ * phase(c)_0 plus the key-switching noise only (applying it last would
+ * multiply that noise by N^-1 mod p, which is not small). */
+void or_trace(int N, int levels, int beta, const u64 *ct, const u64 *autk, u64 *out, int kind) {
+  int rounds = or_trace_rounds(N);
+  u64 ninv = or_inv((u64)N);
+  u64 *c = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+  u64 *t = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+  u64 *ks = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+  for (int j = 0; j < 2 * N; ++j) c[j] = or_mul(ct[j], ninv);
+  for (int k = rounds; k >= 1; --k) {
+    int d = (1 << k) + 1;
+    or_automorphism(c, d, t, N);
+    or_automorphism(c + N, d, t + N, N);
+    or_glwe_keyswitch(N, levels, beta, t, autk + (size_t)(k - 1) * levels * 2 * N, ks, kind);
+    for (int j = 0; j < 2 * N; ++j) c[j] = or_add(c[j], ks[j]);
+  }
+  memcpy(out, c, (size_t)2 * N * sizeof(u64));
+  free(c);
+  free(t);
+  free(ks);
+}
+
+/* GLWE encryption (k = 1) of plaintext polynomials already scaled into Z_p:
+ *   A uniform (stream 11, word q N + x), E Gaussian (stream 12, number
+ *   q N + x), B = A S + M + E. */
+void or_glwe_encrypt(u64 seed, int N, double sigma, const u64 *glwe_key, const u64 *msg,
+                     size_t count, u64 *out) {
+  u64 km = or_stream_key(seed, OR_STREAM_GLWE_ENC_MASK);
+  u64 kn = or_stream_key(seed, OR_STREAM_GLWE_ENC_NOISE);
+#pragma omp parallel
+  {
+    u64 *as = (u64 *)malloc((size_t)N * sizeof(u64));
+#pragma omp for schedule(static)
+    for (long q = 0; q < (long)count; ++q) {
+      u64 *A = out + (size_t)q * 2 * N, *B = A + N;
+      for (int x = 0; x < N; ++x) A[x] = or_uniform(km, (u64)q * (u64)N + (u64)x);
+      or_polymul_ntt(A, glwe_key, as, N);
+      for (int x = 0; x < N; ++x) {
+        u64 b = or_add(as[x], msg[(size_t)q * N + x]);
+        B[x] = or_add(b, or_noise(kn, (u64)q * (u64)N + (u64)x, sigma));
+      }
+    }
+    free(as);
+  }
+}
+
+/* Plaintext-ciphertext "linear mapping" of Sec. 3.2 (Construct): for a
+ * ciphertext (A, B) and plaintext polynomials pa, pb,
+ *   out = (pa * A, pa * B + pb),
+ * whose phase is pa * phase(ct) + pb. */
+void or_glwe_mul_plain(int N, const u64 *ct, const u64 *pa, const u64 *pb, u64 *out, int kind) {
+  u64 *prod = (u64 *)malloc((size_t)N * sizeof(u64));
+  or_polymul(pa, ct, prod, N, kind);
+  u64 *tmp = (u64 *)malloc((size_t)2 * N * sizeof(u64));
+  memcpy(tmp, prod, (size_t)N * sizeof(u64));
+  or_polymul(pa, ct + N, prod, N, kind);
+  for (int x = 0; x < N; ++x) tmp[N + x] = or_add(prod[x], pb ? pb[x] : 0);
+  memcpy(out, tmp, (size_t)2 * N * sizeof(u64));
+  free(prod);
+  free(tmp);
+}
+
+/* Recombination of Sec. 3.2, Step 3 (Phase 2 construct):
+ *   R = sum_{s < count} X^s r_s  (both components). */
+void or_glwe_recombine(int N, const u64 *cts, int count, u64 *out) {
+  u64 *tmp = (u64 *)malloc((size_t)N * sizeof(u64));
+  for (int j = 0; j < 2 * N; ++j) out[j] = 0;
+  for (int s = 0; s < count; ++s)
+    for (int u = 0; u < 2; ++u) {
+      or_poly_monomial_mul(cts + ((size_t)s * 2 + u) * N, s, tmp, N);
+      for (int j = 0; j < N; ++j) out[(size_t)u * N + j] = or_add(out[(size_t)u * N + j], tmp[j]);
+    }
+  free(tmp);
+}
+
+/* Batched forms (independent items over OpenMP threads). */
+void or_blind_rotate_glwe_batch(const or_params *P, const u64 *lwe, const u64 *bsk, const u64 *tp,
+                                u64 *acc, size_t count, int kind, int nthreads) {
+  int n = (int)P->n, N = (int)P->N;
+  int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+  u64 *fbsk = NULL;
+  if (kind == OR_NTT) {
+    fbsk = (u64 *)malloc(or_bsk_words(P) * sizeof(u64));
+    or_bsk_transform(P, bsk, fbsk, nt);
+  }
+#pragma omp parallel for num_threads(nt) schedule(dynamic, 1)
+  for (long q = 0; q < (long)count; ++q)
+    or_blind_rotate_glwe(P, lwe + (size_t)q * (n + 1), bsk, fbsk, tp + (size_t)q * 2 * N,
+                         acc + (size_t)q * 2 * N, kind);
+  free(fbsk);
+}
+
+void or_trace_batch(int N, int levels, int beta, const u64 *ct, const u64 *autk, u64 *out,
+                    size_t count, int kind, int nthreads) {
+  int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#pragma omp parallel for num_threads(nt) schedule(dynamic, 1)
+  for (long q = 0; q < (long)count; ++q)
+    or_trace(N, levels, beta, ct + (size_t)q * 2 * N, autk, out + (size_t)q * 2 * N, kind);
 }

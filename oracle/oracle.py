@@ -102,6 +102,21 @@ def _declare(L):
         "or_keyswitch": (None, [_pp, _u64p, _u64p, _u64p]),
         "or_pbs": (None, [_pp, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p, C.c_size_t,
                           C.c_int, C.c_int]),
+        "or_blind_rotate_glwe": (None, [_pp, _u64p, _u64p, _u64p, _u64p, _u64p, C.c_int]),
+        "or_automorphism": (None, [_u64p, C.c_int, _u64p, C.c_int]),
+        "or_glwe_keyswitch": (None, [C.c_int, C.c_int, C.c_int, _u64p, _u64p, _u64p, C.c_int]),
+        "or_autk_words": (C.c_size_t, [C.c_int, C.c_int]),
+        "or_autk_keygen": (None, [C.c_uint64, C.c_int, C.c_int, C.c_int, C.c_double, _u64p,
+                                  _u64p]),
+        "or_trace": (None, [C.c_int, C.c_int, C.c_int, _u64p, _u64p, _u64p, C.c_int]),
+        "or_glwe_encrypt": (None, [C.c_uint64, C.c_int, C.c_double, _u64p, _u64p, C.c_size_t,
+                                   _u64p]),
+        "or_glwe_mul_plain": (None, [C.c_int, _u64p, _u64p, _u64p, _u64p, C.c_int]),
+        "or_glwe_recombine": (None, [C.c_int, _u64p, C.c_int, _u64p]),
+        "or_blind_rotate_glwe_batch": (None, [_pp, _u64p, _u64p, _u64p, _u64p, C.c_size_t,
+                                              C.c_int, C.c_int]),
+        "or_trace_batch": (None, [C.c_int, C.c_int, C.c_int, _u64p, _u64p, _u64p, C.c_size_t,
+                                  C.c_int, C.c_int]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -306,3 +321,93 @@ def pbs(params: Params, lwe_in, bsk, ksk, v, kind=NTT, nthreads=0,
     if want_acc:
         res.append(acc)
     return res[0] if len(res) == 1 else tuple(res)
+
+
+# --------------------------------------------------------------------------
+# lookup-protocol primitives (Sec. 3.2, Sec. 2.2.3)
+# --------------------------------------------------------------------------
+
+def blind_rotate_glwe(params: Params, lwe, bsk, tp, kind=SCHOOLBOOK) -> np.ndarray:
+    """Blind rotation of one GLWE test-polynomial ciphertext tp [2N]."""
+    lwe, bsk, tp = _u64(lwe), _u64(bsk), _u64(tp)
+    acc = np.zeros(2 * params.N, dtype=np.uint64)
+    lib().or_blind_rotate_glwe(C.byref(params), _ptr(lwe), _ptr(bsk), None, _ptr(tp), _ptr(acc),
+                               kind)
+    return acc
+
+
+def blind_rotate_glwe_batch(params: Params, lwe, bsk, tp, kind=NTT, nthreads=0) -> np.ndarray:
+    lwe = _u64(lwe).reshape(-1, params.n + 1)
+    count = lwe.shape[0]
+    tp = _u64(tp).reshape(count, 2 * params.N)
+    acc = np.zeros((count, 2 * params.N), dtype=np.uint64)
+    lib().or_blind_rotate_glwe_batch(C.byref(params), _ptr(lwe), _ptr(_u64(bsk)), _ptr(tp),
+                                     _ptr(acc), count, kind, nthreads)
+    return acc
+
+
+def automorphism(a, d: int) -> np.ndarray:
+    a = _u64(a)
+    out = np.zeros_like(a)
+    lib().or_automorphism(_ptr(a), d, _ptr(out), a.shape[0])
+    return out
+
+
+def glwe_keyswitch(N: int, levels: int, beta: int, ct, ksk, kind=SCHOOLBOOK) -> np.ndarray:
+    ct, ksk = _u64(ct), _u64(ksk)
+    out = np.zeros(2 * N, dtype=np.uint64)
+    lib().or_glwe_keyswitch(N, levels, beta, _ptr(ct), _ptr(ksk), _ptr(out), kind)
+    return out
+
+
+def autk_words(N: int, levels: int) -> int:
+    return lib().or_autk_words(N, levels)
+
+
+def autk_keygen(seed: int, N: int, levels: int, beta: int, sigma: float, glwe_key) -> np.ndarray:
+    S = _u64(glwe_key)
+    out = np.zeros(autk_words(N, levels), dtype=np.uint64)
+    lib().or_autk_keygen(seed, N, levels, beta, sigma, _ptr(S), _ptr(out))
+    return out
+
+
+def trace(N: int, levels: int, beta: int, ct, autk, kind=SCHOOLBOOK) -> np.ndarray:
+    ct, autk = _u64(ct), _u64(autk)
+    out = np.zeros(2 * N, dtype=np.uint64)
+    lib().or_trace(N, levels, beta, _ptr(ct), _ptr(autk), _ptr(out), kind)
+    return out
+
+
+def trace_batch(N: int, levels: int, beta: int, cts, autk, kind=NTT, nthreads=0) -> np.ndarray:
+    cts = _u64(cts).reshape(-1, 2 * N)
+    out = np.zeros_like(cts)
+    lib().or_trace_batch(N, levels, beta, _ptr(cts), _ptr(_u64(autk)), _ptr(out), cts.shape[0],
+                         kind, nthreads)
+    return out
+
+
+def glwe_encrypt(seed: int, sigma: float, glwe_key, msgs) -> np.ndarray:
+    """GLWE encryptions of plaintext polynomials msgs [count][N] (scaled into Z_p)."""
+    S = _u64(glwe_key)
+    N = S.shape[0]
+    msgs = _u64(msgs).reshape(-1, N)
+    out = np.zeros((msgs.shape[0], 2 * N), dtype=np.uint64)
+    lib().or_glwe_encrypt(seed, N, sigma, _ptr(S), _ptr(msgs), msgs.shape[0], _ptr(out))
+    return out
+
+
+def glwe_mul_plain(ct, pa, pb=None, kind=SCHOOLBOOK) -> np.ndarray:
+    ct, pa = _u64(ct), _u64(pa)
+    N = pa.shape[0]
+    out = np.zeros(2 * N, dtype=np.uint64)
+    pbp = None if pb is None else _u64(pb)
+    lib().or_glwe_mul_plain(N, _ptr(ct), _ptr(pa), _ptr(pbp), _ptr(out), kind)
+    return out
+
+
+def glwe_recombine(cts) -> np.ndarray:
+    cts = _u64(cts)
+    count, twoN = cts.shape
+    out = np.zeros(twoN, dtype=np.uint64)
+    lib().or_glwe_recombine(twoN // 2, _ptr(cts), count, _ptr(out))
+    return out
