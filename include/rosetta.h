@@ -184,6 +184,75 @@ rosetta_status rosetta_ntt_inverse(const uint64_t *in, uint64_t *out, size_t cou
 rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *c, size_t count,
                                 uint32_t N, void *stream);
 
+/* ---- lookup-protocol primitives (Sec. 3.2 "Cryptographic Lookup Protocol",
+ * Steps 2-3 and Algorithm 1; Sec. 2.2.3 "RLWE Trace Computation") ---------
+ *
+ * CONVENTIONS (beyond those above):
+ *  - Galois automorphism tau_d (d odd): a(X) -> a(X^d); X^j goes to
+ *    X^(j d mod 2N), an exponent e >= N standing for -X^(e-N).
+ *  - GLWE key switching with a key K for S' -> S, rows K[t] = GLWE_S(S' g_t):
+ *    (A', B') -> (0, B') - sum_t Dec_t(A') * K[t]  (Dec as for the
+ *    bootstrapping key, with the trace's own level and base_log).
+ *  - Trace: c <- N^-1 c (mod p) first; then for k = log2 N down to 1,
+ *    d = 2^k + 1: c <- c + KS_d(tau_d(c)).  The phase of the result is the
+ *    constant coefficient of the phase of c (plus key-switching noise), all
+ *    other coefficients cancel.
+ *  - Automorphism key (standard layout) [k-1 < log2 N][t < level][c < 2][x < N]:
+ *    row (k-1, t) is a GLWE encryption under S of tau_(2^k+1)(S) g_t. */
+
+/* Blind rotation of ciphertext test polynomials (Sec. 3.2, Step 3
+ * "BlindRot" and the selection of Step 2): for every ciphertext q of the
+ * batch, ACC = X^(-b~) glwe_tp[q] (both components), then the CMux loop of
+ * rosetta_blind_rotate.  glwe_tp [batch][2N] (device, one GLWE ciphertext
+ * under the GLWE key per LWE ciphertext).  extract = 0: out [batch][2N]
+ * holds the accumulators; extract != 0: out [batch][N+1] holds their sample
+ * extractions (then rosetta_keyswitch completes a PBS whose table is
+ * encrypted).  out must not overlap the inputs. */
+rosetta_status rosetta_blind_rotate_glwe(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                         const uint64_t *glwe_tp, uint64_t *out, size_t batch,
+                                         const rosetta_params *params, int extract,
+                                         void *stream);
+
+/* Words of an automorphism key with `level` gadget levels: log2(N) level 2 N. */
+size_t rosetta_autk_words(const rosetta_params *params, uint32_t level);
+
+/* Automorphism key, standard layout -> library layout (device buffers of
+ * rosetta_autk_words words each, not overlapping): every row to the
+ * transform domain, scaled by N^-1.  Only params->N is used beyond the
+ * usual validation. */
+rosetta_status rosetta_autk_prepare(const uint64_t *autk_std_dev, uint64_t *autk_dev,
+                                    const rosetta_params *params, uint32_t level, void *stream);
+
+/* RLWE trace (Sec. 2.2.3) of glwe_in [batch][2N] into glwe_out [batch][2N]
+ * (device; the two may be the same buffer, not partially overlapping), with
+ * a prepared automorphism key.  Supported: 1 <= level <= 4,
+ * base_log <= 30, level*base_log <= 62. */
+rosetta_status rosetta_trace(const uint64_t *glwe_in, const uint64_t *autk_dev,
+                             uint64_t *glwe_out, size_t batch, const rosetta_params *params,
+                             uint32_t level, uint32_t base_log, void *stream);
+
+/* Plaintext polynomials [count][N] (coefficients, device) -> the prepared
+ * form that rosetta_glwe_mul_plain multiplies by (transform domain, N^-1,
+ * library order), into a separate buffer of the same size. */
+rosetta_status rosetta_plain_prepare(const uint64_t *plain_dev, uint64_t *plain_prep_dev,
+                                     size_t count, uint32_t N, void *stream);
+
+/* Plaintext-ciphertext products (Sec. 3.2, "Construct": the linear mapping
+ * p(X) [[x]] + q(X)): for ciphertext q of glwe_in [batch][2N] and plaintext
+ * s < npoly, glwe_out[q][s] = (pa_s * A_q, pa_s * B_q + pb_s), so that
+ * phase(out) = pa_s * phase(in) + pb_s.  pa_prep_dev [npoly][N] from
+ * rosetta_plain_prepare; pb_dev [npoly][N] coefficients, or NULL for none.
+ * glwe_out [batch][npoly][2N] must not overlap the inputs. */
+rosetta_status rosetta_glwe_mul_plain(const uint64_t *glwe_in, const uint64_t *pa_prep_dev,
+                                      const uint64_t *pb_dev, uint64_t *glwe_out, size_t batch,
+                                      uint32_t npoly, uint32_t N, void *stream);
+
+/* Recombination (Sec. 3.2, Step 3 Phase 2): glwe_out[q] = sum_{s < nseg}
+ * X^s glwe_in[q][s], glwe_in [batch][nseg][2N], glwe_out [batch][2N]
+ * (device, not overlapping). */
+rosetta_status rosetta_glwe_recombine(const uint64_t *glwe_in, uint64_t *glwe_out, size_t batch,
+                                      uint32_t nseg, uint32_t N, void *stream);
+
 /* ---- test helpers: host memory, deterministic from the seed ------------ */
 
 /* Binary keys and the two switching keys in standard layout (host arrays of
@@ -215,6 +284,26 @@ rosetta_status rosetta_lwe_decrypt(const rosetta_params *params, const uint64_t 
 /* Test polynomial [N] for a table of M entries in Z_2M (host). */
 rosetta_status rosetta_lut_build(const rosetta_params *params, const uint32_t *table,
                                  uint64_t *test_poly);
+
+/* GLWE encryption (host) of `count` plaintext polynomials msgs [count][N],
+ * already scaled into Z_p, under the GLWE key: mask coefficient x of
+ * ciphertext q from stream 11 word q*N+x, noise from stream 12 Gaussian
+ * q*N+x; B = A*S + M + E.  out [count][2N]. */
+rosetta_status rosetta_glwe_encrypt(uint64_t seed, const rosetta_params *params, double sigma,
+                                    const uint64_t *glwe_key, const uint64_t *msgs, size_t count,
+                                    uint64_t *glwe_out);
+
+/* Phases B - A*S of `count` GLWE ciphertexts [count][2N] (host). */
+rosetta_status rosetta_glwe_phase(const rosetta_params *params, const uint64_t *glwe_key,
+                                  const uint64_t *glwe, size_t count, uint64_t *phase_out);
+
+/* Automorphism key in standard layout (host, rosetta_autk_words words):
+ * row r = (k-1) level + t encrypts tau_(2^k+1)(S) g_t, g_t = 2^(64-(t+1)
+ * base_log), mask coefficient x from stream 9 word r*N+x, noise from
+ * stream 10 Gaussian r*N+x. */
+rosetta_status rosetta_autk_keygen(uint64_t seed, const rosetta_params *params, uint32_t level,
+                                   uint32_t base_log, double sigma, const uint64_t *glwe_key,
+                                   uint64_t *autk_std);
 
 /* Release the library's device state on every device it touched (twiddle
  * tables, workspaces).  The library re-initialises lazily afterwards. */

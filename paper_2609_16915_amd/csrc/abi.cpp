@@ -295,7 +295,7 @@ rosetta_status rosetta_pbs_batch_ws(const uint64_t *lwe_in, const uint64_t *bsk_
   if ((st = get_tables(params->N, tb))) return st;
   uint64_t *big = (uint64_t *)workspace;
   hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, lut, big, batch, *params, tb, BR_EXTRACT,
-                                     (hipStream_t)stream);
+                                     false, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "blind_rotate launch");
   e = launch_keyswitch(big, ksk_dev, lwe_out, batch, *params, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "keyswitch launch");
@@ -329,7 +329,7 @@ rosetta_status rosetta_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_
   Tables tb;
   if ((st = get_tables(params->N, tb))) return st;
   hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, lut, glwe_out, batch, *params, tb, BR_GLWE,
-                                     (hipStream_t)stream);
+                                     false, (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "blind_rotate launch");
 }
 
@@ -346,7 +346,7 @@ rosetta_status rosetta_blind_rotate_extract(const uint64_t *lwe_in, const uint64
   Tables tb;
   if ((st = get_tables(params->N, tb))) return st;
   hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, lut, big_out, batch, *params, tb,
-                                     BR_EXTRACT, (hipStream_t)stream);
+                                     BR_EXTRACT, false, (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "blind_rotate launch");
 }
 
@@ -408,6 +408,133 @@ rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *
   if ((st = get_tables(N, tb))) return st;
   hipError_t e = launch_poly_mul(a, b, c, count, N, tb, (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "poly_mul launch");
+}
+
+// ---- lookup-protocol primitives -----------------------------------------
+
+rosetta_status rosetta_blind_rotate_glwe(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                         const uint64_t *glwe_tp, uint64_t *out, size_t batch,
+                                         const rosetta_params *params, int extract,
+                                         void *stream) {
+  rosetta_status st = check_params(params);
+  if (st) return st;
+  if (batch == 0) return ok();
+  if (!lwe_in || !bsk_dev || !glwe_tp || !out)
+    return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t N = params->N;
+  const size_t out_bytes = batch * (extract ? N + 1 : 2 * N) * 8;
+  if (any_overlap(out, out_bytes, lwe_in, lwe_words(params, batch) * 8) ||
+      any_overlap(out, out_bytes, glwe_tp, batch * 2 * N * 8) ||
+      any_overlap(out, out_bytes, bsk_dev, rosetta_bsk_words(params) * 8))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps an input");
+  Tables tb;
+  if ((st = get_tables(params->N, tb))) return st;
+  hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, glwe_tp, out, batch, *params, tb,
+                                     extract ? BR_EXTRACT : BR_GLWE, true, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "blind_rotate_glwe launch");
+}
+
+static rosetta_status check_trace_params(const rosetta_params *p, uint32_t level,
+                                         uint32_t base_log) {
+  rosetta_status st = check_params(p);
+  if (st) return st;
+  if (level < 1 || base_log < 1)
+    return fail(ROSETTA_ERR_PARAMS, "trace level and base_log must be >= 1");
+  if (level > 4 || base_log > 30 || level * base_log > 62)
+    return fail(ROSETTA_ERR_UNSUPPORTED,
+                "need trace level <= 4, base_log <= 30 and level*base_log <= 62");
+  return ROSETTA_OK;
+}
+
+size_t rosetta_autk_words(const rosetta_params *p, uint32_t level) {
+  return p ? (size_t)ilog2u(p->N) * level * 2 * p->N : 0;
+}
+
+rosetta_status rosetta_autk_prepare(const uint64_t *autk_std_dev, uint64_t *autk_dev,
+                                    const rosetta_params *params, uint32_t level,
+                                    void *stream) {
+  rosetta_status st = check_trace_params(params, level, 1);
+  if (st) return st;
+  if (!autk_std_dev || !autk_dev) return fail(ROSETTA_ERR_NULL, "autk pointer is NULL");
+  const size_t words = rosetta_autk_words(params, level);
+  if (any_overlap(autk_std_dev, words * 8, autk_dev, words * 8))
+    return fail(ROSETTA_ERR_ALIAS, "autk_std_dev and autk_dev overlap");
+  Tables tb;
+  if ((st = get_tables(params->N, tb))) return st;
+  hipError_t e = launch_rows_prepare(autk_std_dev, autk_dev, words / params->N, params->N, tb,
+                                     (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "autk_prepare launch");
+}
+
+rosetta_status rosetta_trace(const uint64_t *glwe_in, const uint64_t *autk_dev,
+                             uint64_t *glwe_out, size_t batch, const rosetta_params *params,
+                             uint32_t level, uint32_t base_log, void *stream) {
+  rosetta_status st = check_trace_params(params, level, base_log);
+  if (st) return st;
+  if (batch == 0) return ok();
+  if (!glwe_in || !autk_dev || !glwe_out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t bytes = batch * 2 * (size_t)params->N * 8;
+  if (partial_overlap(glwe_in, bytes, glwe_out, bytes))
+    return fail(ROSETTA_ERR_ALIAS, "glwe_in and glwe_out partially overlap");
+  if (any_overlap(glwe_out, bytes, autk_dev, rosetta_autk_words(params, level) * 8))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps the automorphism key");
+  Tables tb;
+  if ((st = get_tables(params->N, tb))) return st;
+  hipError_t e = launch_trace(glwe_in, autk_dev, glwe_out, batch, params->N, (int)level,
+                              (int)base_log, tb, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "trace launch");
+}
+
+rosetta_status rosetta_plain_prepare(const uint64_t *plain_dev, uint64_t *plain_prep_dev,
+                                     size_t count, uint32_t N, void *stream) {
+  rosetta_status st = check_ntt_args(plain_dev, plain_prep_dev, count, N);
+  if (st) return st;
+  if (count == 0) return ok();
+  if (any_overlap(plain_dev, count * (size_t)N * 8, plain_prep_dev, count * (size_t)N * 8))
+    return fail(ROSETTA_ERR_ALIAS, "plain_dev and plain_prep_dev overlap");
+  Tables tb;
+  if ((st = get_tables(N, tb))) return st;
+  hipError_t e = launch_rows_prepare(plain_dev, plain_prep_dev, count, N, tb,
+                                     (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "plain_prepare launch");
+}
+
+rosetta_status rosetta_glwe_mul_plain(const uint64_t *glwe_in, const uint64_t *pa_prep_dev,
+                                      const uint64_t *pb_dev, uint64_t *glwe_out, size_t batch,
+                                      uint32_t npoly, uint32_t N, void *stream) {
+  if (!is_pow2_in(N, 256, 4096))
+    return fail(ROSETTA_ERR_UNSUPPORTED, "N must be a power of two in [256, 4096]");
+  if (npoly < 1 || npoly > 4096) return fail(ROSETTA_ERR_PARAMS, "need 1 <= npoly <= 4096");
+  if (batch == 0) return ok();
+  if (!glwe_in || !pa_prep_dev || !glwe_out)
+    return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t in_bytes = batch * 2 * (size_t)N * 8, out_bytes = in_bytes * npoly;
+  const size_t pbytes = (size_t)npoly * N * 8;
+  if (any_overlap(glwe_out, out_bytes, glwe_in, in_bytes) ||
+      any_overlap(glwe_out, out_bytes, pa_prep_dev, pbytes) ||
+      (pb_dev && any_overlap(glwe_out, out_bytes, pb_dev, pbytes)))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps an input");
+  Tables tb;
+  rosetta_status st = get_tables(N, tb);
+  if (st) return st;
+  hipError_t e = launch_glwe_mul_plain(glwe_in, pa_prep_dev, pb_dev, glwe_out, batch, (int)npoly,
+                                       N, tb, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "glwe_mul_plain launch");
+}
+
+rosetta_status rosetta_glwe_recombine(const uint64_t *glwe_in, uint64_t *glwe_out, size_t batch,
+                                      uint32_t nseg, uint32_t N, void *stream) {
+  if (!is_pow2_in(N, 256, 4096))
+    return fail(ROSETTA_ERR_UNSUPPORTED, "N must be a power of two in [256, 4096]");
+  if (nseg < 1 || nseg > N) return fail(ROSETTA_ERR_PARAMS, "need 1 <= nseg <= N");
+  if (batch == 0) return ok();
+  if (!glwe_in || !glwe_out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t out_bytes = batch * 2 * (size_t)N * 8;
+  if (any_overlap(glwe_out, out_bytes, glwe_in, out_bytes * nseg))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps the input");
+  hipError_t e = launch_glwe_recombine(glwe_in, glwe_out, batch, (int)nseg, N,
+                                       (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "glwe_recombine launch");
 }
 
 rosetta_status rosetta_shutdown(void) {

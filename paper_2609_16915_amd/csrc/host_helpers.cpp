@@ -1,5 +1,6 @@
-// Host-side helpers of librosetta: key generation, LWE encryption and
-// decryption, and the test polynomial of a lookup table.  They produce test
+// Host-side helpers of librosetta: key generation (bootstrapping,
+// key-switching and automorphism keys), LWE and GLWE encryption, decryption
+// and phases, and the test polynomial of a lookup table.  They produce test
 // and benchmark inputs; none of them is on the PBS path.  The GLWE products
 // A*S of key generation use a host transform over the same field (merged
 // Cooley-Tukey forward, Gentleman-Sande inverse) and run over all host
@@ -33,7 +34,8 @@ inline u64 sm64(u64 key, u64 idx) {
 
 enum Stream : u64 {
   LWE_KEY = 1, GLWE_KEY = 2, BSK_MASK = 3, BSK_NOISE = 4,
-  KSK_MASK = 5, KSK_NOISE = 6, ENC_MASK = 7, ENC_NOISE = 8
+  KSK_MASK = 5, KSK_NOISE = 6, ENC_MASK = 7, ENC_NOISE = 8,
+  AUTK_MASK = 9, AUTK_NOISE = 10, GLWE_ENC_MASK = 11, GLWE_ENC_NOISE = 12
 };
 
 inline u64 substream(u64 seed, Stream s) { return sm64(seed, (u64)s); }
@@ -112,6 +114,30 @@ void parallel_rows(size_t rows, F &&f) {
       for (size_t r = w; r < rows; r += nt) f(r);
     });
   for (auto &t : th) t.join();
+}
+
+// a(X) -> a(X^d) modulo X^N + 1 (d odd).
+void automorphism(const u64 *a, u64 *out, int N, u64 d) {
+  for (int j = 0; j < N; ++j) {
+    const u64 e = ((u64)j * d) & (2 * (u64)N - 1);
+    if (e < (u64)N)
+      out[e] = a[j];
+    else
+      out[e - N] = gl_neg(a[j]);
+  }
+}
+
+// A * S for a GLWE key S already transformed (fS).
+void mul_by_key(const HostNtt &ntt, const u64 *A, const std::vector<u64> &fS, u64 *out) {
+  std::vector<u64> f(A, A + ntt.N);
+  ntt.forward(f.data());
+  for (int x = 0; x < ntt.N; ++x) f[x] = gl_mul(f[x], fS[x]);
+  ntt.inverse(f.data());
+  std::copy(f.begin(), f.end(), out);
+}
+
+bool ring_ok(const rosetta_params *p) {
+  return p && p->N >= 4 && p->N <= 65536 && (p->N & (p->N - 1)) == 0;
 }
 
 rosetta_status herr(rosetta_status st, const char *msg) {
@@ -220,6 +246,71 @@ rosetta_status rosetta_lut_build(const rosetta_params *p, const uint32_t *table,
   const u64 delta = GL_P / (2ull * M);
   for (int j = 0; j < N - h; ++j) test_poly[j] = gl_mul(delta, table[(j + h) / box]);
   for (int j = N - h; j < N; ++j) test_poly[j] = gl_neg(gl_mul(delta, table[0]));
+  return ROSETTA_OK;
+}
+
+rosetta_status rosetta_glwe_encrypt(uint64_t seed, const rosetta_params *p, double sigma,
+                                    const uint64_t *glwe_key, const uint64_t *msgs, size_t count,
+                                    uint64_t *out) {
+  if (!ring_ok(p)) return herr(p ? ROSETTA_ERR_PARAMS : ROSETTA_ERR_NULL, "need N a power of two");
+  if (!glwe_key || !msgs || !out) return herr(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const int N = (int)p->N;
+  HostNtt ntt(N);
+  std::vector<u64> fS(glwe_key, glwe_key + N);
+  ntt.forward(fS.data());
+  const u64 km = substream(seed, GLWE_ENC_MASK), kn = substream(seed, GLWE_ENC_NOISE);
+  parallel_rows(count, [&](size_t q) {
+    u64 *A = out + q * 2 * N, *B = A + N;
+    for (int x = 0; x < N; ++x) A[x] = uniform_zp(km, (u64)q * N + x);
+    mul_by_key(ntt, A, fS, B);
+    for (int x = 0; x < N; ++x)
+      B[x] = gl_add(gl_add(B[x], msgs[q * N + x]), noise_zp(kn, (u64)q * N + x, sigma));
+  });
+  return ROSETTA_OK;
+}
+
+rosetta_status rosetta_glwe_phase(const rosetta_params *p, const uint64_t *glwe_key,
+                                  const uint64_t *glwe, size_t count, uint64_t *phase_out) {
+  if (!ring_ok(p)) return herr(p ? ROSETTA_ERR_PARAMS : ROSETTA_ERR_NULL, "need N a power of two");
+  if (!glwe_key || !glwe || !phase_out) return herr(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const int N = (int)p->N;
+  HostNtt ntt(N);
+  std::vector<u64> fS(glwe_key, glwe_key + N);
+  ntt.forward(fS.data());
+  parallel_rows(count, [&](size_t q) {
+    const u64 *A = glwe + q * 2 * N, *B = A + N;
+    u64 *o = phase_out + q * N;
+    mul_by_key(ntt, A, fS, o);
+    for (int x = 0; x < N; ++x) o[x] = gl_sub(B[x], o[x]);
+  });
+  return ROSETTA_OK;
+}
+
+rosetta_status rosetta_autk_keygen(uint64_t seed, const rosetta_params *p, uint32_t level,
+                                   uint32_t base_log, double sigma, const uint64_t *glwe_key,
+                                   uint64_t *autk) {
+  if (!ring_ok(p)) return herr(p ? ROSETTA_ERR_PARAMS : ROSETTA_ERR_NULL, "need N a power of two");
+  if (!glwe_key || !autk) return herr(ROSETTA_ERR_NULL, "NULL pointer argument");
+  if (level < 1 || base_log < 1 || level * base_log > 62)
+    return herr(ROSETTA_ERR_PARAMS, "need level, base_log >= 1 and level*base_log <= 62");
+  const int N = (int)p->N;
+  int logn = 0;
+  while ((1 << logn) < N) ++logn;
+  HostNtt ntt(N);
+  std::vector<u64> fS(glwe_key, glwe_key + N);
+  ntt.forward(fS.data());
+  const u64 km = substream(seed, AUTK_MASK), kn = substream(seed, AUTK_NOISE);
+  parallel_rows((size_t)logn * level, [&](size_t r) {
+    const int k = (int)(r / level) + 1, t = (int)(r % level);
+    u64 *A = autk + r * 2 * N, *B = A + N;
+    std::vector<u64> ts(N);
+    automorphism(glwe_key, ts.data(), N, (1ull << k) + 1);
+    const u64 g = gl_pow(2, (u64)(64 - (t + 1) * (int)base_log));
+    for (int x = 0; x < N; ++x) A[x] = uniform_zp(km, (u64)r * N + x);
+    mul_by_key(ntt, A, fS, B);
+    for (int x = 0; x < N; ++x)
+      B[x] = gl_add(gl_add(B[x], noise_zp(kn, (u64)r * N + x, sigma)), gl_mul(ts[x], g));
+  });
   return ROSETTA_OK;
 }
 

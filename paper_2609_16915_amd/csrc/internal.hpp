@@ -36,7 +36,17 @@ hipError_t launch_ksk_prepare(const uint64_t *ksk_std, uint64_t *ksk_dev,
 hipError_t launch_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
                                const uint64_t *lut, uint64_t *out, size_t batch,
                                const rosetta_params &p, const Tables &tb, BrMode mode,
-                               hipStream_t st);
+                               bool tp_glwe, hipStream_t st);
+hipError_t launch_rows_prepare(const uint64_t *rows_std, uint64_t *rows_dev, size_t rows,
+                               uint32_t N, const Tables &tb, hipStream_t st);
+hipError_t launch_trace(const uint64_t *in, const uint64_t *autk_dev, uint64_t *out,
+                        size_t batch, uint32_t N, int level, int base_log, const Tables &tb,
+                        hipStream_t st);
+hipError_t launch_glwe_mul_plain(const uint64_t *in, const uint64_t *pa_dev, const uint64_t *pb,
+                                 uint64_t *out, size_t batch, int npoly, uint32_t N,
+                                 const Tables &tb, hipStream_t st);
+hipError_t launch_glwe_recombine(const uint64_t *in, uint64_t *out, size_t batch, int nseg,
+                                 uint32_t N, hipStream_t st);
 hipError_t launch_keyswitch(const uint64_t *big, const uint64_t *ksk_dev, uint64_t *out,
                             size_t batch, const rosetta_params &p, hipStream_t st);
 hipError_t launch_ntt(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,

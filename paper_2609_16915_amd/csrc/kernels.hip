@@ -184,11 +184,18 @@ size_t br_lds_bytes(int n) {
   return ntt_lds_bytes<S>() + (((size_t)(n + 1) * 2 + 15) & ~(size_t)15);
 }
 
+//
+// With tp_glwe = 0, `lut` is one test polynomial v shared by the batch and
+// the accumulator starts as the trivial ciphertext (0, X^(-b~) v).  With
+// tp_glwe = 1, `lut` holds one GLWE ciphertext [2][N] per ciphertext of the
+// batch (a test polynomial that is itself encrypted, as in the lookup
+// protocol's construct-then-select) and both of its components are rotated
+// by X^(-b~).
 template <class S, int L, typename RT, bool PF>
 __global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(br_waves_per_eu<S>())))
 k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
                const u64 *__restrict__ lut, u64 *__restrict__ out, int n, int beta, int mode,
-               const u64 *__restrict__ zeta) {
+               int tp_glwe, const u64 *__restrict__ zeta) {
   constexpr int N = S::N, E = S::E, T = S::T;
   u64 *tw = lds_dyn;
   LdsPair lds(lds_dyn + S::TW_WORDS, N);
@@ -205,10 +212,12 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
   u64 accA[E], accB[E];
   {
     const int r = (2 * N - (int)rot[n]) & (2 * N - 1);  // X^(-b~)
+    const u64 *tpA = lut + (tp_glwe ? ct * (size_t)(2 * N) : 0);
+    const u64 *tpB = tp_glwe ? tpA + N : lut;
 #pragma unroll
     for (int k = 0; k < E; ++k) {
-      accA[k] = 0;
-      accB[k] = rotated_coef<N>(lut, tid + T * k, r);
+      accA[k] = tp_glwe ? rotated_coef<N>(tpA, tid + T * k, r) : 0;
+      accB[k] = rotated_coef<N>(tpB, tid + T * k, r);
     }
   }
 
@@ -318,6 +327,195 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
       if (j == 0) o[N] = accB[k];
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// RLWE trace, plaintext products, recombination (lookup protocol)
+// ---------------------------------------------------------------------------
+
+// d^-1 modulo 2N for odd d: Newton's iteration x <- x (2 - d x) doubles the
+// number of correct low bits, starting from x = d (d^2 = 1 mod 8).
+__device__ __forceinline__ u32 odd_inverse_mod(u32 d, u32 two_n) {
+  u32 x = d;
+#pragma unroll
+  for (int it = 0; it < 4; ++it) x *= 2u - d * x;
+  return x & (two_n - 1);
+}
+
+// Coefficient j of tau_d(a) = a(X^d): with e = j d^-1 mod 2N, the source
+// is a_e (e < N) or -a_(e-N) (X^N = -1).  `a` is in natural layout in LDS.
+template <int N>
+__device__ __forceinline__ u64 automorphism_coef(const u64 *a, int j, u32 dinv) {
+  const u32 e = ((u32)j * dinv) & (2 * N - 1);
+  const u64 v = a[e & (N - 1)];
+  return e < (u32)N ? v : gl_neg(v);
+}
+
+// Trace of one GLWE ciphertext per workgroup (the RLWE trace of the lookup
+// protocol): c <- N^-1 c, then for k = log2 N down to 1 with d = 2^k + 1,
+//   c <- c + KS_d(tau_d(c)),
+//   KS_d(A', B') = (0, B') - sum_t Dec_t(A') . autk[k-1][t],
+// autk rows prepared like bootstrapping-key rows (transform domain, N^-1).
+// Per round: two automorphisms through LDS, L forward transforms of the
+// digit polynomials, 2L multiply-accumulates with the streamed key rows and
+// two inverse transforms; the ciphertext stays in registers throughout.
+template <class S, int L>
+__global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(br_waves_per_eu<S>())))
+k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restrict__ out,
+        int beta, const u64 *__restrict__ zeta, u64 ninv) {
+  constexpr int N = S::N, E = S::E, T = S::T;
+  u64 *tw = lds_dyn;
+  LdsPair lds(lds_dyn + S::TW_WORDS, N);
+  const int tid = threadIdx.x;
+  const size_t ct = blockIdx.x;
+  load_twiddles<S>(tw, zeta, tid);
+
+  u64 A[E], B[E];
+  {
+    const u64 *c = in + ct * (size_t)(2 * N);
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      A[k] = gl_mul(c[tid + T * k], ninv);
+      B[k] = gl_mul(c[N + tid + T * k], ninv);
+    }
+  }
+  __syncthreads();
+
+  const int s = 64 - L * beta;
+  constexpr size_t round_words = (size_t)L * 2 * N;
+#pragma unroll 1
+  for (int kr = S::LOGN; kr >= 1; --kr) {
+    const u32 dinv = odd_inverse_mod((1u << kr) + 1, 2 * N);
+    // B <- B + tau_d(B)
+    {
+      u64 *buf = lds.next();
+#pragma unroll
+      for (int k = 0; k < E; ++k) buf[tid + T * k] = B[k];
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < E; ++k) B[k] = gl_add(B[k], automorphism_coef<N>(buf, tid + T * k, dinv));
+    }
+    // rounded tau_d(A), the input of the decomposition
+    i64 R[E];
+    {
+      u64 *buf = lds.next();
+#pragma unroll
+      for (int k = 0; k < E; ++k) buf[tid + T * k] = A[k];
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < E; ++k) R[k] = gl_round_top(automorphism_coef<N>(buf, tid + T * k, dinv), s);
+    }
+    u64 Y0[E], Y1[E];
+#pragma unroll
+    for (int k = 0; k < E; ++k) Y0[k] = Y1[k] = 0;
+    gconst_u64 *G = as_global(autk) + (size_t)(kr - 1) * round_words + tid;
+#pragma unroll 1
+    for (int t = 0; t < L; ++t) {
+      u64 x[E];
+      if (beta <= 14) {
+        i64 d[E];
+#pragma unroll
+        for (int k = 0; k < E; ++k) d[k] = digit_of<L, i64>(R[k], beta, t);
+        ntt_forward_small<S, i64>(d, x, lds, tid, tw);
+      } else {
+#pragma unroll
+        for (int k = 0; k < E; ++k) x[k] = gl_from_i64(digit_of<L, i64>(R[k], beta, t));
+        ntt_forward<S>(x, lds, tid, tw);
+      }
+      gconst_u64 *g = G + (size_t)(t * 2) * N;
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        Y0[k] = gl_mul_add(x[k], g[k * T], Y0[k]);
+        Y1[k] = gl_mul_add(x[k], g[N + k * T], Y1[k]);
+      }
+    }
+#pragma unroll 1
+    for (int c = 0; c < 2; ++c) {
+      u64 y[E];
+#pragma unroll
+      for (int k = 0; k < E; ++k) y[k] = c ? Y1[k] : Y0[k];
+      ntt_inverse<S>(y, lds, tid, tw);
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        if (c)
+          B[k] = gl_sub(B[k], y[k]);
+        else
+          A[k] = gl_sub(A[k], y[k]);
+      }
+    }
+  }
+  u64 *o = out + ct * (size_t)(2 * N);
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    o[tid + T * k] = A[k];
+    o[N + tid + T * k] = B[k];
+  }
+}
+
+// Plaintext-ciphertext products (the "construct" of the lookup protocol):
+// for ciphertext q and plaintext s < npoly,
+//   out[q][s] = (pa_s * A_q, pa_s * B_q + pb_s),
+// pa_s prepared like a key row (transform domain, N^-1), pb_s in
+// coefficients (pb may be NULL).  One workgroup per ciphertext: both
+// components are transformed once and reused for every s.
+template <class S>
+__global__ void __launch_bounds__(S::T)
+k_glwe_mul_plain(const u64 *__restrict__ in, const u64 *__restrict__ pa,
+                 const u64 *__restrict__ pb, u64 *__restrict__ out, int npoly,
+                 const u64 *__restrict__ zeta) {
+  constexpr int N = S::N, E = S::E, T = S::T;
+  u64 *tw = lds_dyn;
+  LdsPair lds(lds_dyn + S::TW_WORDS, N);
+  const int tid = threadIdx.x;
+  const size_t ct = blockIdx.x;
+  load_twiddles<S>(tw, zeta, tid);
+  u64 fa[E], fb[E];
+  {
+    const u64 *c = in + ct * (size_t)(2 * N);
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      fa[k] = c[tid + T * k];
+      fb[k] = c[N + tid + T * k];
+    }
+  }
+  __syncthreads();
+  ntt_forward<S>(fa, lds, tid, tw);
+  ntt_forward<S>(fb, lds, tid, tw);
+#pragma unroll 1
+  for (int sp = 0; sp < npoly; ++sp) {
+    const u64 *w = pa + (size_t)sp * N + tid;
+    u64 *o = out + (ct * (size_t)npoly + sp) * (size_t)(2 * N);
+#pragma unroll 1
+    for (int c = 0; c < 2; ++c) {
+      u64 y[E];
+#pragma unroll
+      for (int k = 0; k < E; ++k) y[k] = gl_mul(c ? fb[k] : fa[k], w[k * T]);
+      ntt_inverse<S>(y, lds, tid, tw);
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        const int j = tid + T * k;
+        o[c * N + j] = (c && pb) ? gl_add(y[k], pb[(size_t)sp * N + j]) : y[k];
+      }
+    }
+  }
+}
+
+// Recombination: out[q] = sum_{s < nseg} X^s in[q][s] (both components).
+// One thread per output coefficient.
+__global__ void k_glwe_recombine(const u64 *__restrict__ in, u64 *__restrict__ out, size_t batch,
+                                 int nseg, int N) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t total = batch * 2 * (size_t)N;
+  if (i >= total) return;
+  const int j = (int)(i % N);
+  const size_t qc = i / N;  // q * 2 + c
+  const size_t q = qc / 2, c = qc % 2;
+  u64 acc = 0;
+  for (int s = 0; s < nseg; ++s) {
+    const u64 v = in[((q * nseg + s) * 2 + c) * N + ((j - s) & (N - 1))];
+    acc = j >= s ? gl_add(acc, v) : gl_sub(acc, v);
+  }
+  out[i] = acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -469,26 +667,27 @@ template <class S, int L>
 static hipError_t launch_br_levels(const uint64_t *lwe_in, const uint64_t *bsk_dev,
                                    const uint64_t *lut, uint64_t *out, size_t batch,
                                    const rosetta_params &p, const Tables &tb, int mode,
-                                   hipStream_t st) {
+                                   int tp_glwe, hipStream_t st) {
   const int n = (int)p.n, beta = (int)p.pbs_base_log;
   const size_t lds = br_lds_bytes<S>(n);
   if (L * beta <= 30)
     ROSETTA_LAUNCH((k_blind_rotate<S, L, int32_t, BR_PREFETCH>), dim3(batch), dim3(S::T), lds,
-                   st, lwe_in, bsk_dev, lut, out, n, beta, mode, tb.zeta);
+                   st, lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);
   else
     ROSETTA_LAUNCH((k_blind_rotate<S, L, int64_t, BR_PREFETCH>), dim3(batch), dim3(S::T), lds,
-                   st, lwe_in, bsk_dev, lut, out, n, beta, mode, tb.zeta);
+                   st, lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);
   return hipSuccess;
 }
 
 hipError_t launch_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
                                const uint64_t *lut, uint64_t *out, size_t batch,
                                const rosetta_params &p, const Tables &tb, BrMode mode,
-                               hipStream_t st) {
+                               bool tp_glwe, hipStream_t st) {
   hipError_t e = hipSuccess;
-#define ROSETTA_BR_L(LV)                                                                  \
-  case LV:                                                                                \
-    e = launch_br_levels<S, LV>(lwe_in, bsk_dev, lut, out, batch, p, tb, (int)mode, st); \
+  const int tpg = tp_glwe ? 1 : 0;
+#define ROSETTA_BR_L(LV)                                                                       \
+  case LV:                                                                                     \
+    e = launch_br_levels<S, LV>(lwe_in, bsk_dev, lut, out, batch, p, tb, (int)mode, tpg, st); \
     break;
   ROSETTA_DISPATCH_N(ilog2(p.N), switch (p.pbs_level) {
     ROSETTA_BR_L(1) ROSETTA_BR_L(2) ROSETTA_BR_L(3) ROSETTA_BR_L(4)
@@ -496,6 +695,48 @@ hipError_t launch_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
   });
 #undef ROSETTA_BR_L
   if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_prepare(const uint64_t *rows_std, uint64_t *rows_dev, size_t rows,
+                               uint32_t N, const Tables &tb, hipStream_t st) {
+  ROSETTA_DISPATCH_N(ilog2(N), ROSETTA_LAUNCH(k_bsk_prepare<S>, dim3(rows), dim3(S::T),
+                                              ntt_lds_bytes<S>(), st, rows_std, rows_dev,
+                                              tb.zeta, tb.ninv));
+  return hipGetLastError();
+}
+
+hipError_t launch_trace(const uint64_t *in, const uint64_t *autk_dev, uint64_t *out,
+                        size_t batch, uint32_t N, int level, int base_log, const Tables &tb,
+                        hipStream_t st) {
+#define ROSETTA_TR_L(LV)                                                                 \
+  case LV:                                                                               \
+    ROSETTA_LAUNCH((k_trace<S, LV>), dim3(batch), dim3(S::T), ntt_lds_bytes<S>(), st, in, \
+                   autk_dev, out, base_log, tb.zeta, tb.ninv);                           \
+    break;
+  ROSETTA_DISPATCH_N(ilog2(N), switch (level) {
+    ROSETTA_TR_L(1) ROSETTA_TR_L(2) ROSETTA_TR_L(3) ROSETTA_TR_L(4)
+    default: return hipErrorInvalidValue;
+  });
+#undef ROSETTA_TR_L
+  return hipGetLastError();
+}
+
+hipError_t launch_glwe_mul_plain(const uint64_t *in, const uint64_t *pa_dev, const uint64_t *pb,
+                                 uint64_t *out, size_t batch, int npoly, uint32_t N,
+                                 const Tables &tb, hipStream_t st) {
+  ROSETTA_DISPATCH_N(ilog2(N), ROSETTA_LAUNCH(k_glwe_mul_plain<S>, dim3(batch), dim3(S::T),
+                                              ntt_lds_bytes<S>(), st, in, pa_dev, pb, out,
+                                              npoly, tb.zeta));
+  return hipGetLastError();
+}
+
+hipError_t launch_glwe_recombine(const uint64_t *in, uint64_t *out, size_t batch, int nseg,
+                                 uint32_t N, hipStream_t st) {
+  const size_t total = batch * 2 * (size_t)N;
+  const unsigned blocks = (unsigned)((total + 255) / 256);
+  hipLaunchKernelGGL(k_glwe_recombine, dim3(blocks), dim3(256), 0, st, in, out, batch, nseg,
+                     (int)N);
   return hipGetLastError();
 }
 

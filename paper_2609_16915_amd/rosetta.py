@@ -80,6 +80,22 @@ SIGNATURES = {
     "rosetta_lwe_decrypt": (_ST, [_pp, _u64p, C.c_uint32, _u64p, C.c_size_t, _u64p]),
     "rosetta_lut_build": (_ST, [_pp, _u64p, _u64p]),
     "rosetta_shutdown": (_ST, []),
+    "rosetta_blind_rotate_glwe": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp, C.c_int,
+                                        C.c_void_p]),
+    "rosetta_autk_words": (C.c_size_t, [_pp, C.c_uint32]),
+    "rosetta_autk_prepare": (_ST, [_u64p, _u64p, _pp, C.c_uint32, C.c_void_p]),
+    "rosetta_trace": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, _pp, C.c_uint32, C.c_uint32,
+                            C.c_void_p]),
+    "rosetta_plain_prepare": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
+    "rosetta_glwe_mul_plain": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, C.c_uint32,
+                                     C.c_uint32, C.c_void_p]),
+    "rosetta_glwe_recombine": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_uint32,
+                                     C.c_void_p]),
+    "rosetta_glwe_encrypt": (_ST, [C.c_uint64, _pp, C.c_double, _u64p, _u64p, C.c_size_t,
+                                   _u64p]),
+    "rosetta_glwe_phase": (_ST, [_pp, _u64p, _u64p, C.c_size_t, _u64p]),
+    "rosetta_autk_keygen": (_ST, [C.c_uint64, _pp, C.c_uint32, C.c_uint32, C.c_double, _u64p,
+                                  _u64p]),
 }
 
 _lib = None
@@ -271,6 +287,73 @@ def shutdown():
     _check(lib().rosetta_shutdown())
 
 
+# lookup-protocol primitives ------------------------------------------------
+
+def blind_rotate_glwe(lwe_in, bsk_dev, glwe_tp, params, extract=False, out=None, stream=None):
+    """Blind rotation of per-ciphertext GLWE test polynomials glwe_tp [batch][2N]."""
+    p = _params(params)
+    batch = lwe_in.numel() // (p.n + 1)
+    if out is None:
+        out = empty((batch, p.N + 1) if extract else (batch, 2 * p.N), lwe_in.device)
+    _check(lib().rosetta_blind_rotate_glwe(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
+                                           _dev(glwe_tp, "glwe_tp"), _dev(out, "out"), batch,
+                                           C.byref(p), 1 if extract else 0, _stream(stream)))
+    return out
+
+
+def autk_words(params, level: int) -> int:
+    return lib().rosetta_autk_words(C.byref(_params(params)), level)
+
+
+def autk_prepare(autk_std, params, level: int, out=None, stream=None):
+    p = _params(params)
+    if out is None:
+        out = empty(autk_words(p, level), autk_std.device)
+    _check(lib().rosetta_autk_prepare(_dev(autk_std, "autk_std"), _dev(out, "autk_dev"),
+                                      C.byref(p), level, _stream(stream)))
+    return out
+
+
+def trace(glwe_in, autk_dev, params, level: int, base_log: int, out=None, stream=None):
+    p = _params(params)
+    batch = glwe_in.numel() // (2 * p.N)
+    if out is None:
+        out = empty((batch, 2 * p.N), glwe_in.device)
+    _check(lib().rosetta_trace(_dev(glwe_in, "glwe_in"), _dev(autk_dev, "autk_dev"),
+                               _dev(out, "glwe_out"), batch, C.byref(p), level, base_log,
+                               _stream(stream)))
+    return out
+
+
+def plain_prepare(plain, N: int, out=None, stream=None):
+    count = plain.numel() // N
+    out = empty(plain.shape, plain.device) if out is None else out
+    _check(lib().rosetta_plain_prepare(_dev(plain, "plain"), _dev(out, "plain_prep"), count, N,
+                                       _stream(stream)))
+    return out
+
+
+def glwe_mul_plain(glwe_in, pa_prep, pb, N: int, out=None, stream=None):
+    """out[q][s] = pa_s * glwe_in[q] + (0, pb_s); pb may be None."""
+    batch = glwe_in.numel() // (2 * N)
+    npoly = pa_prep.numel() // N
+    if out is None:
+        out = empty((batch, npoly, 2 * N), glwe_in.device)
+    _check(lib().rosetta_glwe_mul_plain(_dev(glwe_in, "glwe_in"), _dev(pa_prep, "pa_prep"),
+                                        None if pb is None else _dev(pb, "pb"),
+                                        _dev(out, "glwe_out"), batch, npoly, N, _stream(stream)))
+    return out
+
+
+def glwe_recombine(glwe_in, nseg: int, N: int, out=None, stream=None):
+    batch = glwe_in.numel() // (2 * N * nseg)
+    if out is None:
+        out = empty((batch, 2 * N), glwe_in.device)
+    _check(lib().rosetta_glwe_recombine(_dev(glwe_in, "glwe_in"), _dev(out, "glwe_out"), batch,
+                                        nseg, N, _stream(stream)))
+    return out
+
+
 # --------------------------------------------------------------------------
 # host helpers (numpy)
 # --------------------------------------------------------------------------
@@ -319,3 +402,33 @@ def lut_build(params, table) -> np.ndarray:
     v = np.zeros(p.N, np.uint64)
     _check(lib().rosetta_lut_build(C.byref(p), _np_ptr(table), _np_ptr(v)))
     return v
+
+
+def glwe_encrypt(seed: int, params, sigma: float, glwe_key: np.ndarray, msgs) -> np.ndarray:
+    p = _params(params)
+    key = np.ascontiguousarray(glwe_key, np.uint64)
+    msgs = np.ascontiguousarray(msgs, np.uint64).reshape(-1, p.N)
+    out = np.zeros((msgs.shape[0], 2 * p.N), np.uint64)
+    _check(lib().rosetta_glwe_encrypt(seed, C.byref(p), sigma, _np_ptr(key), _np_ptr(msgs),
+                                      msgs.shape[0], _np_ptr(out)))
+    return out
+
+
+def glwe_phase(params, glwe_key: np.ndarray, cts) -> np.ndarray:
+    p = _params(params)
+    key = np.ascontiguousarray(glwe_key, np.uint64)
+    cts = np.ascontiguousarray(cts, np.uint64).reshape(-1, 2 * p.N)
+    out = np.zeros((cts.shape[0], p.N), np.uint64)
+    _check(lib().rosetta_glwe_phase(C.byref(p), _np_ptr(key), _np_ptr(cts), cts.shape[0],
+                                    _np_ptr(out)))
+    return out
+
+
+def autk_keygen(seed: int, params, level: int, base_log: int, sigma: float,
+                glwe_key: np.ndarray) -> np.ndarray:
+    p = _params(params)
+    key = np.ascontiguousarray(glwe_key, np.uint64)
+    out = np.zeros(autk_words(p, level), np.uint64)
+    _check(lib().rosetta_autk_keygen(seed, C.byref(p), level, base_log, sigma, _np_ptr(key),
+                                     _np_ptr(out)))
+    return out

@@ -133,3 +133,53 @@ def test_encrypt_decrypt_lut_match_oracle(O):
         w2 = W.get(name)
         op2 = O.Params.make(**{k: v for k, v in w2.params().items() if k != "k"})
         assert np.array_equal(R.lut_build(w2.params(), w2.table()), O.test_poly(op2, w2.table()))
+
+
+# ------------------------------------------------ lookup-protocol entry points ---
+
+def test_lookup_validation_touches_no_device(L):
+    p = P()
+    fake = 1 << 40
+    assert L.rosetta_autk_words(C.byref(p), 4) == 8 * 4 * 2 * 256
+    # trace parameters
+    for lv, bl, st in [(0, 12, 2), (5, 12, 3), (4, 31, 3), (4, 16, 3), (4, 12, 0)]:
+        got = L.rosetta_trace(fake, fake + 10 ** 9, fake + 2 * 10 ** 9, 2, C.byref(p), lv, bl, None)
+        if st == 0:
+            continue                 # valid arguments would launch; not on a CPU machine
+        assert got == st, (lv, bl)
+    # empty batches are no-ops, NULL pointers are rejected
+    assert L.rosetta_trace(None, None, None, 0, C.byref(p), 4, 12, None) == 0
+    assert L.rosetta_trace(None, fake, fake, 1, C.byref(p), 4, 12, None) == 1
+    assert L.rosetta_blind_rotate_glwe(None, None, None, None, 0, C.byref(p), 0, None) == 0
+    assert L.rosetta_blind_rotate_glwe(fake, fake, None, fake, 1, C.byref(p), 0, None) == 1
+    assert L.rosetta_glwe_mul_plain(None, None, None, None, 0, 2, 256, None) == 0
+    assert L.rosetta_glwe_mul_plain(fake, fake, None, fake, 1, 0, 256, None) == 2
+    assert L.rosetta_glwe_mul_plain(fake, fake, None, fake, 1, 2, 100, None) == 3
+    assert L.rosetta_glwe_recombine(None, None, 0, 2, 256, None) == 0
+    assert L.rosetta_glwe_recombine(fake, fake, 1, 0, 256, None) == 2
+    # aliasing
+    two_n = 2 * p.N * 8
+    assert L.rosetta_trace(fake, fake + 10 ** 9, fake + 8, 2, C.byref(p), 4, 12, None) == 4
+    assert L.rosetta_blind_rotate_glwe(fake, fake + 10 ** 9, fake + 2 * 10 ** 9,
+                                       fake + 2 * 10 ** 9 + 8, 1, C.byref(p), 0, None) == 4
+    assert L.rosetta_glwe_recombine(fake, fake + two_n, 1, 2, 256, None) == 4
+    assert L.rosetta_glwe_mul_plain(fake, fake + 10 ** 9, None, fake + two_n // 2, 1, 1, 256,
+                                    None) == 4
+
+
+def test_glwe_helpers_match_oracle(O):
+    w = W.get("tiny")
+    prm = w.params()
+    op = O.Params.make(**{k: v for k, v in prm.items() if k != "k"})
+    ks = O.KeySet(op, w.key_seed, w.sigma_lwe, w.sigma_glwe)
+    rng = np.random.default_rng(5)
+    msgs = rng.integers(0, 2 ** 63, (3, w.N), dtype=np.uint64)
+    a = R.glwe_encrypt(77, prm, 2.0 ** -40, ks.glwe_key, msgs)
+    assert np.array_equal(a, O.glwe_encrypt(77, 2.0 ** -40, ks.glwe_key, msgs))
+    ph = R.glwe_phase(prm, ks.glwe_key, a)
+    for q in range(3):
+        assert np.array_equal(ph[q], O.glwe_phase(ks.glwe_key, a[q]))
+    for lv, bl in ((4, 12), (2, 20)):
+        k1 = R.autk_keygen(78, prm, lv, bl, 2.0 ** -51, ks.glwe_key)
+        k2 = O.autk_keygen(78, w.N, lv, bl, 2.0 ** -51, ks.glwe_key)
+        assert k1.shape == k2.shape and np.array_equal(k1, k2)
