@@ -91,6 +91,55 @@ def cpu_baseline(w, keys, cts, v, seconds_target: float):
                       f"includes its once-per-call key transform"}
 
 
+TRACE_LEVEL, TRACE_BASE_LOG = 4, 12
+
+
+def lookup_select(R, W, w, p, keys, d_in, bsk, stream, steps):
+    """Select step of the lookup protocol over the batch: blind rotation of
+    one GLWE test-polynomial ciphertext per input, then the RLWE trace.
+    Ciphertext test polynomials are uniform (the work is data-oblivious);
+    the automorphism key comes from the library's host helper."""
+    import torch
+    rng = np.random.default_rng(w.data_seed + 1)
+    P = 0xFFFFFFFF00000001
+    tp = R.to_device(rng.integers(0, P, (w.batch, 2 * w.N), dtype=np.uint64))
+    autk = R.autk_prepare(R.to_device(R.autk_keygen(w.key_seed + 1, p, TRACE_LEVEL, TRACE_BASE_LOG,
+                                                    w.sigma_glwe, keys["glwe_key"])),
+                          p, TRACE_LEVEL)
+    acc = R.empty((w.batch, 2 * w.N))
+    out = R.empty((w.batch, 2 * w.N))
+
+    def run(evs=None):
+        if evs:
+            evs[0].record(stream)
+        R.blind_rotate_glwe(d_in, bsk, tp, p, out=acc)
+        if evs:
+            evs[1].record(stream)
+        R.trace(acc, autk, p, TRACE_LEVEL, TRACE_BASE_LOG, out=out)
+        if evs:
+            evs[2].record(stream)
+
+    run()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for e in ev:
+        run(e)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    br_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
+    tr_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
+    tr_mm = w.trace_modmul(TRACE_LEVEL) * w.batch
+    tr_t = tr_mm / (tr_ms * 1e-3) / 1e12
+    return {"batch": w.batch, "trace_level": TRACE_LEVEL, "trace_base_log": TRACE_BASE_LOG,
+            "selects_per_s": round(w.batch / wall, 2), "ms_per_step": round(wall * 1e3, 3),
+            "kernels_ms": {"blind_rotate_glwe": round(br_ms, 3), "trace": round(tr_ms, 3)},
+            "roofline_trace": {"bound": "alu", "kernel": "k_trace",
+                               "achieved": round(tr_t, 4), "peak": round(MODMUL_PEAK_T, 4),
+                               "unit": "Tmodmul/s", "frac": round(tr_t / MODMUL_PEAK_T, 4),
+                               "per_launch_modmul": tr_mm, "launch_ms": round(tr_ms, 3)}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -101,6 +150,8 @@ def main():
                     help="target CPU time of the oracle baseline sample (0 = skip)")
     ap.add_argument("--batch", type=int, default=None,
                     help="override the workload's batch (experiments only)")
+    ap.add_argument("--lookup-steps", type=int, default=3,
+                    help="timed steps of the lookup select (0 = skip)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB, outside the timed "
                          "region, as the reference kernel for memory-traffic counters")
@@ -213,6 +264,10 @@ def main():
         "checks": {"split_equals_pbs_batch": same, "decrypt_equals_table_rate": round(ok_rate, 5)},
         "roofline": roofline,
     }
+    if args.lookup_steps > 0:
+        log("[bench] lookup select (blind rotation of ciphertext test polynomials + trace)")
+        result["lookup_select"] = lookup_select(R, W, w, p, keys, d_in, bsk, stream,
+                                                args.lookup_steps)
     if args.cpu_seconds > 0:
         log("[bench] CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(w, keys, cts, v, args.cpu_seconds)

@@ -74,7 +74,7 @@ class Workload:
     def ksk_words(self) -> int:
         return self.N * self.ks_level * (self.n + 1)
 
-    # ---- algorithmic work per PBS (see the design doc for the derivation) ---
+    # ---- algorithmic work (radix-2 transform counts) --------------------
     def br_modmul_per_pbs(self) -> int:
         """Modular multiplications of one blind rotation with radix-2 NTTs:
         n steps x [(2l forward + 2 inverse) x (N/2) log2 N butterflies
@@ -85,6 +85,16 @@ class Workload:
 
     def ks_mac_per_pbs(self) -> int:
         return self.N * self.ks_level * (self.n + 1)
+
+    def trace_modmul(self, level: int) -> int:
+        """Modular multiplications of one RLWE trace: 2N for the N^-1
+        scaling, then log2 N rounds of [(level forward + 2 inverse) x
+        (N/2) log2 N butterflies + 2 level N pointwise products]."""
+        L = int(math.log2(self.N))
+        return 2 * self.N + L * ((level + 2) * (self.N // 2) * L + 2 * level * self.N)
+
+    def autk_words(self, level: int) -> int:
+        return int(math.log2(self.N)) * level * 2 * self.N
 
     # ---- seeded inputs ---------------------------------------------------
     def messages(self, count: int | None = None, seed: int | None = None) -> np.ndarray:
