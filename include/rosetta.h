@@ -253,6 +253,62 @@ rosetta_status rosetta_glwe_mul_plain(const uint64_t *glwe_in, const uint64_t *p
 rosetta_status rosetta_glwe_recombine(const uint64_t *glwe_in, uint64_t *glwe_out, size_t batch,
                                       uint32_t nseg, uint32_t N, void *stream);
 
+/* ---- adaptive segmented LUT (Sec. 3.1), host ---------------------------
+ *
+ * The domain [tau_0, tau_nseg] is cut into nseg segments; segment s holds
+ * nbr equal intervals; interval i of segment s carries a_si x + b_si.
+ * Coefficient arrays are [nseg][nbr] doubles.  Linear fits interpolate f at
+ * the interval's two Chebyshev nodes c -+ r cos(pi/4) (c midpoint, r
+ * half-width); constant fits store f(c) (the single-LUT baseline).  Lookup:
+ * S = #{j in 1..nseg-1 : x >= tau_j}, I = floor((x - tau_S) nbr /
+ * (tau_{S+1} - tau_S)) clamped to [0, nbr), y = a_SI x + b_SI. */
+typedef enum {
+  ROSETTA_FN_INV = 0,      /* 1/x */
+  ROSETTA_FN_INV_SQRT = 1, /* 1/sqrt(x) */
+  ROSETTA_FN_SILU = 2,     /* x / (1 + e^-x) */
+  ROSETTA_FN_GELU = 3,     /* x (1 + erf(x / sqrt 2)) / 2 */
+  ROSETTA_FN_EXP = 4       /* e^x */
+} rosetta_function;
+typedef enum { ROSETTA_SPACING_UNIFORM = 0, ROSETTA_SPACING_LOG = 1 } rosetta_spacing;
+typedef enum { ROSETTA_FIT_LINEAR = 0, ROSETTA_FIT_CONSTANT = 1 } rosetta_fit;
+
+/* Boundaries tau[nseg+1] on [lo, hi]: uniform, or geometric (lo > 0; the
+ * evaluation setup of Sec. 5.1 spaces them logarithmically for 1/x and
+ * 1/sqrt(x) and uniformly for SiLU and GELU). */
+rosetta_status rosetta_seglut_boundaries(double lo, double hi, uint32_t nseg, int spacing,
+                                         double *tau);
+
+/* Coefficients a, b [nseg][nbr] of `function` (rosetta_function) with the
+ * given fit (rosetta_fit) over strictly increasing boundaries tau[nseg+1]. */
+rosetta_status rosetta_seglut_build(int function, const double *tau, uint32_t nseg, uint32_t nbr,
+                                    int fit, double *a, double *b);
+
+/* Step 2 polynomials of Sec. 3.2: p[s] = nbr / (tau_{s+1} - tau_s),
+ * q[s] = -tau_s nbr / (tau_{s+1} - tau_s), so that p[s] x + q[s] is the
+ * (real) local interval index of x in segment s. */
+rosetta_status rosetta_seglut_protocol_polys(const double *tau, uint32_t nseg, uint32_t nbr,
+                                             double *p, double *q);
+
+/* Cleartext three-step lookup of x[count] into y[count].  index_offset
+ * (NULL for none) adds offset[k] to input k's interval index before the
+ * coefficients are read (clamped to [0, nbr)): a model of the selection
+ * error of the encrypted lookup, drawn by the caller. */
+rosetta_status rosetta_seglut_eval(const double *tau, uint32_t nseg, uint32_t nbr,
+                                   const double *a, const double *b, const double *x,
+                                   const int32_t *index_offset, size_t count, double *y);
+
+/* Precision in bits, -log2 of the RMS error of the cleartext lookup (with
+ * the optional index offsets) against `function` over x[count] (count >= 1). */
+rosetta_status rosetta_seglut_precision(int function, const double *tau, uint32_t nseg,
+                                        uint32_t nbr, const double *a, const double *b,
+                                        const double *x, const int32_t *index_offset,
+                                        size_t count, double *bits);
+
+/* Fixed-point encoding into Z_p: out[k] = round(v[k] 2^scale_log) mod p
+ * (round half to even); |v 2^scale_log| must stay below 2^62. */
+rosetta_status rosetta_encode_fixed(const double *v, size_t count, int scale_log,
+                                    uint64_t *out);
+
 /* ---- test helpers: host memory, deterministic from the seed ------------ */
 
 /* Binary keys and the two switching keys in standard layout (host arrays of

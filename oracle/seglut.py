@@ -97,12 +97,16 @@ def interval_index(x, taus, S, nbr: int) -> np.ndarray:
     return np.clip(I, 0, nbr - 1)
 
 
-def evaluate(x, taus, A, B) -> np.ndarray:
-    """The three-step cleartext lookup of Sec. 3.1."""
+def evaluate(x, taus, A, B, index_offset=None) -> np.ndarray:
+    """The three-step cleartext lookup of Sec. 3.1; index_offset (one integer
+    per input, or None) shifts the interval index before the coefficients
+    are read, clamped to the segment."""
     x = np.asarray(x, dtype=np.float64)
     nbr = A.shape[1]
     S = segment_index(x, taus)
     I = interval_index(x, taus, S, nbr)
+    if index_offset is not None:
+        I = np.clip(I + np.asarray(index_offset, dtype=np.int64), 0, nbr - 1)
     return A[S, I] * x + B[S, I]
 
 
@@ -122,6 +126,6 @@ def max_relative_error(f, taus, A, B, samples: int = 200001) -> float:
     return float(np.max(np.abs(evaluate(xs, taus, A, B) - y) / np.abs(y)))
 
 
-def precision_bits(f, taus, A, B, xs) -> float:
-    err = evaluate(xs, taus, A, B) - f(np.asarray(xs, dtype=np.float64))
+def precision_bits(f, taus, A, B, xs, index_offset=None) -> float:
+    err = evaluate(xs, taus, A, B, index_offset) - f(np.asarray(xs, dtype=np.float64))
     return float(-math.log2(math.sqrt(float(np.mean(err * err)))))

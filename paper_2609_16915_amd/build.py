@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "librosetta.so")
-SOURCES = ["kernels.hip", "abi.cpp", "host_helpers.cpp"]
+SOURCES = ["kernels.hip", "abi.cpp", "host_helpers.cpp", "seglut.cpp"]
 ARCH = os.environ.get("ROSETTA_OFFLOAD_ARCH", "gfx950")
 
 
@@ -26,28 +26,43 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def command(out: str) -> list:
-    return [hipcc(), "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-shared",
-            # packed fp32 instructions are kept out of all device code
-            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-ffp-contract=off", "-Wall", "-Wno-unused-result",
-            f"-I{INCLUDE}", f"-I{CSRC}",
-            *[os.path.join(CSRC, s) for s in SOURCES], "-o", out]
+FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",
+         # packed fp32 instructions are kept out of all device code
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-ffp-contract=off", "-Wall", "-Wno-unused-result",
+         f"-I{INCLUDE}", f"-I{CSRC}"]
+
+
+def _filter(stderr: str) -> str:
+    return "\n".join(l for l in (stderr or "").splitlines() if "packed-fp32-ops" not in l)
 
 
 def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = command(tmp)
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    errs = "\n".join(l for l in (res.stderr or "").splitlines()
-                     if "packed-fp32-ops" not in l)
-    if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{errs}")
-    if verbose and errs.strip():
-        print(errs, flush=True)
-    os.replace(tmp, LIB)
+    """Compile every source to an object (in parallel), then link."""
+    import concurrent.futures
+    import tempfile
+    with tempfile.TemporaryDirectory(prefix="rosetta_build_") as tmpdir:
+        objs = [os.path.join(tmpdir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
+        cmds = [[hipcc(), *FLAGS, "-c", os.path.join(CSRC, s), "-o", o]
+                for s, o in zip(SOURCES, objs)]
+        if verbose:
+            for c in cmds:
+                print(" ".join(c), flush=True)
+        with concurrent.futures.ThreadPoolExecutor(len(cmds)) as ex:
+            results = list(ex.map(lambda c: subprocess.run(c, capture_output=True, text=True),
+                                  cmds))
+        for src, res in zip(SOURCES, results):
+            if res.returncode != 0:
+                raise RuntimeError(f"hipcc failed on {src} ({res.returncode}):\n"
+                                   f"{_filter(res.stderr)}")
+            if verbose and _filter(res.stderr).strip():
+                print(_filter(res.stderr), flush=True)
+        tmp = LIB + ".tmp"
+        link = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+        res = subprocess.run(link, capture_output=True, text=True)
+        if res.returncode != 0:
+            raise RuntimeError(f"link failed ({res.returncode}):\n{_filter(res.stderr)}")
+        os.replace(tmp, LIB)
     return LIB
 
 

@@ -96,7 +96,20 @@ SIGNATURES = {
     "rosetta_glwe_phase": (_ST, [_pp, _u64p, _u64p, C.c_size_t, _u64p]),
     "rosetta_autk_keygen": (_ST, [C.c_uint64, _pp, C.c_uint32, C.c_uint32, C.c_double, _u64p,
                                   _u64p]),
+    "rosetta_seglut_boundaries": (_ST, [C.c_double, C.c_double, C.c_uint32, C.c_int, _u64p]),
+    "rosetta_seglut_build": (_ST, [C.c_int, _u64p, C.c_uint32, C.c_uint32, C.c_int, _u64p,
+                                   _u64p]),
+    "rosetta_seglut_protocol_polys": (_ST, [_u64p, C.c_uint32, C.c_uint32, _u64p, _u64p]),
+    "rosetta_seglut_eval": (_ST, [_u64p, C.c_uint32, C.c_uint32, _u64p, _u64p, _u64p, _u64p,
+                                  C.c_size_t, _u64p]),
+    "rosetta_seglut_precision": (_ST, [C.c_int, _u64p, C.c_uint32, C.c_uint32, _u64p, _u64p,
+                                       _u64p, _u64p, C.c_size_t, _u64p]),
+    "rosetta_encode_fixed": (_ST, [_u64p, C.c_size_t, C.c_int, _u64p]),
 }
+
+FUNCTIONS = {"inv": 0, "inv_sqrt": 1, "silu": 2, "gelu": 3, "exp": 4}
+SPACINGS = {"uniform": 0, "log": 1}
+FITS = {"linear": 0, "constant": 1}
 
 _lib = None
 
@@ -431,4 +444,70 @@ def autk_keygen(seed: int, params, level: int, base_log: int, sigma: float,
     out = np.zeros(autk_words(p, level), np.uint64)
     _check(lib().rosetta_autk_keygen(seed, C.byref(p), level, base_log, sigma, _np_ptr(key),
                                      _np_ptr(out)))
+    return out
+
+
+# segmented LUT (host) --------------------------------------------------------
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def seglut_boundaries(lo: float, hi: float, nseg: int, spacing: str) -> np.ndarray:
+    tau = np.zeros(nseg + 1, np.float64)
+    _check(lib().rosetta_seglut_boundaries(lo, hi, nseg, SPACINGS[spacing], _np_ptr(tau)))
+    return tau
+
+
+def seglut_build(function: str, tau, nbr: int, fit: str = "linear"):
+    tau = _f64(tau)
+    nseg = tau.shape[0] - 1
+    a = np.zeros((nseg, nbr), np.float64)
+    b = np.zeros((nseg, nbr), np.float64)
+    _check(lib().rosetta_seglut_build(FUNCTIONS[function], _np_ptr(tau), nseg, nbr, FITS[fit],
+                                      _np_ptr(a), _np_ptr(b)))
+    return a, b
+
+
+def seglut_protocol_polys(tau, nbr: int):
+    tau = _f64(tau)
+    nseg = tau.shape[0] - 1
+    p = np.zeros(nseg, np.float64)
+    q = np.zeros(nseg, np.float64)
+    _check(lib().rosetta_seglut_protocol_polys(_np_ptr(tau), nseg, nbr, _np_ptr(p), _np_ptr(q)))
+    return p, q
+
+
+def _offsets(index_offset, count):
+    if index_offset is None:
+        return None, None
+    off = np.ascontiguousarray(index_offset, dtype=np.int32)
+    if off.size != count:
+        raise ValueError("index_offset must have one entry per input")
+    return off, _np_ptr(off)
+
+
+def seglut_eval(tau, a, b, x, index_offset=None) -> np.ndarray:
+    tau, a, b, x = _f64(tau), _f64(a), _f64(b), _f64(x)
+    y = np.zeros_like(x)
+    off, off_p = _offsets(index_offset, x.size)
+    _check(lib().rosetta_seglut_eval(_np_ptr(tau), tau.shape[0] - 1, a.shape[1], _np_ptr(a),
+                                     _np_ptr(b), _np_ptr(x), off_p, x.size, _np_ptr(y)))
+    return y
+
+
+def seglut_precision(function: str, tau, a, b, x, index_offset=None) -> float:
+    tau, a, b, x = _f64(tau), _f64(a), _f64(b), _f64(x)
+    bits = np.zeros(1, np.float64)
+    off, off_p = _offsets(index_offset, x.size)
+    _check(lib().rosetta_seglut_precision(FUNCTIONS[function], _np_ptr(tau), tau.shape[0] - 1,
+                                          a.shape[1], _np_ptr(a), _np_ptr(b), _np_ptr(x), off_p,
+                                          x.size, _np_ptr(bits)))
+    return float(bits[0])
+
+
+def encode_fixed(v, scale_log: int) -> np.ndarray:
+    v = _f64(v)
+    out = np.zeros(v.shape, np.uint64)
+    _check(lib().rosetta_encode_fixed(_np_ptr(v), v.size, scale_log, _np_ptr(out)))
     return out
