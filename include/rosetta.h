@@ -247,11 +247,29 @@ rosetta_status rosetta_glwe_mul_plain(const uint64_t *glwe_in, const uint64_t *p
                                       const uint64_t *pb_dev, uint64_t *glwe_out, size_t batch,
                                       uint32_t npoly, uint32_t N, void *stream);
 
-/* Recombination (Sec. 3.2, Step 3 Phase 2): glwe_out[q] = sum_{s < nseg}
- * X^s glwe_in[q][s], glwe_in [batch][nseg][2N], glwe_out [batch][2N]
+/* Recombination (Sec. 3.2, Step 3 Phase 2, and the recombination of
+ * Sec. 3.3.2): glwe_out[q] = sum_{s < count} X^(e_s) glwe_in[q][s],
+ * glwe_in [batch][count][2N], glwe_out [batch][2N] (device, not
+ * overlapping).  exps: host array of `count` exponents in [0, 2N), or NULL
+ * for e_s = s; 1 <= count <= 256. */
+rosetta_status rosetta_glwe_recombine(const uint64_t *glwe_in, const uint32_t *exps,
+                                      uint64_t *glwe_out, size_t batch, uint32_t count,
+                                      uint32_t N, void *stream);
+
+/* Monomial copies (Sec. 3.3.2, multi-value batching: X^(-c) moves the value
+ * at coefficient c to the constant term): glwe_out[q][s] = X^(e_s)
+ * glwe_in[q], glwe_in [batch][2N], glwe_out [batch][count][2N] (device, not
+ * overlapping); exps: host array of `count` exponents in [0, 2N)
+ * (X^(-c) = X^(2N-c)); 1 <= count <= 256. */
+rosetta_status rosetta_glwe_monomial_mul(const uint64_t *glwe_in, const uint32_t *exps,
+                                         uint64_t *glwe_out, size_t batch, uint32_t count,
+                                         uint32_t N, void *stream);
+
+/* Sample extraction alone (LWE Extract, Sec. 2.2.3): big_out[q] = (A_0,
+ * -A_{N-1}, .., -A_1, B_0) from glwe_in [batch][2N]; big_out [batch][N+1]
  * (device, not overlapping). */
-rosetta_status rosetta_glwe_recombine(const uint64_t *glwe_in, uint64_t *glwe_out, size_t batch,
-                                      uint32_t nseg, uint32_t N, void *stream);
+rosetta_status rosetta_sample_extract(const uint64_t *glwe_in, uint64_t *big_out, size_t batch,
+                                      uint32_t N, void *stream);
 
 /* ---- adaptive segmented LUT (Sec. 3.1), host ---------------------------
  *

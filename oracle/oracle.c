@@ -889,14 +889,16 @@ void or_glwe_mul_plain(int N, const u64 *ct, const u64 *pa, const u64 *pb, u64 *
   free(tmp);
 }
 
-/* Recombination of Sec. 3.2, Step 3 (Phase 2 construct):
- *   R = sum_{s < count} X^s r_s  (both components). */
-void or_glwe_recombine(int N, const u64 *cts, int count, u64 *out) {
+/* Recombination of Sec. 3.2, Step 3 (Phase 2 construct), and of the
+ * multi-value batching of Sec. 3.3.2:
+ *   R = sum_{s < count} X^(e_s) r_s  (both components),
+ * e_s = exps[s], or s when exps is NULL. */
+void or_glwe_recombine(int N, const u64 *cts, int count, const uint32_t *exps, u64 *out) {
   u64 *tmp = (u64 *)malloc((size_t)N * sizeof(u64));
   for (int j = 0; j < 2 * N; ++j) out[j] = 0;
   for (int s = 0; s < count; ++s)
     for (int u = 0; u < 2; ++u) {
-      or_poly_monomial_mul(cts + ((size_t)s * 2 + u) * N, s, tmp, N);
+      or_poly_monomial_mul(cts + ((size_t)s * 2 + u) * N, exps ? (int)exps[s] : s, tmp, N);
       for (int j = 0; j < N; ++j) out[(size_t)u * N + j] = or_add(out[(size_t)u * N + j], tmp[j]);
     }
   free(tmp);

@@ -112,7 +112,7 @@ def _declare(L):
         "or_glwe_encrypt": (None, [C.c_uint64, C.c_int, C.c_double, _u64p, _u64p, C.c_size_t,
                                    _u64p]),
         "or_glwe_mul_plain": (None, [C.c_int, _u64p, _u64p, _u64p, _u64p, C.c_int]),
-        "or_glwe_recombine": (None, [C.c_int, _u64p, C.c_int, _u64p]),
+        "or_glwe_recombine": (None, [C.c_int, _u64p, C.c_int, _u32p, _u64p]),
         "or_blind_rotate_glwe_batch": (None, [_pp, _u64p, _u64p, _u64p, _u64p, C.c_size_t,
                                               C.c_int, C.c_int]),
         "or_trace_batch": (None, [C.c_int, C.c_int, C.c_int, _u64p, _u64p, _u64p, C.c_size_t,
@@ -405,9 +405,11 @@ def glwe_mul_plain(ct, pa, pb=None, kind=SCHOOLBOOK) -> np.ndarray:
     return out
 
 
-def glwe_recombine(cts) -> np.ndarray:
+def glwe_recombine(cts, exps=None) -> np.ndarray:
+    """sum_s X^(exps[s]) cts[s] (exps None: X^s)."""
     cts = _u64(cts)
     count, twoN = cts.shape
     out = np.zeros(twoN, dtype=np.uint64)
-    lib().or_glwe_recombine(twoN // 2, _ptr(cts), count, _ptr(out))
+    e = None if exps is None else np.ascontiguousarray(exps, dtype=np.uint32)
+    lib().or_glwe_recombine(twoN // 2, _ptr(cts), count, _ptr(e, _u32p), _ptr(out))
     return out

@@ -522,19 +522,65 @@ rosetta_status rosetta_glwe_mul_plain(const uint64_t *glwe_in, const uint64_t *p
   return e == hipSuccess ? ok() : hip_fail(e, "glwe_mul_plain launch");
 }
 
-rosetta_status rosetta_glwe_recombine(const uint64_t *glwe_in, uint64_t *glwe_out, size_t batch,
-                                      uint32_t nseg, uint32_t N, void *stream) {
+static rosetta_status load_exponents(const uint32_t *exps, uint32_t count, uint32_t N,
+                                     Exponents &ex) {
+  if (count < 1 || count > (uint32_t)MAX_MONOMIALS)
+    return fail(ROSETTA_ERR_PARAMS, "need 1 <= count <= %d", MAX_MONOMIALS);
+  for (uint32_t s = 0; s < count; ++s) {
+    const uint32_t e = exps ? exps[s] : s;
+    if (e >= 2 * N) return fail(ROSETTA_ERR_PARAMS, "exponent %u is not below 2N", e);
+    ex.e[s] = (uint16_t)e;
+  }
+  return ROSETTA_OK;
+}
+
+rosetta_status rosetta_glwe_recombine(const uint64_t *glwe_in, const uint32_t *exps,
+                                      uint64_t *glwe_out, size_t batch, uint32_t count,
+                                      uint32_t N, void *stream) {
   if (!is_pow2_in(N, 256, 4096))
     return fail(ROSETTA_ERR_UNSUPPORTED, "N must be a power of two in [256, 4096]");
-  if (nseg < 1 || nseg > N) return fail(ROSETTA_ERR_PARAMS, "need 1 <= nseg <= N");
+  Exponents ex;
+  rosetta_status st = load_exponents(exps, count, N, ex);
+  if (st) return st;
   if (batch == 0) return ok();
   if (!glwe_in || !glwe_out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
   const size_t out_bytes = batch * 2 * (size_t)N * 8;
-  if (any_overlap(glwe_out, out_bytes, glwe_in, out_bytes * nseg))
+  if (any_overlap(glwe_out, out_bytes, glwe_in, out_bytes * count))
     return fail(ROSETTA_ERR_ALIAS, "output overlaps the input");
-  hipError_t e = launch_glwe_recombine(glwe_in, glwe_out, batch, (int)nseg, N,
+  hipError_t e = launch_glwe_recombine(glwe_in, glwe_out, batch, (int)count, ex, N,
                                        (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "glwe_recombine launch");
+}
+
+rosetta_status rosetta_glwe_monomial_mul(const uint64_t *glwe_in, const uint32_t *exps,
+                                         uint64_t *glwe_out, size_t batch, uint32_t count,
+                                         uint32_t N, void *stream) {
+  if (!is_pow2_in(N, 256, 4096))
+    return fail(ROSETTA_ERR_UNSUPPORTED, "N must be a power of two in [256, 4096]");
+  if (!exps) return fail(ROSETTA_ERR_NULL, "exps is NULL");
+  Exponents ex;
+  rosetta_status st = load_exponents(exps, count, N, ex);
+  if (st) return st;
+  if (batch == 0) return ok();
+  if (!glwe_in || !glwe_out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t in_bytes = batch * 2 * (size_t)N * 8;
+  if (any_overlap(glwe_out, in_bytes * count, glwe_in, in_bytes))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps the input");
+  hipError_t e = launch_glwe_monomial_mul(glwe_in, glwe_out, batch, (int)count, ex, N,
+                                          (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "glwe_monomial_mul launch");
+}
+
+rosetta_status rosetta_sample_extract(const uint64_t *glwe_in, uint64_t *big_out, size_t batch,
+                                      uint32_t N, void *stream) {
+  if (!is_pow2_in(N, 256, 4096))
+    return fail(ROSETTA_ERR_UNSUPPORTED, "N must be a power of two in [256, 4096]");
+  if (batch == 0) return ok();
+  if (!glwe_in || !big_out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  if (any_overlap(big_out, batch * (size_t)(N + 1) * 8, glwe_in, batch * 2 * (size_t)N * 8))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps the input");
+  hipError_t e = launch_sample_extract(glwe_in, big_out, batch, N, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "sample_extract launch");
 }
 
 rosetta_status rosetta_shutdown(void) {

@@ -45,8 +45,18 @@ hipError_t launch_trace(const uint64_t *in, const uint64_t *autk_dev, uint64_t *
 hipError_t launch_glwe_mul_plain(const uint64_t *in, const uint64_t *pa_dev, const uint64_t *pb,
                                  uint64_t *out, size_t batch, int npoly, uint32_t N,
                                  const Tables &tb, hipStream_t st);
-hipError_t launch_glwe_recombine(const uint64_t *in, uint64_t *out, size_t batch, int nseg,
-                                 uint32_t N, hipStream_t st);
+// Monomial exponents (each in [0, 2N)) passed by value to the kernels.
+constexpr int MAX_MONOMIALS = 256;
+struct Exponents {
+  uint16_t e[MAX_MONOMIALS];
+};
+
+hipError_t launch_glwe_recombine(const uint64_t *in, uint64_t *out, size_t batch, int count,
+                                 const Exponents &ex, uint32_t N, hipStream_t st);
+hipError_t launch_glwe_monomial_mul(const uint64_t *in, uint64_t *out, size_t batch, int count,
+                                    const Exponents &ex, uint32_t N, hipStream_t st);
+hipError_t launch_sample_extract(const uint64_t *in, uint64_t *out, size_t batch, uint32_t N,
+                                 hipStream_t st);
 hipError_t launch_keyswitch(const uint64_t *big, const uint64_t *ksk_dev, uint64_t *out,
                             size_t batch, const rosetta_params &p, hipStream_t st);
 hipError_t launch_ntt(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,

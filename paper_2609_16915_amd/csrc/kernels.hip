@@ -500,22 +500,51 @@ k_glwe_mul_plain(const u64 *__restrict__ in, const u64 *__restrict__ pa,
   }
 }
 
-// Recombination: out[q] = sum_{s < nseg} X^s in[q][s] (both components).
-// One thread per output coefficient.
+// Coefficient j of X^e a (0 <= e < 2N; X^N = -1).
+__device__ __forceinline__ u64 monomial_coef(const u64 *a, int j, int e, int N) {
+  const int r = e & (N - 1);
+  const bool neg = (j < r) != (e >= N);
+  const u64 v = a[(j - r) & (N - 1)];
+  return neg ? gl_neg(v) : v;
+}
+
+// Recombination: out[q] = sum_{s < count} X^(e_s) in[q][s] (both
+// components).  One thread per output coefficient.
 __global__ void k_glwe_recombine(const u64 *__restrict__ in, u64 *__restrict__ out, size_t batch,
-                                 int nseg, int N) {
+                                 int count, Exponents ex, int N) {
   const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const size_t total = batch * 2 * (size_t)N;
-  if (i >= total) return;
+  if (i >= batch * 2 * (size_t)N) return;
   const int j = (int)(i % N);
   const size_t qc = i / N;  // q * 2 + c
   const size_t q = qc / 2, c = qc % 2;
   u64 acc = 0;
-  for (int s = 0; s < nseg; ++s) {
-    const u64 v = in[((q * nseg + s) * 2 + c) * N + ((j - s) & (N - 1))];
-    acc = j >= s ? gl_add(acc, v) : gl_sub(acc, v);
-  }
+  for (int s = 0; s < count; ++s)
+    acc = gl_add(acc, monomial_coef(in + ((q * count + s) * 2 + c) * N, j, ex.e[s], N));
   out[i] = acc;
+}
+
+// Monomial copies: out[q][s] = X^(e_s) in[q] (both components).
+__global__ void k_glwe_monomial_mul(const u64 *__restrict__ in, u64 *__restrict__ out,
+                                    size_t batch, int count, Exponents ex, int N) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= batch * count * 2 * (size_t)N) return;
+  const int j = (int)(i % N);
+  const size_t c = (i / N) % 2;
+  const size_t s = (i / (2 * (size_t)N)) % count;
+  const size_t q = i / (2 * (size_t)N * count);
+  out[i] = monomial_coef(in + (q * 2 + c) * N, j, ex.e[s], N);
+}
+
+// Sample extraction of the constant coefficient of GLWE ciphertexts:
+// a'_0 = A_0, a'_j = -A_{N-j}, b' = B_0 (the BR_EXTRACT epilogue, alone).
+__global__ void k_sample_extract(const u64 *__restrict__ in, u64 *__restrict__ out, size_t batch,
+                                 int N) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= batch * (size_t)(N + 1)) return;
+  const size_t q = i / (N + 1);
+  const int j = (int)(i % (N + 1));
+  const u64 *g = in + q * 2 * (size_t)N;
+  out[i] = j == N ? g[N] : (j == 0 ? g[0] : gl_neg(g[N - j]));
 }
 
 // ---------------------------------------------------------------------------
@@ -731,12 +760,26 @@ hipError_t launch_glwe_mul_plain(const uint64_t *in, const uint64_t *pa_dev, con
   return hipGetLastError();
 }
 
-hipError_t launch_glwe_recombine(const uint64_t *in, uint64_t *out, size_t batch, int nseg,
-                                 uint32_t N, hipStream_t st) {
-  const size_t total = batch * 2 * (size_t)N;
-  const unsigned blocks = (unsigned)((total + 255) / 256);
-  hipLaunchKernelGGL(k_glwe_recombine, dim3(blocks), dim3(256), 0, st, in, out, batch, nseg,
-                     (int)N);
+static unsigned grid_of(size_t total) { return (unsigned)((total + 255) / 256); }
+
+hipError_t launch_glwe_recombine(const uint64_t *in, uint64_t *out, size_t batch, int count,
+                                 const Exponents &ex, uint32_t N, hipStream_t st) {
+  hipLaunchKernelGGL(k_glwe_recombine, dim3(grid_of(batch * 2 * (size_t)N)), dim3(256), 0, st,
+                     in, out, batch, count, ex, (int)N);
+  return hipGetLastError();
+}
+
+hipError_t launch_glwe_monomial_mul(const uint64_t *in, uint64_t *out, size_t batch, int count,
+                                    const Exponents &ex, uint32_t N, hipStream_t st) {
+  hipLaunchKernelGGL(k_glwe_monomial_mul, dim3(grid_of(batch * count * 2 * (size_t)N)),
+                     dim3(256), 0, st, in, out, batch, count, ex, (int)N);
+  return hipGetLastError();
+}
+
+hipError_t launch_sample_extract(const uint64_t *in, uint64_t *out, size_t batch, uint32_t N,
+                                 hipStream_t st) {
+  hipLaunchKernelGGL(k_sample_extract, dim3(grid_of(batch * (size_t)(N + 1))), dim3(256), 0, st,
+                     in, out, batch, (int)N);
   return hipGetLastError();
 }
 

@@ -89,8 +89,11 @@ SIGNATURES = {
     "rosetta_plain_prepare": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
     "rosetta_glwe_mul_plain": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, C.c_uint32,
                                      C.c_uint32, C.c_void_p]),
-    "rosetta_glwe_recombine": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_uint32,
+    "rosetta_glwe_recombine": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, C.c_uint32, C.c_uint32,
                                      C.c_void_p]),
+    "rosetta_glwe_monomial_mul": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, C.c_uint32,
+                                        C.c_uint32, C.c_void_p]),
+    "rosetta_sample_extract": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
     "rosetta_glwe_encrypt": (_ST, [C.c_uint64, _pp, C.c_double, _u64p, _u64p, C.c_size_t,
                                    _u64p]),
     "rosetta_glwe_phase": (_ST, [_pp, _u64p, _u64p, C.c_size_t, _u64p]),
@@ -358,12 +361,43 @@ def glwe_mul_plain(glwe_in, pa_prep, pb, N: int, out=None, stream=None):
     return out
 
 
-def glwe_recombine(glwe_in, nseg: int, N: int, out=None, stream=None):
-    batch = glwe_in.numel() // (2 * N * nseg)
+def _exps(exps, count):
+    if exps is None:
+        return None, None
+    e = np.ascontiguousarray(exps, dtype=np.uint32)
+    if e.size != count:
+        raise ValueError("need one exponent per ciphertext")
+    return e, _np_ptr(e)
+
+
+def glwe_recombine(glwe_in, count: int, N: int, exps=None, out=None, stream=None):
+    """out[q] = sum_s X^(exps[s]) glwe_in[q][s] (exps None: X^s)."""
+    batch = glwe_in.numel() // (2 * N * count)
     if out is None:
         out = empty((batch, 2 * N), glwe_in.device)
-    _check(lib().rosetta_glwe_recombine(_dev(glwe_in, "glwe_in"), _dev(out, "glwe_out"), batch,
-                                        nseg, N, _stream(stream)))
+    e, ep = _exps(exps, count)
+    _check(lib().rosetta_glwe_recombine(_dev(glwe_in, "glwe_in"), ep, _dev(out, "glwe_out"),
+                                        batch, count, N, _stream(stream)))
+    return out
+
+
+def glwe_monomial_mul(glwe_in, exps, N: int, out=None, stream=None):
+    """out[q][s] = X^(exps[s]) glwe_in[q]."""
+    batch = glwe_in.numel() // (2 * N)
+    e, ep = _exps(exps, len(exps))
+    if out is None:
+        out = empty((batch, e.size, 2 * N), glwe_in.device)
+    _check(lib().rosetta_glwe_monomial_mul(_dev(glwe_in, "glwe_in"), ep, _dev(out, "glwe_out"),
+                                           batch, e.size, N, _stream(stream)))
+    return out
+
+
+def sample_extract(glwe_in, N: int, out=None, stream=None):
+    batch = glwe_in.numel() // (2 * N)
+    if out is None:
+        out = empty((batch, N + 1), glwe_in.device)
+    _check(lib().rosetta_sample_extract(_dev(glwe_in, "glwe_in"), _dev(out, "big_out"), batch, N,
+                                        _stream(stream)))
     return out
 
 

@@ -155,14 +155,21 @@ def test_lookup_validation_touches_no_device(L):
     assert L.rosetta_glwe_mul_plain(None, None, None, None, 0, 2, 256, None) == 0
     assert L.rosetta_glwe_mul_plain(fake, fake, None, fake, 1, 0, 256, None) == 2
     assert L.rosetta_glwe_mul_plain(fake, fake, None, fake, 1, 2, 100, None) == 3
-    assert L.rosetta_glwe_recombine(None, None, 0, 2, 256, None) == 0
-    assert L.rosetta_glwe_recombine(fake, fake, 1, 0, 256, None) == 2
+    assert L.rosetta_glwe_recombine(None, None, None, 0, 2, 256, None) == 0
+    assert L.rosetta_glwe_recombine(fake, None, fake, 1, 0, 256, None) == 2
+    assert L.rosetta_glwe_recombine(fake, None, fake, 1, 257, 256, None) == 2
+    bad = (C.c_uint32 * 2)(0, 512)                     # exponent not below 2N
+    assert L.rosetta_glwe_recombine(fake, C.addressof(bad), fake, 1, 2, 256, None) == 2
+    assert L.rosetta_glwe_monomial_mul(fake, None, fake, 1, 2, 256, None) == 1
+    assert L.rosetta_glwe_monomial_mul(fake, C.addressof(bad), fake, 1, 2, 256, None) == 2
+    assert L.rosetta_sample_extract(None, None, 0, 256, None) == 0
+    assert L.rosetta_sample_extract(fake, fake + 8, 1, 256, None) == 4
     # aliasing
     two_n = 2 * p.N * 8
     assert L.rosetta_trace(fake, fake + 10 ** 9, fake + 8, 2, C.byref(p), 4, 12, None) == 4
     assert L.rosetta_blind_rotate_glwe(fake, fake + 10 ** 9, fake + 2 * 10 ** 9,
                                        fake + 2 * 10 ** 9 + 8, 1, C.byref(p), 0, None) == 4
-    assert L.rosetta_glwe_recombine(fake, fake + two_n, 1, 2, 256, None) == 4
+    assert L.rosetta_glwe_recombine(fake, None, fake + two_n, 1, 2, 256, None) == 4
     assert L.rosetta_glwe_mul_plain(fake, fake + 10 ** 9, None, fake + two_n // 2, 1, 1, 256,
                                     None) == 4
 

@@ -147,6 +147,28 @@ def test_glwe_recombine_vs_oracle(O, torch_dev, N, nseg, batch):
     got = R.to_host(R.glwe_recombine(R.to_device(cts), nseg, N))
     for q in range(batch):
         assert np.array_equal(got[q], O.glwe_recombine(cts[q]))
+    exps = rng.integers(0, 2 * N, nseg).astype(np.uint32)
+    exps[0] = 2 * N - 1
+    got = R.to_host(R.glwe_recombine(R.to_device(cts), nseg, N, exps=exps))
+    for q in range(batch):
+        assert np.array_equal(got[q], O.glwe_recombine(cts[q], exps))
+
+
+@pytest.mark.parametrize("N,count,batch", [(256, 3, 4), (2048, 16, 3), (4096, 5, 2)])
+def test_monomial_copies_and_extract_vs_oracle(O, torch_dev, N, count, batch):
+    rng = np.random.default_rng(N + count + 1)
+    cts = rng.integers(0, P, (batch, 2 * N), dtype=np.uint64)
+    exps = rng.integers(0, 2 * N, count).astype(np.uint32)
+    exps[0], exps[-1] = 0, 2 * N - 1
+    got = R.to_host(R.glwe_monomial_mul(R.to_device(cts), exps, N)).reshape(batch, count, 2 * N)
+    for q in range(batch):
+        for s in range(count):
+            want = np.concatenate([O.monomial_mul(cts[q, :N], int(exps[s])),
+                                   O.monomial_mul(cts[q, N:], int(exps[s]))])
+            assert np.array_equal(got[q, s], want)
+    big = R.to_host(R.sample_extract(R.to_device(cts), N))
+    for q in range(batch):
+        assert np.array_equal(big[q], O.sample_extract(N, cts[q]))
 
 
 # ------------------------------------------------- Step 3 of the lookup, chained ---
@@ -189,3 +211,33 @@ def test_select_chain_bit_exact(O, torch_dev):
         fin = O.trace(N, 4, 12, O.blind_rotate_glwe_batch(op, lwe_S[q:q + 1], ks.bsk,
                                                           Rq[None, :], O.NTT)[0], autk, O.NTT)
         assert np.array_equal(got[q], fin)
+
+
+def test_multi_value_batching_chain_bit_exact(O, torch_dev):
+    """Sec. 3.3.2 on the GPU: K = 16 values packed in one ciphertext per
+    batch item, moved to the constant term (monomial copies), isolated by
+    the trace, extracted and key-switched to LWE inputs, then shifted back
+    and recombined; every intermediate equals the oracle's."""
+    w, op, ks, bsk, ksk = keyset(O, "llama3_8b_silu")
+    N, K, batch = w.N, 16, 2
+    rng = np.random.default_rng(30)
+    autk = O.autk_keygen(31, N, 4, 12, SIGMA, ks.glwe_key)
+    autk_dev = R.autk_prepare(R.to_device(autk), w.params(), 4)
+    packed = O.glwe_encrypt(32, SIGMA, ks.glwe_key, rng.integers(0, P, (batch, N), dtype=np.uint64))
+    pos = np.sort(rng.choice(N, K, replace=False)).astype(np.uint32)
+    moved = R.glwe_monomial_mul(R.to_device(packed), (2 * N - pos) % (2 * N), N)
+    singles = R.trace(moved.reshape(batch * K, 2 * N), autk_dev, w.params(), 4, 12)
+    lwe = R.keyswitch(R.sample_extract(singles, N), ksk, w.params())
+    back = R.glwe_recombine(singles, K, N, exps=pos)
+    got_s, got_l, got_b = R.to_host(singles), R.to_host(lwe), R.to_host(back)
+    for q in range(batch):
+        mv = np.stack([np.concatenate([O.monomial_mul(packed[q, :N], int(2 * N - c)),
+                                       O.monomial_mul(packed[q, N:], int(2 * N - c))])
+                       for c in pos])
+        tr = O.trace_batch(N, 4, 12, mv, autk, O.NTT)
+        assert np.array_equal(got_s.reshape(batch, K, 2 * N)[q], tr)
+        for j in range(K):
+            big = O.sample_extract(N, tr[j])
+            assert np.array_equal(got_l.reshape(batch, K, w.n + 1)[q, j],
+                                  O.keyswitch(op, big, ks.ksk))
+        assert np.array_equal(got_b[q], O.glwe_recombine(tr, pos))

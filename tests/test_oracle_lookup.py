@@ -330,3 +330,58 @@ def test_paper_lookup_example_end_to_end(O):
     assert abs(ph[0] - pr["r_0"][1]) <= 5e-4 and abs(ph[1] - pr["r_1"][1]) <= 5e-4
     out = dec_phase(select(R, 0), sx + sp)                  # S = 0
     assert abs(out[0] - pr["result"]) <= 5e-4 and all(abs(v) < 1e-6 for v in out[1:])
+
+
+# ---------------------------------------------------------- multi-value batching ---
+
+def test_multi_value_batching_trivial_exact(O):
+    """Sec. 3.3.2: element j of a packed ciphertext is moved to the constant
+    term by X^(-c_j) and isolated by the trace; shifting each result back by
+    X^(c_j) and summing restores the packed values.  On a mask-free
+    ciphertext every step is exact."""
+    rng = np.random.default_rng(20)
+    N = 64
+    S = np.asarray(rng.integers(0, 2, N), dtype=np.uint64)
+    autk = O.autk_keygen(22, N, TR_L, TR_B, 2.0 ** -40, S)
+    m = rand_poly(rng, N)
+    c = np.concatenate([np.zeros(N, np.uint64), m])
+    pos = [0, 3, 17, 40, 63]
+    singles = []
+    for cj in pos:
+        moved = np.concatenate([O.monomial_mul(c[:N], (2 * N - cj) % (2 * N)),
+                                O.monomial_mul(c[N:], (2 * N - cj) % (2 * N))])
+        t = O.trace(N, TR_L, TR_B, moved, autk)
+        assert np.all(t[:N] == 0) and int(t[N]) == int(m[cj]) and np.all(t[N + 1:] == 0)
+        singles.append(t)
+    back = O.glwe_recombine(np.stack(singles), np.array(pos, np.uint32))
+    want = np.zeros(N, np.uint64)
+    want[pos] = m[pos]
+    assert np.all(back[:N] == 0) and np.array_equal(back[N:], want)
+
+
+def test_multi_value_batching_noise_free_bound(O):
+    """With noise-free keys each extracted element's phase is the packed
+    value within the trace bound (N-1) N 2^(s-1), and the recombined phase
+    holds every value at its position within K times that."""
+    rng = np.random.default_rng(21)
+    N = 32
+    s_bits = 64 - TR_L * TR_B
+    S = np.asarray(rng.integers(0, 2, N), dtype=np.uint64)
+    autk = O.autk_keygen(23, N, TR_L, TR_B, 0.0, S)
+    c = rand_poly(rng, 2 * N)
+    ph = O.glwe_phase(S, c, O.SCHOOLBOOK)
+    pos = [1, 5, 30]
+    bound = (N - 1) * N * 2 ** (s_bits - 1)
+    singles = []
+    for cj in pos:
+        moved = np.concatenate([O.monomial_mul(c[:N], 2 * N - cj), O.monomial_mul(c[N:], 2 * N - cj)])
+        t = O.trace(N, TR_L, TR_B, moved, autk)
+        pt = O.glwe_phase(S, t, O.SCHOOLBOOK)
+        assert abs(centred(int(pt[0]) - int(ph[cj]))) <= bound
+        assert all(abs(centred(v)) <= bound for v in pt[1:])
+        singles.append(t)
+    back = O.glwe_phase(S, O.glwe_recombine(np.stack(singles), np.array(pos, np.uint32)),
+                        O.SCHOOLBOOK)
+    for j in range(N):
+        want = int(ph[j]) if j in pos else 0
+        assert abs(centred(int(back[j]) - want)) <= len(pos) * bound
