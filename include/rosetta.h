@@ -201,17 +201,32 @@ rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *
  *    row (k-1, t) is a GLWE encryption under S of tau_(2^k+1)(S) g_t. */
 
 /* Blind rotation of ciphertext test polynomials (Sec. 3.2, Step 3
- * "BlindRot" and the selection of Step 2): for every ciphertext q of the
- * batch, ACC = X^(-b~) glwe_tp[q] (both components), then the CMux loop of
- * rosetta_blind_rotate.  glwe_tp [batch][2N] (device, one GLWE ciphertext
- * under the GLWE key per LWE ciphertext).  extract = 0: out [batch][2N]
- * holds the accumulators; extract != 0: out [batch][N+1] holds their sample
- * extractions (then rosetta_keyswitch completes a PBS whose table is
- * encrypted).  out must not overlap the inputs. */
+ * "BlindRot" and the selection of Step 2): LWE selector q of lwe_in
+ * [batch][n+1] is paired with the `group` consecutive GLWE ciphertexts
+ * glwe_tp[q*group .. q*group+group) (device, [batch*group][2N], under the
+ * GLWE key); for each, ACC = X^(-b~) tp (both components), then the CMux
+ * loop of rosetta_blind_rotate.  extract = 0: out [batch*group][2N] holds
+ * the accumulators; extract != 0: out [batch*group][N+1] holds their
+ * sample extractions (rosetta_keyswitch then completes a PBS whose table is
+ * encrypted).  1 <= group <= 4096; out must not overlap the inputs. */
 rosetta_status rosetta_blind_rotate_glwe(const uint64_t *lwe_in, const uint64_t *bsk_dev,
                                          const uint64_t *glwe_tp, uint64_t *out, size_t batch,
-                                         const rosetta_params *params, int extract,
-                                         void *stream);
+                                         uint32_t group, const rosetta_params *params,
+                                         int extract, void *stream);
+
+/* LWE copies with shifted bodies (comparison inputs x - tau_j of Step 1):
+ * lwe_out[q][j] = lwe_in[q] + (0, .., 0, consts[j]) for j < count, with
+ * lwe_in [batch][dim+1], lwe_out [batch][count][dim+1] (device, not
+ * overlapping); consts: host array, values below p; 1 <= count <= 64. */
+rosetta_status rosetta_lwe_add_consts(const uint64_t *lwe_in, const uint64_t *consts,
+                                      uint64_t *lwe_out, size_t batch, uint32_t count,
+                                      uint32_t dim, void *stream);
+
+/* Group sums (the segment index S = sum_j [x >= tau_j] of Step 1):
+ * lwe_out[q] = sum_{j < count} lwe_in[q][j] + (0, .., 0, c0), lwe_in
+ * [batch][count][dim+1], lwe_out [batch][dim+1] (device, not overlapping). */
+rosetta_status rosetta_lwe_sum_groups(const uint64_t *lwe_in, uint64_t c0, uint64_t *lwe_out,
+                                      size_t batch, uint32_t count, uint32_t dim, void *stream);
 
 /* Words of an automorphism key with `level` gadget levels: log2(N) level 2 N. */
 size_t rosetta_autk_words(const rosetta_params *params, uint32_t level);
@@ -270,6 +285,98 @@ rosetta_status rosetta_glwe_monomial_mul(const uint64_t *glwe_in, const uint32_t
  * (device, not overlapping). */
 rosetta_status rosetta_sample_extract(const uint64_t *glwe_in, uint64_t *big_out, size_t batch,
                                       uint32_t N, void *stream);
+
+/* ---- the TFHE core of the cryptographic lookup (Sec. 3.2, Algorithm 1,
+ * Steps 1-3) ---------------------------------------------------------------
+ *
+ * For a batch of inputs x, each given as a GLWE ciphertext [[x]]_RLWE of
+ * round(x 2^sx) in the constant coefficient and an LWE ciphertext
+ * [[x]]_cmp of round(x 2^sc) under the LWE key, the pipeline returns GLWE
+ * ciphertexts of round(f~(x) 2^(sx+sp)) in the constant coefficient (other
+ * coefficients zero up to noise) at scale 2^(sx+sv), f~ the segmented LUT
+ * (a, b, tau) of rosetta_seglut_build.
+ *
+ * ENCODINGS (the paper names the steps but not their encodings):
+ *  - Step 1, HomComp(x, tau_j) for j = 1..nseg-1: a PBS of
+ *    [[x]]_cmp - round(tau_j 2^sc) with the constant test polynomial
+ *    mu = floor(p / 4 nseg) (a sign bootstrap), plus mu: 2 mu if x >= tau_j,
+ *    else 0 (up to noise; inputs within the bootstrap's resolution of tau_j
+ *    may fall on either side).  S = sum_j of them: the segment index at scale
+ *    2 mu ~ p / 2 nseg, i.e. a rotation by S N / nseg.
+ *  - Step 2, construct: t = p(X) [[x]]_RLWE + q(X), where coefficient j of
+ *    p and q holds segment s = floor((j + h) / box)'s slope
+ *    nbr / (tau_{s+1} - tau_s) at scale 2^sp and offset
+ *    -tau_s nbr / (tau_{s+1} - tau_s) - 1/2 + margin at 2^(sx+sp)
+ *    (box = N / nseg, h = box / 2; coefficients j >= N - h hold segment 0's
+ *    values negated, the negacyclic image).  Select: I = PBS(t, S) (blind
+ *    rotation of t by S, extraction, key switching); with
+ *    sx + sp = 63 - log2 N one unit of t is one rotation step, so I rotates
+ *    by floor(t_S) + margin.
+ *  - Step 3, construct: r_s = a_s(X) [[x]]_RLWE + b_s(X), coefficient j
+ *    holding interval clamp(j - margin, 0, nbr-1) of segment s (slope at
+ *    2^sv, offset at 2^(sx+sv): the values get their own scale, larger than
+ *    the rotation unit of the selectors, since the trace's key-switching
+ *    noise grows with N).  Select by I: Trace(BlindRot(r_s, I)) for
+ *    every s (one selector, nseg test polynomials).  Recombine:
+ *    R = sum_s X^(s box) r_s, spread over each segment's window by the
+ *    product with W(X) = sum_{k=-h}^{box-h-1} X^k.  Select by S:
+ *    Trace(BlindRot(R W, S)).
+ *  - Requirements: nseg a power of two in [2, 16]; nbr + 2 margin <= N;
+ *    sx + sp = 63 - log2 N; sx + sv <= 62; |x - tau_j| 2^sc < p / 4.  Coefficients are
+ *    round(v 2^k) (half to even, as doubles) reduced exactly mod p, so
+ *    offsets larger than the scale allows (q_s) wrap harmlessly: only
+ *    p_s x + q_s, in [0, nbr) for the selected segment, must fit.
+ *
+ * The plaintext block [(4 + 2 nseg) N] words: p, q, a_0..a_{nseg-1},
+ * b_0..b_{nseg-1}, W, the sign test polynomial; constants [nseg]:
+ * -round(tau_j 2^sc) mod p for j = 1..nseg-1, then (nseg-1) mu. */
+typedef struct rosetta_lookup_params {
+  uint32_t nseg;           /* N_seg, a power of two in [2, 16] */
+  uint32_t nbr;            /* intervals per segment */
+  uint32_t margin;         /* guard coefficients before and after the intervals */
+  uint32_t x_scale_log;    /* sx: scale of [[x]]_RLWE */
+  uint32_t coef_scale_log; /* sp: scale of Step 2 slopes (sx + sp = 63 - log2 N) */
+  uint32_t val_scale_log;  /* sv: scale of Step 3 slopes; output at 2^(sx+sv) */
+  uint32_t cmp_scale_log;  /* sc: scale of [[x]]_cmp */
+  uint32_t trace_level;    /* automorphism key levels */
+  uint32_t trace_base_log; /* automorphism key base log */
+} rosetta_lookup_params;
+
+/* Words of the plaintext block: (4 + 2 nseg) N. */
+size_t rosetta_lookup_plain_words(const rosetta_params *params,
+                                  const rosetta_lookup_params *lp);
+
+/* Host encoder of the plaintext block and constants (layouts above) from
+ * boundaries tau[nseg+1] and coefficients a, b [nseg][nbr] (host arrays). */
+rosetta_status rosetta_lookup_encode(const rosetta_params *params,
+                                     const rosetta_lookup_params *lp, const double *tau,
+                                     const double *a, const double *b, uint64_t *plain,
+                                     uint64_t *consts);
+
+/* Plaintext block (device) -> prepared block (device, same size, not
+ * overlapping): p, the a_s and W to the multiplier form of
+ * rosetta_plain_prepare, the rest copied. */
+rosetta_status rosetta_lookup_prepare(const uint64_t *plain_dev, uint64_t *plain_prep_dev,
+                                      const rosetta_params *params,
+                                      const rosetta_lookup_params *lp, void *stream);
+
+/* Device workspace of rosetta_lookup_eval for `batch` inputs. */
+size_t rosetta_lookup_workspace_bytes(const rosetta_params *params,
+                                      const rosetta_lookup_params *lp, size_t batch);
+
+/* Steps 1-3 for a batch: x_rlwe [batch][2N], x_cmp [batch][n+1], prepared
+ * keys (bootstrapping, key switching, automorphism), the prepared plaintext
+ * block and the host constants; out [batch][2N] (device, not overlapping the
+ * workspace).  Per input: nseg-1 PBS (Step 1), one blind rotation of an
+ * encrypted test polynomial + extraction + key switch (Step 2), nseg + 1
+ * blind rotations of encrypted test polynomials and traces (Step 3), and
+ * nseg + 2 plaintext products. */
+rosetta_status rosetta_lookup_eval(const uint64_t *x_rlwe, const uint64_t *x_cmp,
+                                   const uint64_t *bsk_dev, const uint64_t *ksk_dev,
+                                   const uint64_t *autk_dev, const uint64_t *plain_prep_dev,
+                                   const uint64_t *consts, uint64_t *out, size_t batch,
+                                   const rosetta_params *params, const rosetta_lookup_params *lp,
+                                   void *workspace, size_t workspace_bytes, void *stream);
 
 /* ---- adaptive segmented LUT (Sec. 3.1), host ---------------------------
  *

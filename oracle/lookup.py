@@ -1,0 +1,114 @@
+"""Oracle of the TFHE core of the cryptographic lookup (ROSETTA Sec. 3.2,
+Algorithm 1, Steps 1-3), composed from the C oracle's primitives.
+
+TEST INFRASTRUCTURE ONLY (tests/ and nothing in the product path).  The
+encodings follow the conventions stated in the library header for
+rosetta_lookup_params, written out here independently:
+
+  Step 1  y_j = [[x]]_cmp - round(tau_j 2^sc); c_j = PBS(y_j, v = mu) + mu,
+          mu = floor(p / 4 nseg); S = sum_j c_j.
+  Step 2  t = p(X) [[x]] + q(X) (segment s over the window of rotations
+          rounding to s N/nseg, the wrapped part negated); I = KS(SE(
+          BlindRot(t, S))).
+  Step 3  r_s = a_s(X) [[x]] + b_s(X) (interval i at coefficient i + margin,
+          slopes at 2^sv, offsets and the result at 2^(sx+sv));
+          r_s <- Trace(BlindRot(r_s, I)); R = sum_s X^(s N/nseg) r_s;
+          out = Trace(BlindRot(W R, S)).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import oracle as O
+
+P = O.P
+
+
+def enc(v: float, k: int) -> int:
+    """round(v 2^k) (half to even, of the double v 2^k) as an element of Z_p."""
+    return round(float(v) * 2.0 ** k) % P
+
+
+def encode(N, nseg, nbr, margin, sx, sp, sv, sc, tau, a, b):
+    """Plaintext polynomials and constants of the lookup (host side)."""
+    box = N // nseg
+    h = box // 2
+    p_hat = np.zeros(N, np.uint64)
+    q_hat = np.zeros(N, np.uint64)
+    for j in range(N):
+        wrapped = j >= N - h
+        s = 0 if wrapped else (j + h) // box
+        width = tau[s + 1] - tau[s]
+        pv = enc(nbr / width, sp)
+        qv = enc(-tau[s] * nbr / width - 0.5 + margin, sx + sp)
+        p_hat[j] = (P - pv) % P if wrapped else pv
+        q_hat[j] = (P - qv) % P if wrapped else qv
+    a_hat = np.zeros((nseg, N), np.uint64)
+    b_hat = np.zeros((nseg, N), np.uint64)
+    for s in range(nseg):
+        for j in range(N):
+            i = min(max(j - margin, 0), nbr - 1)
+            a_hat[s, j] = enc(a[s][i], sv)
+            b_hat[s, j] = enc(b[s][i], sx + sv)
+    window = np.zeros(N, np.uint64)
+    for k in range(-h, box - h):
+        if k >= 0:
+            window[k] = 1
+        else:
+            window[N + k] = P - 1          # X^k = -X^(N+k)
+    mu = P // (4 * nseg)
+    sign_lut = np.full(N, mu, np.uint64)
+    consts = np.array([enc(-tau[j], sc) for j in range(1, nseg)] + [(nseg - 1) * mu % P],
+                      dtype=np.uint64)
+    return dict(p_hat=p_hat, q_hat=q_hat, a_hat=a_hat, b_hat=b_hat, window=window,
+                sign_lut=sign_lut, consts=consts)
+
+
+def block(parts) -> np.ndarray:
+    """The library's plaintext block order: p, q, a_s, b_s, W, sign LUT."""
+    return np.concatenate([parts["p_hat"], parts["q_hat"], parts["a_hat"].reshape(-1),
+                           parts["b_hat"].reshape(-1), parts["window"], parts["sign_lut"]])
+
+
+def lwe_add(a, b):
+    return ((a.astype(object) + b.astype(object)) % P).astype(np.uint64)
+
+
+def evaluate(prm, ks, autk, trace_level, trace_base_log, parts, nseg, x_rlwe, x_cmp,
+             kind=O.NTT, nthreads=0, want_steps=False):
+    n, N = prm.n, prm.N
+    batch = x_cmp.shape[0]
+    consts = parts["consts"]
+    # Step 1
+    ys = np.zeros((batch, nseg - 1, n + 1), np.uint64)
+    for q in range(batch):
+        for j in range(nseg - 1):
+            ys[q, j] = x_cmp[q]
+            ys[q, j, n] = (int(x_cmp[q, n]) + int(consts[j])) % P
+    cmp = O.pbs(prm, ys.reshape(-1, n + 1), ks.bsk, ks.ksk, parts["sign_lut"], kind, nthreads)
+    cmp = cmp.reshape(batch, nseg - 1, n + 1)
+    S = np.zeros((batch, n + 1), np.uint64)
+    for q in range(batch):
+        acc = np.zeros(n + 1, np.uint64)
+        acc[n] = consts[nseg - 1]
+        for j in range(nseg - 1):
+            acc = lwe_add(acc, cmp[q, j])
+        S[q] = acc
+    # Step 2
+    T = np.stack([O.glwe_mul_plain(x_rlwe[q], parts["p_hat"], parts["q_hat"], kind)
+                  for q in range(batch)])
+    acc = O.blind_rotate_glwe_batch(prm, S, ks.bsk, T, kind, nthreads)
+    I = np.stack([O.keyswitch(prm, O.sample_extract(N, acc[q]), ks.ksk) for q in range(batch)])
+    # Step 3
+    rs = np.stack([O.glwe_mul_plain(x_rlwe[q], parts["a_hat"][s], parts["b_hat"][s], kind)
+                   for q in range(batch) for s in range(nseg)])
+    sel = O.blind_rotate_glwe_batch(prm, np.repeat(I, nseg, axis=0), ks.bsk, rs, kind, nthreads)
+    sel = O.trace_batch(N, trace_level, trace_base_log, sel, autk, kind, nthreads)
+    exps = np.array([s * (N // nseg) for s in range(nseg)], np.uint32)
+    R = np.stack([O.glwe_recombine(sel[q * nseg:(q + 1) * nseg], exps) for q in range(batch)])
+    RB = np.stack([O.glwe_mul_plain(R[q], parts["window"], None, kind) for q in range(batch)])
+    fin = O.blind_rotate_glwe_batch(prm, S, ks.bsk, RB, kind, nthreads)
+    out = O.trace_batch(N, trace_level, trace_base_log, fin, autk, kind, nthreads)
+    if want_steps:
+        return out, dict(cmp=cmp, S=S, T=T, I=I, r=rs, sel=sel, R=R, RB=RB)
+    return out

@@ -295,7 +295,7 @@ rosetta_status rosetta_pbs_batch_ws(const uint64_t *lwe_in, const uint64_t *bsk_
   if ((st = get_tables(params->N, tb))) return st;
   uint64_t *big = (uint64_t *)workspace;
   hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, lut, big, batch, *params, tb, BR_EXTRACT,
-                                     false, (hipStream_t)stream);
+                                     0, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "blind_rotate launch");
   e = launch_keyswitch(big, ksk_dev, lwe_out, batch, *params, (hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "keyswitch launch");
@@ -329,7 +329,7 @@ rosetta_status rosetta_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_
   Tables tb;
   if ((st = get_tables(params->N, tb))) return st;
   hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, lut, glwe_out, batch, *params, tb, BR_GLWE,
-                                     false, (hipStream_t)stream);
+                                     0, (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "blind_rotate launch");
 }
 
@@ -346,7 +346,7 @@ rosetta_status rosetta_blind_rotate_extract(const uint64_t *lwe_in, const uint64
   Tables tb;
   if ((st = get_tables(params->N, tb))) return st;
   hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, lut, big_out, batch, *params, tb,
-                                     BR_EXTRACT, false, (hipStream_t)stream);
+                                     BR_EXTRACT, 0, (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "blind_rotate launch");
 }
 
@@ -414,24 +414,63 @@ rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *
 
 rosetta_status rosetta_blind_rotate_glwe(const uint64_t *lwe_in, const uint64_t *bsk_dev,
                                          const uint64_t *glwe_tp, uint64_t *out, size_t batch,
-                                         const rosetta_params *params, int extract,
-                                         void *stream) {
+                                         uint32_t group, const rosetta_params *params,
+                                         int extract, void *stream) {
   rosetta_status st = check_params(params);
   if (st) return st;
+  if (group < 1 || group > 4096) return fail(ROSETTA_ERR_PARAMS, "need 1 <= group <= 4096");
   if (batch == 0) return ok();
   if (!lwe_in || !bsk_dev || !glwe_tp || !out)
     return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
-  const size_t N = params->N;
-  const size_t out_bytes = batch * (extract ? N + 1 : 2 * N) * 8;
+  const size_t N = params->N, tps = batch * group;
+  const size_t out_bytes = tps * (extract ? N + 1 : 2 * N) * 8;
   if (any_overlap(out, out_bytes, lwe_in, lwe_words(params, batch) * 8) ||
-      any_overlap(out, out_bytes, glwe_tp, batch * 2 * N * 8) ||
+      any_overlap(out, out_bytes, glwe_tp, tps * 2 * N * 8) ||
       any_overlap(out, out_bytes, bsk_dev, rosetta_bsk_words(params) * 8))
     return fail(ROSETTA_ERR_ALIAS, "output overlaps an input");
   Tables tb;
   if ((st = get_tables(params->N, tb))) return st;
-  hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, glwe_tp, out, batch, *params, tb,
-                                     extract ? BR_EXTRACT : BR_GLWE, true, (hipStream_t)stream);
+  hipError_t e = launch_blind_rotate(lwe_in, bsk_dev, glwe_tp, out, tps, *params, tb,
+                                     extract ? BR_EXTRACT : BR_GLWE, (int)group,
+                                     (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "blind_rotate_glwe launch");
+}
+
+rosetta_status rosetta_lwe_add_consts(const uint64_t *lwe_in, const uint64_t *consts,
+                                      uint64_t *lwe_out, size_t batch, uint32_t count,
+                                      uint32_t dim, void *stream) {
+  if (count < 1 || count > (uint32_t)(MAX_MONOMIALS / 4))
+    return fail(ROSETTA_ERR_PARAMS, "need 1 <= count <= %d", MAX_MONOMIALS / 4);
+  if (dim < 1) return fail(ROSETTA_ERR_PARAMS, "need dim >= 1");
+  if (!consts) return fail(ROSETTA_ERR_NULL, "consts is NULL");
+  Consts cs;
+  for (uint32_t j = 0; j < count; ++j) {
+    if (consts[j] >= GL_P) return fail(ROSETTA_ERR_PARAMS, "constant %u is not below p", j);
+    cs.c[j] = consts[j];
+  }
+  if (batch == 0) return ok();
+  if (!lwe_in || !lwe_out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t w = (size_t)dim + 1;
+  if (any_overlap(lwe_out, batch * count * w * 8, lwe_in, batch * w * 8))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps the input");
+  hipError_t e = launch_lwe_add_consts(lwe_in, lwe_out, batch, (int)count, (int)dim, cs,
+                                       (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "lwe_add_consts launch");
+}
+
+rosetta_status rosetta_lwe_sum_groups(const uint64_t *lwe_in, uint64_t c0, uint64_t *lwe_out,
+                                      size_t batch, uint32_t count, uint32_t dim,
+                                      void *stream) {
+  if (count < 1 || dim < 1) return fail(ROSETTA_ERR_PARAMS, "need count, dim >= 1");
+  if (c0 >= GL_P) return fail(ROSETTA_ERR_PARAMS, "constant is not below p");
+  if (batch == 0) return ok();
+  if (!lwe_in || !lwe_out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t w = (size_t)dim + 1;
+  if (any_overlap(lwe_out, batch * w * 8, lwe_in, batch * count * w * 8))
+    return fail(ROSETTA_ERR_ALIAS, "output overlaps the input");
+  hipError_t e = launch_lwe_sum_groups(lwe_in, lwe_out, batch, (int)count, (int)dim, c0,
+                                       (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "lwe_sum_groups launch");
 }
 
 static rosetta_status check_trace_params(const rosetta_params *p, uint32_t level,

@@ -36,7 +36,7 @@ hipError_t launch_ksk_prepare(const uint64_t *ksk_std, uint64_t *ksk_dev,
 hipError_t launch_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
                                const uint64_t *lut, uint64_t *out, size_t batch,
                                const rosetta_params &p, const Tables &tb, BrMode mode,
-                               bool tp_glwe, hipStream_t st);
+                               int tp_glwe, hipStream_t st);
 hipError_t launch_rows_prepare(const uint64_t *rows_std, uint64_t *rows_dev, size_t rows,
                                uint32_t N, const Tables &tb, hipStream_t st);
 hipError_t launch_trace(const uint64_t *in, const uint64_t *autk_dev, uint64_t *out,
@@ -57,6 +57,15 @@ hipError_t launch_glwe_monomial_mul(const uint64_t *in, uint64_t *out, size_t ba
                                     const Exponents &ex, uint32_t N, hipStream_t st);
 hipError_t launch_sample_extract(const uint64_t *in, uint64_t *out, size_t batch, uint32_t N,
                                  hipStream_t st);
+
+// Per-copy constants passed by value (at most MAX_MONOMIALS).
+struct Consts {
+  uint64_t c[MAX_MONOMIALS / 4];
+};
+hipError_t launch_lwe_add_consts(const uint64_t *in, uint64_t *out, size_t batch, int count,
+                                int dim, const Consts &cs, hipStream_t st);
+hipError_t launch_lwe_sum_groups(const uint64_t *in, uint64_t *out, size_t batch, int count,
+                                 int dim, uint64_t c0, hipStream_t st);
 hipError_t launch_keyswitch(const uint64_t *big, const uint64_t *ksk_dev, uint64_t *out,
                             size_t batch, const rosetta_params &p, hipStream_t st);
 hipError_t launch_ntt(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,

@@ -191,6 +191,10 @@ size_t br_lds_bytes(int n) {
 // batch (a test polynomial that is itself encrypted, as in the lookup
 // protocol's construct-then-select) and both of its components are rotated
 // by X^(-b~).
+//
+// tp_glwe = g > 1 pairs each LWE selector with g consecutive test-polynomial
+// ciphertexts (workgroup b uses selector b / g), so that one encrypted
+// index selects in several ciphertexts at once.
 template <class S, int L, typename RT, bool PF>
 __global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(br_waves_per_eu<S>())))
 k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
@@ -204,7 +208,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
   const size_t ct = blockIdx.x;
 
   // a1: rounded rotation amounts of the whole ciphertext; twiddles
-  const u64 *lwe = lwe_in + ct * (size_t)(n + 1);
+  const u64 *lwe = lwe_in + (ct / (size_t)(tp_glwe > 1 ? tp_glwe : 1)) * (size_t)(n + 1);
   for (int i = tid; i <= n; i += T) rot[i] = (uint16_t)gl_modswitch(lwe[i], S::LOGN);
   load_twiddles<S>(tw, zeta, tid);
   __syncthreads();
@@ -548,6 +552,33 @@ __global__ void k_sample_extract(const u64 *__restrict__ in, u64 *__restrict__ o
 }
 
 // ---------------------------------------------------------------------------
+// LWE linear maps (comparison inputs and index sums of the lookup)
+// ---------------------------------------------------------------------------
+
+// out[q][j] = in[q] + (0, .., 0, c_j): `count` shifted copies per ciphertext.
+__global__ void k_lwe_add_consts(const u64 *__restrict__ in, u64 *__restrict__ out,
+                                 size_t batch, int count, int dim, Consts cs) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t w = (size_t)dim + 1;
+  if (i >= batch * count * w) return;
+  const size_t c = i % w, j = (i / w) % count, q = i / (w * count);
+  const u64 v = in[q * w + c];
+  out[i] = c == (size_t)dim ? gl_add(v, cs.c[j]) : v;
+}
+
+// out[q] = sum_{j < count} in[q][j] + (0, .., 0, c): sums of groups.
+__global__ void k_lwe_sum_groups(const u64 *__restrict__ in, u64 *__restrict__ out,
+                                 size_t batch, int count, int dim, u64 c0) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t w = (size_t)dim + 1;
+  if (i >= batch * w) return;
+  const size_t c = i % w, q = i / w;
+  u64 acc = c == (size_t)dim ? c0 : 0;
+  for (int j = 0; j < count; ++j) acc = gl_add(acc, in[(q * count + j) * w + c]);
+  out[i] = acc;
+}
+
+// ---------------------------------------------------------------------------
 // Key switching
 // ---------------------------------------------------------------------------
 
@@ -711,9 +742,9 @@ static hipError_t launch_br_levels(const uint64_t *lwe_in, const uint64_t *bsk_d
 hipError_t launch_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
                                const uint64_t *lut, uint64_t *out, size_t batch,
                                const rosetta_params &p, const Tables &tb, BrMode mode,
-                               bool tp_glwe, hipStream_t st) {
+                               int tp_glwe, hipStream_t st) {
   hipError_t e = hipSuccess;
-  const int tpg = tp_glwe ? 1 : 0;
+  const int tpg = tp_glwe;
 #define ROSETTA_BR_L(LV)                                                                       \
   case LV:                                                                                     \
     e = launch_br_levels<S, LV>(lwe_in, bsk_dev, lut, out, batch, p, tb, (int)mode, tpg, st); \
@@ -773,6 +804,20 @@ hipError_t launch_glwe_monomial_mul(const uint64_t *in, uint64_t *out, size_t ba
                                     const Exponents &ex, uint32_t N, hipStream_t st) {
   hipLaunchKernelGGL(k_glwe_monomial_mul, dim3(grid_of(batch * count * 2 * (size_t)N)),
                      dim3(256), 0, st, in, out, batch, count, ex, (int)N);
+  return hipGetLastError();
+}
+
+hipError_t launch_lwe_add_consts(const uint64_t *in, uint64_t *out, size_t batch, int count,
+                                int dim, const Consts &cs, hipStream_t st) {
+  hipLaunchKernelGGL(k_lwe_add_consts, dim3(grid_of(batch * count * (size_t)(dim + 1))),
+                     dim3(256), 0, st, in, out, batch, count, dim, cs);
+  return hipGetLastError();
+}
+
+hipError_t launch_lwe_sum_groups(const uint64_t *in, uint64_t *out, size_t batch, int count,
+                                 int dim, uint64_t c0, hipStream_t st) {
+  hipLaunchKernelGGL(k_lwe_sum_groups, dim3(grid_of(batch * (size_t)(dim + 1))), dim3(256), 0,
+                     st, in, out, batch, count, dim, (u64)c0);
   return hipGetLastError();
 }
 

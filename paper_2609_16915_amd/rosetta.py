@@ -80,8 +80,12 @@ SIGNATURES = {
     "rosetta_lwe_decrypt": (_ST, [_pp, _u64p, C.c_uint32, _u64p, C.c_size_t, _u64p]),
     "rosetta_lut_build": (_ST, [_pp, _u64p, _u64p]),
     "rosetta_shutdown": (_ST, []),
-    "rosetta_blind_rotate_glwe": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp, C.c_int,
-                                        C.c_void_p]),
+    "rosetta_blind_rotate_glwe": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, C.c_uint32,
+                                        _pp, C.c_int, C.c_void_p]),
+    "rosetta_lwe_add_consts": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, C.c_uint32, C.c_uint32,
+                                     C.c_void_p]),
+    "rosetta_lwe_sum_groups": (_ST, [_u64p, C.c_uint64, _u64p, C.c_size_t, C.c_uint32,
+                                     C.c_uint32, C.c_void_p]),
     "rosetta_autk_words": (C.c_size_t, [_pp, C.c_uint32]),
     "rosetta_autk_prepare": (_ST, [_u64p, _u64p, _pp, C.c_uint32, C.c_void_p]),
     "rosetta_trace": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, _pp, C.c_uint32, C.c_uint32,
@@ -109,6 +113,26 @@ SIGNATURES = {
                                        _u64p, _u64p, C.c_size_t, _u64p]),
     "rosetta_encode_fixed": (_ST, [_u64p, C.c_size_t, C.c_int, _u64p]),
 }
+
+
+
+class LookupParams(C.Structure):
+    """rosetta_lookup_params (include/rosetta.h)."""
+
+    _fields_ = [(name, C.c_uint32) for name in
+                ("nseg", "nbr", "margin", "x_scale_log", "coef_scale_log", "val_scale_log",
+                 "cmp_scale_log", "trace_level", "trace_base_log")]
+
+
+_lpp = C.POINTER(LookupParams)
+SIGNATURES.update({
+    "rosetta_lookup_plain_words": (C.c_size_t, [_pp, _lpp]),
+    "rosetta_lookup_encode": (_ST, [_pp, _lpp, _u64p, _u64p, _u64p, _u64p, _u64p]),
+    "rosetta_lookup_prepare": (_ST, [_u64p, _u64p, _pp, _lpp, C.c_void_p]),
+    "rosetta_lookup_workspace_bytes": (C.c_size_t, [_pp, _lpp, C.c_size_t]),
+    "rosetta_lookup_eval": (_ST, [_u64p, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p,
+                                  C.c_size_t, _pp, _lpp, _u64p, C.c_size_t, C.c_void_p]),
+})
 
 FUNCTIONS = {"inv": 0, "inv_sqrt": 1, "silu": 2, "gelu": 3, "exp": 4}
 SPACINGS = {"uniform": 0, "log": 1}
@@ -305,15 +329,40 @@ def shutdown():
 
 # lookup-protocol primitives ------------------------------------------------
 
-def blind_rotate_glwe(lwe_in, bsk_dev, glwe_tp, params, extract=False, out=None, stream=None):
-    """Blind rotation of per-ciphertext GLWE test polynomials glwe_tp [batch][2N]."""
+def blind_rotate_glwe(lwe_in, bsk_dev, glwe_tp, params, extract=False, group=1, out=None,
+                      stream=None):
+    """Blind rotation of GLWE test polynomials glwe_tp [batch*group][2N], each
+    LWE selector of lwe_in [batch][n+1] serving `group` consecutive ones."""
     p = _params(params)
     batch = lwe_in.numel() // (p.n + 1)
     if out is None:
-        out = empty((batch, p.N + 1) if extract else (batch, 2 * p.N), lwe_in.device)
+        shape = (batch * group, p.N + 1) if extract else (batch * group, 2 * p.N)
+        out = empty(shape, lwe_in.device)
     _check(lib().rosetta_blind_rotate_glwe(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
                                            _dev(glwe_tp, "glwe_tp"), _dev(out, "out"), batch,
-                                           C.byref(p), 1 if extract else 0, _stream(stream)))
+                                           group, C.byref(p), 1 if extract else 0,
+                                           _stream(stream)))
+    return out
+
+
+def lwe_add_consts(lwe_in, consts, dim: int, out=None, stream=None):
+    """out[q][j] = lwe_in[q] + (0, .., 0, consts[j])."""
+    batch = lwe_in.numel() // (dim + 1)
+    c = np.ascontiguousarray(consts, dtype=np.uint64)
+    if out is None:
+        out = empty((batch, c.size, dim + 1), lwe_in.device)
+    _check(lib().rosetta_lwe_add_consts(_dev(lwe_in, "lwe_in"), _np_ptr(c), _dev(out, "lwe_out"),
+                                        batch, c.size, dim, _stream(stream)))
+    return out
+
+
+def lwe_sum_groups(lwe_in, count: int, dim: int, c0: int = 0, out=None, stream=None):
+    """out[q] = sum_j lwe_in[q][j] + (0, .., 0, c0)."""
+    batch = lwe_in.numel() // ((dim + 1) * count)
+    if out is None:
+        out = empty((batch, dim + 1), lwe_in.device)
+    _check(lib().rosetta_lwe_sum_groups(_dev(lwe_in, "lwe_in"), c0, _dev(out, "lwe_out"), batch,
+                                        count, dim, _stream(stream)))
     return out
 
 
@@ -544,4 +593,47 @@ def encode_fixed(v, scale_log: int) -> np.ndarray:
     v = _f64(v)
     out = np.zeros(v.shape, np.uint64)
     _check(lib().rosetta_encode_fixed(_np_ptr(v), v.size, scale_log, _np_ptr(out)))
+    return out
+
+
+# lookup protocol (Algorithm 1, Steps 1-3) ----------------------------------
+
+def lookup_encode(params, lp: LookupParams, tau, a, b):
+    """Host plaintext block [(4 + 2 nseg) N] and constants [nseg]."""
+    p = _params(params)
+    tau, a, b = _f64(tau), _f64(a), _f64(b)
+    plain = np.zeros(lib().rosetta_lookup_plain_words(C.byref(p), C.byref(lp)), np.uint64)
+    consts = np.zeros(lp.nseg, np.uint64)
+    _check(lib().rosetta_lookup_encode(C.byref(p), C.byref(lp), _np_ptr(tau), _np_ptr(a),
+                                       _np_ptr(b), _np_ptr(plain), _np_ptr(consts)))
+    return plain, consts
+
+
+def lookup_prepare(plain_dev, params, lp: LookupParams, out=None, stream=None):
+    p = _params(params)
+    out = empty(plain_dev.shape, plain_dev.device) if out is None else out
+    _check(lib().rosetta_lookup_prepare(_dev(plain_dev, "plain"), _dev(out, "plain_prep"),
+                                        C.byref(p), C.byref(lp), _stream(stream)))
+    return out
+
+
+def lookup_workspace_bytes(params, lp: LookupParams, batch: int) -> int:
+    return lib().rosetta_lookup_workspace_bytes(C.byref(_params(params)), C.byref(lp), batch)
+
+
+def lookup_eval(x_rlwe, x_cmp, bsk_dev, ksk_dev, autk_dev, plain_prep, consts, params,
+                lp: LookupParams, workspace=None, out=None, stream=None):
+    p = _params(params)
+    batch = x_cmp.numel() // (p.n + 1)
+    if out is None:
+        out = empty((batch, 2 * p.N), x_cmp.device)
+    if workspace is None:
+        workspace = empty(lookup_workspace_bytes(p, lp, batch) // 8, x_cmp.device)
+    c = np.ascontiguousarray(consts, np.uint64)
+    _check(lib().rosetta_lookup_eval(_dev(x_rlwe, "x_rlwe"), _dev(x_cmp, "x_cmp"),
+                                     _dev(bsk_dev, "bsk"), _dev(ksk_dev, "ksk"),
+                                     _dev(autk_dev, "autk"), _dev(plain_prep, "plain_prep"),
+                                     _np_ptr(c), _dev(out, "out"), batch, C.byref(p),
+                                     C.byref(lp), _dev(workspace, "workspace"),
+                                     workspace.numel() * 8, _stream(stream)))
     return out

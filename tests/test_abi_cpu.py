@@ -150,8 +150,9 @@ def test_lookup_validation_touches_no_device(L):
     # empty batches are no-ops, NULL pointers are rejected
     assert L.rosetta_trace(None, None, None, 0, C.byref(p), 4, 12, None) == 0
     assert L.rosetta_trace(None, fake, fake, 1, C.byref(p), 4, 12, None) == 1
-    assert L.rosetta_blind_rotate_glwe(None, None, None, None, 0, C.byref(p), 0, None) == 0
-    assert L.rosetta_blind_rotate_glwe(fake, fake, None, fake, 1, C.byref(p), 0, None) == 1
+    assert L.rosetta_blind_rotate_glwe(None, None, None, None, 0, 1, C.byref(p), 0, None) == 0
+    assert L.rosetta_blind_rotate_glwe(fake, fake, fake, fake, 1, 0, C.byref(p), 0, None) == 2
+    assert L.rosetta_blind_rotate_glwe(fake, fake, None, fake, 1, 1, C.byref(p), 0, None) == 1
     assert L.rosetta_glwe_mul_plain(None, None, None, None, 0, 2, 256, None) == 0
     assert L.rosetta_glwe_mul_plain(fake, fake, None, fake, 1, 0, 256, None) == 2
     assert L.rosetta_glwe_mul_plain(fake, fake, None, fake, 1, 2, 100, None) == 3
@@ -168,7 +169,7 @@ def test_lookup_validation_touches_no_device(L):
     two_n = 2 * p.N * 8
     assert L.rosetta_trace(fake, fake + 10 ** 9, fake + 8, 2, C.byref(p), 4, 12, None) == 4
     assert L.rosetta_blind_rotate_glwe(fake, fake + 10 ** 9, fake + 2 * 10 ** 9,
-                                       fake + 2 * 10 ** 9 + 8, 1, C.byref(p), 0, None) == 4
+                                       fake + 2 * 10 ** 9 + 8, 1, 1, C.byref(p), 0, None) == 4
     assert L.rosetta_glwe_recombine(fake, None, fake + two_n, 1, 2, 256, None) == 4
     assert L.rosetta_glwe_mul_plain(fake, fake + 10 ** 9, None, fake + two_n // 2, 1, 1, 256,
                                     None) == 4
