@@ -140,6 +140,64 @@ def lookup_select(R, W, w, p, keys, d_in, bsk, stream, steps):
                                "per_launch_modmul": tr_mm, "launch_ms": round(tr_ms, 3)}}
 
 
+def lookup_protocol(R, W, w, p, keys, bsk, ksk, stream, steps, batch):
+    """The lookup pipeline of Algorithm 1 (Steps 1-3) for SiLU on [-20, 20]
+    with 4 uniform segments over the batch: inputs x ~ N(0, 1) (the FFN
+    activations) encrypted as [[x]]_RLWE and [[x]]_cmp with the library's
+    host helpers; timed on the device; a sample of outputs is decrypted and
+    compared with the cleartext segmented LUT."""
+    import torch
+    sx, sv, sc, margin, nseg = 40, 18, 57, 192, 4
+    sp = 63 - int(math.log2(w.N)) - sx
+    lp = R.LookupParams(nseg=nseg, nbr=w.N - 2 * margin, margin=margin, x_scale_log=sx,
+                        coef_scale_log=sp, val_scale_log=sv, cmp_scale_log=sc,
+                        trace_level=TRACE_LEVEL, trace_base_log=TRACE_BASE_LOG)
+    tau = R.seglut_boundaries(-20.0, 20.0, nseg, "uniform")
+    a, b = R.seglut_build("silu", tau, lp.nbr)
+    plain, consts = R.lookup_encode(p, lp, tau, a, b)
+    prep = R.lookup_prepare(R.to_device(plain), p, lp)
+    autk = R.autk_prepare(R.to_device(R.autk_keygen(w.key_seed + 1, p, TRACE_LEVEL, TRACE_BASE_LOG,
+                                                    w.sigma_glwe, keys["glwe_key"])),
+                          p, TRACE_LEVEL)
+    rng = np.random.default_rng(w.data_seed + 2)
+    xs = np.clip(rng.normal(0.0, 1.0, batch), -20.0, 20.0)
+    m = np.zeros((batch, w.N), np.uint64)
+    m[:, 0] = R.encode_fixed(xs, sx)
+    x_rlwe = R.to_device(R.glwe_encrypt(w.enc_seed + 1, p, w.sigma_glwe, keys["glwe_key"], m))
+    x_cmp = R.to_device(R.lwe_encrypt_plain(w.enc_seed + 2, p, w.sigma_lwe, keys["lwe_key"],
+                                            R.encode_fixed(xs, sc)))
+    ws = R.empty(R.lookup_workspace_bytes(p, lp, batch) // 8)
+    out = R.empty((batch, 2 * w.N))
+
+    def run():
+        R.lookup_eval(x_rlwe, x_cmp, bsk, ksk, autk, prep, consts, p, lp, workspace=ws, out=out)
+
+    run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    sample = np.arange(0, batch, max(1, batch // 512))
+    ph = R.glwe_phase(p, keys["glwe_key"], R.to_host(out)[sample])[:, 0].astype(object)
+    P = 0xFFFFFFFF00000001
+    got = np.array([(v if v <= P // 2 else v - P) / 2.0 ** (sx + sv) for v in ph], dtype=float)
+    err = np.abs(got - R.seglut_eval(tau, a, b, xs[sample]))
+    return {"function": "silu", "domain": [-20.0, 20.0], "nseg": nseg, "nbr": lp.nbr,
+            "batch": batch, "lookups_per_s": round(batch / wall, 2),
+            "ms_per_step": round(wall * 1e3, 3),
+            "events_ms_per_step": round(e0.elapsed_time(e1) / steps, 3),
+            "per_lookup": {"pbs": nseg - 1, "blind_rotations_encrypted_tp": nseg + 2,
+                           "traces": nseg + 1, "plaintext_products": nseg + 2},
+            "decrypt_check": {"sample": int(sample.size), "median_abs_err": float(np.median(err)),
+                              "p99_abs_err": float(np.quantile(err, 0.99)),
+                              "max_abs_err": float(err.max())}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -152,6 +210,10 @@ def main():
                     help="override the workload's batch (experiments only)")
     ap.add_argument("--lookup-steps", type=int, default=3,
                     help="timed steps of the lookup select (0 = skip)")
+    ap.add_argument("--protocol-steps", type=int, default=1,
+                    help="timed steps of the full lookup pipeline (0 = skip)")
+    ap.add_argument("--protocol-batch", type=int, default=0,
+                    help="inputs of the lookup pipeline (default: the workload's batch)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB, outside the timed "
                          "region, as the reference kernel for memory-traffic counters")
@@ -268,6 +330,11 @@ def main():
         log("[bench] lookup select (blind rotation of ciphertext test polynomials + trace)")
         result["lookup_select"] = lookup_select(R, W, w, p, keys, d_in, bsk, stream,
                                                 args.lookup_steps)
+    if args.protocol_steps > 0:
+        log("[bench] lookup pipeline (Algorithm 1, Steps 1-3)")
+        result["lookup_protocol"] = lookup_protocol(R, W, w, p, keys, bsk, ksk, stream,
+                                                    args.protocol_steps,
+                                                    args.protocol_batch or w.batch)
     if args.cpu_seconds > 0:
         log("[bench] CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(w, keys, cts, v, args.cpu_seconds)

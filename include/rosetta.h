@@ -457,6 +457,12 @@ rosetta_status rosetta_lwe_encrypt(uint64_t seed, const rosetta_params *params, 
                                    const uint64_t *key, uint32_t dim, const uint32_t *msgs,
                                    size_t count, uint64_t *lwe_out);
 
+/* Encryption of plaintexts already in Z_p (host; same randomness as
+ * rosetta_lwe_encrypt: masks stream 7, noise stream 8). */
+rosetta_status rosetta_lwe_encrypt_plain(uint64_t seed, double sigma, const uint64_t *key,
+                                         uint32_t dim, const uint64_t *plain, size_t count,
+                                         uint64_t *lwe_out);
+
 /* Decryption of `count` ciphertexts of dimension `dim` to Z_2M (host). */
 rosetta_status rosetta_lwe_decrypt(const rosetta_params *params, const uint64_t *key,
                                    uint32_t dim, const uint64_t *lwe, size_t count,

@@ -220,6 +220,24 @@ rosetta_status rosetta_lwe_encrypt(uint64_t seed, const rosetta_params *p, doubl
   return ROSETTA_OK;
 }
 
+rosetta_status rosetta_lwe_encrypt_plain(uint64_t seed, double sigma, const uint64_t *key,
+                                         uint32_t dim, const uint64_t *plain, size_t count,
+                                         uint64_t *out) {
+  if (!key || !plain || !out) return herr(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const u64 km = substream(seed, ENC_MASK), kn = substream(seed, ENC_NOISE);
+  parallel_rows(count, [&](size_t q) {
+    u64 *ct = out + q * (dim + 1);
+    u64 b = 0;
+    for (uint32_t c = 0; c < dim; ++c) {
+      ct[c] = uniform_zp(km, (u64)q * dim + c);
+      b = gl_add(b, gl_mul(ct[c], key[c]));
+    }
+    b = gl_add(b, plain[q] >= GL_P ? plain[q] - GL_P : plain[q]);
+    ct[dim] = gl_add(b, noise_zp(kn, (u64)q, sigma));
+  });
+  return ROSETTA_OK;
+}
+
 rosetta_status rosetta_lwe_decrypt(const rosetta_params *p, const uint64_t *key, uint32_t dim,
                                    const uint64_t *lwe, size_t count, uint32_t *msgs_out) {
   if (!p) return herr(ROSETTA_ERR_NULL, "params is NULL");

@@ -78,6 +78,8 @@ SIGNATURES = {
     "rosetta_lwe_encrypt": (_ST, [C.c_uint64, _pp, C.c_double, _u64p, C.c_uint32, _u64p,
                                   C.c_size_t, _u64p]),
     "rosetta_lwe_decrypt": (_ST, [_pp, _u64p, C.c_uint32, _u64p, C.c_size_t, _u64p]),
+    "rosetta_lwe_encrypt_plain": (_ST, [C.c_uint64, C.c_double, _u64p, C.c_uint32, _u64p,
+                                        C.c_size_t, _u64p]),
     "rosetta_lut_build": (_ST, [_pp, _u64p, _u64p]),
     "rosetta_shutdown": (_ST, []),
     "rosetta_blind_rotate_glwe": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, C.c_uint32,
@@ -476,6 +478,18 @@ def lwe_encrypt(seed: int, params, sigma: float, key: np.ndarray, msgs) -> np.nd
     out = np.zeros((msgs.shape[0], dim + 1), np.uint64)
     _check(lib().rosetta_lwe_encrypt(seed, C.byref(p), sigma, _np_ptr(key), dim, _np_ptr(msgs),
                                      msgs.shape[0], _np_ptr(out)))
+    return out
+
+
+def lwe_encrypt_plain(seed: int, params, sigma: float, key: np.ndarray, plain) -> np.ndarray:
+    """LWE encryptions of plaintexts already in Z_p (params unused beyond
+    symmetry with lwe_encrypt)."""
+    key = np.ascontiguousarray(key, np.uint64)
+    plain = np.ascontiguousarray(plain, np.uint64)
+    dim = key.shape[0]
+    out = np.zeros((plain.shape[0], dim + 1), np.uint64)
+    _check(lib().rosetta_lwe_encrypt_plain(seed, sigma, _np_ptr(key), dim, _np_ptr(plain),
+                                           plain.shape[0], _np_ptr(out)))
     return out
 
 

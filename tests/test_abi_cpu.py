@@ -125,6 +125,10 @@ def test_encrypt_decrypt_lut_match_oracle(O):
     b = O.lwe_encrypt(op, w.enc_seed, w.sigma_lwe, ks.lwe_key, msgs)
     assert np.array_equal(a, b)
     assert np.array_equal(R.lwe_decrypt(w.params(), ks.lwe_key, a), msgs)
+    plain = np.random.default_rng(3).integers(0, 2 ** 64 - 2 ** 32, 9, dtype=np.uint64)
+    assert np.array_equal(R.lwe_encrypt_plain(w.enc_seed, w.params(), w.sigma_lwe, ks.lwe_key,
+                                              plain),
+                          O.lwe_encrypt_plain(w.enc_seed, w.sigma_lwe, ks.lwe_key, plain))
     assert np.array_equal(R.lwe_decrypt(w.params(), ks.lwe_key, a), O.lwe_decrypt(op, ks.lwe_key, a))
     for fn in ("identity", "square_mod"):
         t = w.table(fn)
