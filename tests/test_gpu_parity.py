@@ -170,3 +170,44 @@ def test_determinism(O, torch_dev):
     a = R.to_host(R.pbs_batch(d_in, bsk, ksk, d_v, w.params()))
     b = R.to_host(R.pbs_batch(d_in, bsk, ksk, d_v, w.params()))
     assert np.array_equal(a, b)
+
+
+# --------------------------------------------------- parameter corners ---
+
+CORNERS = {
+    # l*beta > 30 (64-bit rounded value) and beta > 14 (general first stage)
+    "l2_b16_N1024": dict(n=32, N=1024, pbs_level=2, pbs_base_log=16, ks_level=4,
+                         ks_base_log=4, msg_bits=2),
+    # l*beta = 60, the most key-switching levels
+    "l4_b15_N512": dict(n=16, N=512, pbs_level=4, pbs_base_log=15, ks_level=8, ks_base_log=3,
+                        msg_bits=2),
+    # one level of 30 bits, the smallest LWE dimension
+    "l1_b30_N256_n1": dict(n=1, N=256, pbs_level=1, pbs_base_log=30, ks_level=2,
+                           ks_base_log=10, msg_bits=1),
+    # the largest LWE dimension
+    "n2048_N2048": dict(n=2048, N=2048, pbs_level=3, pbs_base_log=8, ks_level=2, ks_base_log=8,
+                        msg_bits=3),
+    # the largest ring, general first stage, 2 waves per SIMD
+    "l4_b15_N4096": dict(n=24, N=4096, pbs_level=4, pbs_base_log=15, ks_level=3, ks_base_log=6,
+                         msg_bits=3),
+}
+
+
+@pytest.mark.parametrize("name", list(CORNERS))
+def test_parameter_corners_bit_exact(O, torch_dev, name):
+    prm = CORNERS[name]
+    op = O.Params.make(**prm)
+    say(f"[corner {name}] oracle keygen")
+    ks = O.KeySet(op, 17, 2.0 ** -40, 2.0 ** -40)
+    bsk = R.bsk_prepare(R.to_device(ks.bsk), prm | {"k": 1})
+    ksk = R.ksk_prepare(R.to_device(ks.ksk), prm | {"k": 1})
+    rng = np.random.default_rng(len(name))
+    cts = rng.integers(0, P, (3, prm["n"] + 1), dtype=np.uint64)
+    v = rng.integers(0, P, prm["N"], dtype=np.uint64)
+    say(f"[corner {name}] GPU")
+    out = R.to_host(R.pbs_batch(R.to_device(cts), bsk, ksk, R.to_device(v), prm | {"k": 1}))
+    big = R.to_host(R.blind_rotate_extract(R.to_device(cts), bsk, R.to_device(v), prm | {"k": 1}))
+    say(f"[corner {name}] oracle")
+    ref_out, ref_big = O.pbs(op, cts, ks.bsk, ks.ksk, v, O.NTT, 0, want_big=True)
+    assert np.array_equal(big, ref_big)
+    assert np.array_equal(out, ref_out)
