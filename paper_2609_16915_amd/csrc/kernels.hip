@@ -20,12 +20,13 @@ namespace rosetta {
 // ---------------------------------------------------------------------------
 
 // Dynamic LDS of the transform kernels: the twiddle area (TW_WORDS words:
-// zeta[N] then the radix-8 powers), then two N-word transpose buffers.
+// zeta[N] then the radix-8 powers), then the exchange buffers (XCHG_WORDS,
+// see LdsBufs).
 extern __shared__ __align__(16) u64 lds_dyn[];
 
 template <class S>
 constexpr size_t ntt_lds_bytes() {
-  return (size_t)(S::TW_WORDS + 2 * S::N) * sizeof(u64);
+  return (size_t)(S::TW_WORDS + S::XCHG_WORDS) * sizeof(u64);
 }
 
 // Row r of the standard key (N coefficients) -> transform domain, scaled by
@@ -36,7 +37,7 @@ __global__ void __launch_bounds__(S::T)
 k_bsk_prepare(const u64 *__restrict__ std_key, u64 *__restrict__ dev_key,
               const u64 *__restrict__ zeta, u64 ninv) {
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::TW_WORDS, S::N);
+  LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   const int tid = threadIdx.x;
   const size_t row = blockIdx.x;
   load_twiddles<S>(tw, zeta, tid);
@@ -69,7 +70,7 @@ template <class S>
 __global__ void __launch_bounds__(S::T)
 k_ntt_forward(const u64 *in, u64 *out, const u64 *__restrict__ zeta) {
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::TW_WORDS, S::N);
+  LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   const int tid = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * S::N;
   load_twiddles<S>(tw, zeta, tid);
@@ -86,7 +87,7 @@ template <class S>
 __global__ void __launch_bounds__(S::T)
 k_ntt_inverse(const u64 *in, u64 *out, const u64 *__restrict__ zeta, u64 ninv) {
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::TW_WORDS, S::N);
+  LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   const int tid = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * S::N;
   load_twiddles<S>(tw, zeta, tid);
@@ -103,7 +104,7 @@ template <class S>
 __global__ void __launch_bounds__(S::T)
 k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta, u64 ninv) {
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::TW_WORDS, S::N);
+  LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   const int tid = threadIdx.x;
   const size_t base = (size_t)blockIdx.x * S::N;
   load_twiddles<S>(tw, zeta, tid);
@@ -177,7 +178,7 @@ __device__ __forceinline__ RT digit_of(RT r, int beta, int t) {
 // into registers before its forward transform, so their latency overlaps
 // the transform.
 //
-// Dynamic LDS: twiddle area [TW_WORDS], two transpose buffers [N] each,
+// Dynamic LDS: twiddle area [TW_WORDS], exchange buffers [XCHG_WORDS],
 // then the n+1 rounded rotation amounts (u16).
 template <class S>
 size_t br_lds_bytes(int n) {
@@ -202,8 +203,8 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
                int tp_glwe, const u64 *__restrict__ zeta) {
   constexpr int N = S::N, E = S::E, T = S::T;
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::TW_WORDS, N);
-  uint16_t *rot = (uint16_t *)(lds_dyn + S::TW_WORDS + 2 * N);
+  LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
+  uint16_t *rot = (uint16_t *)(lds_dyn + S::TW_WORDS + S::XCHG_WORDS);
   const int tid = threadIdx.x;
   const size_t ct = blockIdx.x;
 
@@ -244,7 +245,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
         u64 cur[E];
 #pragma unroll
         for (int k = 0; k < E; ++k) cur[k] = u ? accB[k] : accA[k];
-        u64 *buf = lds.next();
+        u64 *buf = lds.cross();
 #pragma unroll
         for (int k = 0; k < E; ++k) buf[tid + T * k] = cur[k];
         __syncthreads();
@@ -369,7 +370,7 @@ k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restric
         int beta, const u64 *__restrict__ zeta, u64 ninv) {
   constexpr int N = S::N, E = S::E, T = S::T;
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::TW_WORDS, N);
+  LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   const int tid = threadIdx.x;
   const size_t ct = blockIdx.x;
   load_twiddles<S>(tw, zeta, tid);
@@ -392,7 +393,7 @@ k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restric
     const u32 dinv = odd_inverse_mod((1u << kr) + 1, 2 * N);
     // B <- B + tau_d(B)
     {
-      u64 *buf = lds.next();
+      u64 *buf = lds.cross();
 #pragma unroll
       for (int k = 0; k < E; ++k) buf[tid + T * k] = B[k];
       __syncthreads();
@@ -402,7 +403,7 @@ k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restric
     // rounded tau_d(A), the input of the decomposition
     i64 R[E];
     {
-      u64 *buf = lds.next();
+      u64 *buf = lds.cross();
 #pragma unroll
       for (int k = 0; k < E; ++k) buf[tid + T * k] = A[k];
       __syncthreads();
@@ -469,7 +470,7 @@ k_glwe_mul_plain(const u64 *__restrict__ in, const u64 *__restrict__ pa,
                  const u64 *__restrict__ zeta) {
   constexpr int N = S::N, E = S::E, T = S::T;
   u64 *tw = lds_dyn;
-  LdsPair lds(lds_dyn + S::TW_WORDS, N);
+  LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   const int tid = threadIdx.x;
   const size_t ct = blockIdx.x;
   load_twiddles<S>(tw, zeta, tid);

@@ -84,6 +84,21 @@ struct Ntt {
   static constexpr int TW8_WORDS = tw8_base(PASSES);
   // words of the LDS twiddle area: zeta[N] then the radix-8 powers
   static constexpr int TW_WORDS = N + TW8_WORDS;
+  // In pass q each wave (64 threads) holds one contiguous block of
+  // 2^(6+LE) indices when lo(q) <= 6 (the wave id then sets the top index
+  // bits), or the whole transform when the workgroup is one wave.  An
+  // exchange between two such passes moves data only within each wave.
+  __host__ __device__ static constexpr bool wave_block(int q) { return T <= 64 || lo(q) <= 6; }
+  __host__ __device__ static constexpr bool local_exchange(int qa, int qb) {
+    return wave_block(qa) && wave_block(qb);
+  }
+  // exchange buffers that move data between waves: two (used alternately,
+  // one barrier per exchange) when the LDS allows it, else one (a barrier
+  // before each write as well)
+  static constexpr int NCROSS = (T > 64 && LOGN >= 12) ? 2 : 1;
+  // words after the twiddle area: the cross-wave buffers, then one N-word
+  // buffer in which every wave exchanges within its own block
+  static constexpr int XCHG_WORDS = (NCROSS + 1) * N;
 };
 
 // Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
@@ -339,34 +354,64 @@ __device__ __forceinline__ void ntt_inv_pass(u64 (&x)[S::E], int tid, const u64 
   }
 }
 
-// Move from the layout of pass QW to that of pass QR through one LDS buffer
-// (swizzled word addresses).
-template <class S, int QW, int QR>
-__device__ __forceinline__ void ntt_exchange(u64 (&x)[S::E], u64 *lds, int tid) {
-  const int wb = swz(S::idx(QW, tid, 0));
-#pragma unroll
-  for (int k = 0; k < S::E; ++k) lds[wb ^ swz(k << S::lo(QW))] = x[k];
-  __syncthreads();
-  const int rb = swz(S::idx(QR, tid, 0));
-#pragma unroll
-  for (int k = 0; k < S::E; ++k) x[k] = lds[rb ^ swz(k << S::lo(QR))];
+// Order this wave's LDS accesses (compiler and hardware) without waiting
+// for the other waves of the workgroup.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Two LDS buffers of `words` words each, used alternately.
-struct LdsPair {
+// LDS exchange buffers after the twiddle area (layout in Ntt::XCHG_WORDS).
+// cross(): a buffer for an exchange between waves, free of the previous
+// contents every wave may still read (alternation with one buffer in
+// between, or a barrier).  local(): the buffer of exchanges inside each
+// wave's own block; no other wave touches that block of it.
+template <class S>
+struct LdsBufs {
   u64 *base;
-  int words;
   int par;
-  __device__ __forceinline__ LdsPair(u64 *b, int w) : base(b), words(w), par(0) {}
-  __device__ __forceinline__ u64 *next() {
-    u64 *p = base + par * words;
-    par ^= 1;
-    return p;
+  __device__ __forceinline__ explicit LdsBufs(u64 *b) : base(b), par(0) {}
+  __device__ __forceinline__ u64 *cross() {
+    if constexpr (S::NCROSS == 1) {
+      __syncthreads();
+      return base;
+    } else {
+      u64 *p = base + par * S::N;
+      par ^= 1;
+      return p;
+    }
   }
+  __device__ __forceinline__ u64 *local() { return base + S::NCROSS * S::N; }
 };
 
+// Move from the layout of pass QW to that of pass QR through an LDS buffer
+// (swizzled word addresses); within each wave when both layouts keep the
+// wave's block, else through a cross-wave buffer and a barrier.
+template <class S, int QW, int QR>
+__device__ __forceinline__ void ntt_exchange(u64 (&x)[S::E], LdsBufs<S> &lds, int tid) {
+  const int wb = swz(S::idx(QW, tid, 0));
+  const int rb = swz(S::idx(QR, tid, 0));
+  if constexpr (S::local_exchange(QW, QR)) {
+    u64 *buf = lds.local();
+    wave_sync();
+#pragma unroll
+    for (int k = 0; k < S::E; ++k) buf[wb ^ swz(k << S::lo(QW))] = x[k];
+    wave_sync();
+#pragma unroll
+    for (int k = 0; k < S::E; ++k) x[k] = buf[rb ^ swz(k << S::lo(QR))];
+  } else {
+    u64 *buf = lds.cross();
+#pragma unroll
+    for (int k = 0; k < S::E; ++k) buf[wb ^ swz(k << S::lo(QW))] = x[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < S::E; ++k) x[k] = buf[rb ^ swz(k << S::lo(QR))];
+  }
+}
+
 template <class S, int Q>
-__device__ __forceinline__ void ntt_fwd_from(u64 (&x)[S::E], LdsPair &lds, int tid,
+__device__ __forceinline__ void ntt_fwd_from(u64 (&x)[S::E], LdsBufs<S> &lds, int tid,
                                              const u64 *tw) {
   if constexpr (Q == 0)
     ntt_fwd_pass0<S, 0>(x);
@@ -375,13 +420,13 @@ __device__ __forceinline__ void ntt_fwd_from(u64 (&x)[S::E], LdsPair &lds, int t
   else
     ntt_fwd_pass<S, Q>(x, tid, tw);
   if constexpr (Q + 1 < S::PASSES) {
-    ntt_exchange<S, Q, Q + 1>(x, lds.next(), tid);
+    ntt_exchange<S, Q, Q + 1>(x, lds, tid);
     ntt_fwd_from<S, Q + 1>(x, lds, tid, tw);
   }
 }
 
 template <class S, int Q>
-__device__ __forceinline__ void ntt_inv_from(u64 (&x)[S::E], LdsPair &lds, int tid,
+__device__ __forceinline__ void ntt_inv_from(u64 (&x)[S::E], LdsBufs<S> &lds, int tid,
                                              const u64 *tw) {
   if constexpr (Q == 0)
     ntt_inv_pass0<S>(x);
@@ -390,7 +435,7 @@ __device__ __forceinline__ void ntt_inv_from(u64 (&x)[S::E], LdsPair &lds, int t
   else
     ntt_inv_pass<S, Q>(x, tid, tw);
   if constexpr (Q > 0) {
-    ntt_exchange<S, Q, Q - 1>(x, lds.next(), tid);
+    ntt_exchange<S, Q, Q - 1>(x, lds, tid);
     ntt_inv_from<S, Q - 1>(x, lds, tid, tw);
   }
 }
@@ -398,7 +443,7 @@ __device__ __forceinline__ void ntt_inv_from(u64 (&x)[S::E], LdsPair &lds, int t
 // Natural layout in, in-place (bit-reversed evaluation) layout of the last
 // pass out.
 template <class S>
-__device__ __forceinline__ void ntt_forward(u64 (&x)[S::E], LdsPair &lds, int tid,
+__device__ __forceinline__ void ntt_forward(u64 (&x)[S::E], LdsBufs<S> &lds, int tid,
                                             const u64 *tw) {
   ntt_fwd_from<S, 0>(x, lds, tid, tw);
 }
@@ -407,18 +452,18 @@ __device__ __forceinline__ void ntt_forward(u64 (&x)[S::E], LdsPair &lds, int ti
 // (|d| < 2^14): stage 0 in integer arithmetic, then as ntt_forward.
 template <class S, typename RT>
 __device__ __forceinline__ void ntt_forward_small(const RT (&d)[S::E], u64 (&x)[S::E],
-                                                  LdsPair &lds, int tid, const u64 *tw) {
+                                                  LdsBufs<S> &lds, int tid, const u64 *tw) {
   ntt_fwd_stage0_small<S, RT>(d, x);
   ntt_fwd_pass0<S, 1>(x);
   if constexpr (S::PASSES > 1) {
-    ntt_exchange<S, 0, 1>(x, lds.next(), tid);
+    ntt_exchange<S, 0, 1>(x, lds, tid);
     ntt_fwd_from<S, 1>(x, lds, tid, tw);
   }
 }
 
 // Last-pass layout in, natural layout out, result scaled by N.
 template <class S>
-__device__ __forceinline__ void ntt_inverse(u64 (&x)[S::E], LdsPair &lds, int tid,
+__device__ __forceinline__ void ntt_inverse(u64 (&x)[S::E], LdsBufs<S> &lds, int tid,
                                             const u64 *tw) {
   ntt_inv_from<S, S::PASSES - 1>(x, lds, tid, tw);
 }
