@@ -211,3 +211,35 @@ def test_parameter_corners_bit_exact(O, torch_dev, name):
     ref_out, ref_big = O.pbs(op, cts, ks.bsk, ks.ksk, v, O.NTT, 0, want_big=True)
     assert np.array_equal(big, ref_big)
     assert np.array_equal(out, ref_out)
+
+
+def test_streams(O, torch_dev):
+    """Work is enqueued on the stream given: two batches on two non-default
+    streams, each with its own workspace, run concurrently and each equals
+    the oracle; the default-stream result is the same bits."""
+    torch = torch_dev
+    w, op, ks, bsk, ksk = keyset(O, "gpt2_gelu")
+    v = O.test_poly(op, w.table())
+    d_v = R.to_device(v)
+    batches = []
+    for seed, count in ((21, 300), (22, 517)):
+        cts = O.lwe_encrypt(op, seed, w.sigma_lwe, ks.lwe_key, w.messages(count, seed=seed))
+        batches.append(cts)
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs, ins = [], []
+    for cts, st in zip(batches, streams):
+        d_in = R.to_device(cts)
+        ws = R.empty(R.pbs_workspace_bytes(w.params(), cts.shape[0]) // 8)
+        out = R.empty((cts.shape[0], w.n + 1))
+        torch.cuda.synchronize()
+        R.pbs_batch_ws(d_in, bsk, ksk, d_v, w.params(), ws, out=out, stream=st)
+        outs.append((out, ws))
+        ins.append(d_in)
+    for st in streams:
+        st.synchronize()
+    for (out, _), cts, d_in in zip(outs, batches, ins):
+        got = R.to_host(out)
+        picks = [0, cts.shape[0] // 2, cts.shape[0] - 1]
+        assert np.array_equal(got[picks], O.pbs(op, cts[picks], ks.bsk, ks.ksk, v, O.NTT))
+        assert np.array_equal(got, R.to_host(R.pbs_batch(d_in, bsk, ksk, d_v, w.params())))
