@@ -53,6 +53,24 @@
  * The exact noise bits of a bootstrapped ciphertext are fixed by the
  * conventions above (loop order, CMux form, rounding rules) and are checked
  * only through these component pins and tier agreement.
+ *
+ * Lookup-protocol primitives (end of file; tests/test_oracle_lookup.py):
+ *   automorphism  evaluation at z^d for every root z; group law; ring map;
+ *                 sum over the Galois group = N a_0
+ *   autk keys     noise-free rows have phase tau_d(S) g_t exactly
+ *   GLWE KS       phase kept within N 2^(s-1); mask-free input unchanged
+ *   trace         (0, m) -> (0, m_0) exactly; noise-free within
+ *                 (N-1) N 2^(s-1) of (phase_0, 0, ..)
+ *   blind rot.    of a ciphertext test polynomial: exact for a trivial
+ *                 selector, equal to the PBS accumulator for (0, v), within
+ *                 n (1+N) 2^(s-1) of X^-rot phase(TP) with a noise-free key
+ *   construct     phase(pa * c + pb) = pa * phase(c) + pb exactly;
+ *                 recombination likewise
+ *   example       the paper's running lookup (Sec. 3.2): t, r_0, r_1 and
+ *                 the selected 4.571 to printed precision
+ * What the comparison of Step 1 of Algorithm 1 returns near a boundary is
+ * not fixed by the paper (it cites HE3DB's construction): parity unpinned
+ * there beyond oracle agreement.
  */
 #include <math.h>
 #include <omp.h>

@@ -364,8 +364,16 @@ __device__ __forceinline__ u64 automorphism_coef(const u64 *a, int j, u32 dinv) 
 // Per round: two automorphisms through LDS, L forward transforms of the
 // digit polynomials, 2L multiply-accumulates with the streamed key rows and
 // two inverse transforms; the ciphertext stays in registers throughout.
+#ifndef TRACE_WAVES_PER_EU
+#define TRACE_WAVES_PER_EU 3
+#endif
+template <class S>
+constexpr int trace_waves_per_eu() {
+  return S::LOGN >= 12 ? 2 : TRACE_WAVES_PER_EU;
+}
+
 template <class S, int L>
-__global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(br_waves_per_eu<S>())))
+__global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(trace_waves_per_eu<S>())))
 k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restrict__ out,
         int beta, const u64 *__restrict__ zeta, u64 ninv) {
   constexpr int N = S::N, E = S::E, T = S::T;
