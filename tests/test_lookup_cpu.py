@@ -106,3 +106,34 @@ def test_oracle_pipeline_decrypts_to_the_segmented_lut(O):
         s_phase = int(O.lwe_phase(ks.lwe_key, st["S"][q:q + 1])[0])
         s_phase = s_phase if s_phase <= P // 2 else s_phase - P
         assert round(s_phase / (P / (2 * lp.nseg))) == int(G.segment_index(x, tau))
+
+
+def test_lookup_eval_validation_touches_no_device():
+    """Argument checks of the pipeline entry point run on the host before
+    anything is enqueued."""
+    import ctypes as C
+    L = R.lib()
+    p = R.Params.from_dict(SMALL)
+    lp = lookup_params(256, margin=64)
+    fake = 1 << 40
+    consts = (C.c_uint64 * 4)()
+    ws = L.rosetta_lookup_workspace_bytes(C.byref(p), C.byref(lp), 3)
+    assert ws > 0
+    args = [fake, fake + 10 ** 8, fake + 2 * 10 ** 8, fake + 3 * 10 ** 8, fake + 4 * 10 ** 8,
+            fake + 5 * 10 ** 8, C.addressof(consts), fake + 6 * 10 ** 8, 3, C.byref(p), C.byref(lp),
+            fake + 7 * 10 ** 8, ws, None]
+    # empty batch: no-op
+    a = list(args); a[8] = 0
+    assert L.rosetta_lookup_eval(*a) == 0
+    # NULL input, too small a workspace, output overlapping the workspace
+    a = list(args); a[0] = None
+    assert L.rosetta_lookup_eval(*a) == 1
+    a = list(args); a[12] = ws - 8
+    assert L.rosetta_lookup_eval(*a) == 7
+    a = list(args); a[7] = a[11] + 64
+    assert L.rosetta_lookup_eval(*a) == 4
+    # invalid lookup parameters
+    bad = lookup_params(256, margin=64)
+    bad.nseg = 3
+    a = list(args); a[10] = C.byref(bad)
+    assert L.rosetta_lookup_eval(*a) == 2
