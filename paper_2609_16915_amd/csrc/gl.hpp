@@ -3,8 +3,7 @@
 // 2^64 = 2^32 - 1 (mod p), so a 128-bit value hi*2^64 + lo with
 // hi = h1*2^32 + h0 reduces to lo - h1 + h0*(2^32 - 1)  (since 2^96 = -1).
 // All functions take and return canonical values in [0, p).  The 64x64
-// product is built from the low and high halves of four 32x32 products,
-// which gfx950 issues at full rate (v_mad_u64_u32 runs at half rate).
+// product is built from four 32x32+64-bit multiply-adds.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -50,23 +49,22 @@ __host__ __device__ __forceinline__ u64 gl_sub(u64 a, u64 b) {
 
 __host__ __device__ __forceinline__ u64 gl_neg(u64 a) { return a ? GL_P - a : 0; }
 
-// 128-bit product a*b as 32-bit limbs c0..c3 (c0 least significant): four
-// 32x32 products, low and high halves (v_mul_lo_u32 / v_mul_hi_u32, both
-// full rate on gfx950), summed with carries.
+// 128-bit product a*b as 32-bit limbs c0..c3 (c0 least significant), from
+// four 32x32+64-bit multiply-adds (v_mad_u64_u32, which gfx950 issues at
+// full rate): with p00 = a0 b0, p01 = a0 b1 + hi(p00), p10 = a1 b0 + lo(p01)
+// and p11 = a1 b1 + hi(p01) + hi(p10), a b = lo(p00) + 2^32 lo(p10) +
+// 2^64 p11, and no partial sum exceeds (2^32-1)^2 + 2 (2^32-1) = 2^64 - 1.
 __host__ __device__ __forceinline__ void gl_mul_limbs(u64 a, u64 b, u32 &c0, u32 &c1, u32 &c2,
                                                       u32 &c3) {
   const u32 a0 = (u32)a, a1 = (u32)(a >> 32), b0 = (u32)b, b1 = (u32)(b >> 32);
-  c0 = a0 * b0;
-  const u32 x = (u32)(((u64)a0 * b0) >> 32);
-  const u32 yl = a0 * b1, yh = (u32)(((u64)a0 * b1) >> 32);
-  const u32 zl = a1 * b0, zh = (u32)(((u64)a1 * b0) >> 32);
-  const u32 wl = a1 * b1, wh = (u32)(((u64)a1 * b1) >> 32);
-  u32 k1, k2, k3, k4;
-  c1 = __builtin_addc(x, yl, 0u, &k1);
-  c1 = __builtin_addc(c1, zl, 0u, &k2);
-  c2 = __builtin_addc(yh, zh, k1, &k3);
-  c2 = __builtin_addc(c2, wl, k2, &k4);
-  c3 = wh + k3 + k4;
+  const u64 p00 = (u64)a0 * b0;
+  const u64 p01 = (u64)a0 * b1 + (p00 >> 32);
+  const u64 p10 = (u64)a1 * b0 + (u32)p01;
+  const u64 p11 = (u64)a1 * b1 + ((p01 >> 32) + (p10 >> 32));
+  c0 = (u32)p00;
+  c1 = (u32)p10;
+  c2 = (u32)p11;
+  c3 = (u32)(p11 >> 32);
 }
 
 // c0 + c1 2^32 + c2 2^64 + c3 2^96  mod p
@@ -125,16 +123,16 @@ __host__ __device__ __forceinline__ u64 gl_mul_pow2(u64 x) {
   }
 }
 
-// (a * b + c) mod p with one reduction: the 128-bit product plus a value
-// below p stays below p^2 + p < 2^128.
+// (a * b + c) mod p with one reduction: c enters the multiply-adds of
+// gl_mul_limbs (its low half with a0 b0, its high half with a0 b1), which
+// keeps every partial sum below 2^64; a b + c < p^2 + p < 2^128.
 __host__ __device__ __forceinline__ u64 gl_mul_add(u64 a, u64 b, u64 c) {
-  u32 c0, c1, c2, c3, k;
-  gl_mul_limbs(a, b, c0, c1, c2, c3);
-  c0 = __builtin_addc(c0, (u32)c, 0u, &k);
-  c1 = __builtin_addc(c1, (u32)(c >> 32), k, &k);
-  c2 = __builtin_addc(c2, 0u, k, &k);
-  c3 = c3 + k;
-  return gl_reduce_limbs(c0, c1, c2, c3);
+  const u32 a0 = (u32)a, a1 = (u32)(a >> 32), b0 = (u32)b, b1 = (u32)(b >> 32);
+  const u64 p00 = (u64)a0 * b0 + (u32)c;
+  const u64 p01 = (u64)a0 * b1 + ((p00 >> 32) + (c >> 32));
+  const u64 p10 = (u64)a1 * b0 + (u32)p01;
+  const u64 p11 = (u64)a1 * b1 + ((p01 >> 32) + (p10 >> 32));
+  return gl_reduce_limbs((u32)p00, (u32)p10, (u32)p11, (u32)(p11 >> 32));
 }
 
 __host__ __device__ inline u64 gl_pow(u64 a, u64 e) {
