@@ -27,24 +27,29 @@ __host__ __device__ __forceinline__ u64 gl_mk(u32 lo, u32 hi) { return ((u64)hi 
 //   s - p == s + EPS (mod 2^64), so "wrapped past 2^64" and "s >= p" are
 //   both fixed by adding EPS;  and  d + p == d - EPS (mod 2^64).
 
-// (a + b) mod p for canonical a, b.
+// (a + b) mod p for canonical a, b: s = a + b wraps past 2^64 or reaches p
+// exactly when the result is s + EPS (mod 2^64); the condition selects the
+// 32-bit addend, one 64-bit add applies it.
 __host__ __device__ __forceinline__ u64 gl_add(u64 a, u64 b) {
-  u32 c1, c2;
+  u32 c1;
   const u32 s0 = __builtin_addc((u32)a, (u32)b, 0u, &c1);
   const u32 s1 = __builtin_addc((u32)(a >> 32), (u32)(b >> 32), c1, &c1);
-  const u32 t0 = __builtin_addc(s0, 0xFFFFFFFFu, 0u, &c2);  // s + EPS, carry iff s >= p
-  const u32 t1 = __builtin_addc(s1, 0u, c2, &c2);
-  return (c1 | c2) ? gl_mk(t0, t1) : gl_mk(s0, s1);
+  const u64 s = gl_mk(s0, s1);
+  const u32 adj = (c1 | (s >= GL_P)) ? 0xFFFFFFFFu : 0u;
+  return s + adj;
 }
 
-// (a - b) mod p for canonical a, b.
+// (a - b) mod p for canonical a, b: on a borrow add p, i.e. subtract EPS
+// mod 2^64, spelled as +borrow on the low word and -borrow on the high word
+// with the low word's carry.
 __host__ __device__ __forceinline__ u64 gl_sub(u64 a, u64 b) {
-  u32 b1, b2;
+  u32 b1, k;
   const u32 d0 = __builtin_subc((u32)a, (u32)b, 0u, &b1);
   const u32 d1 = __builtin_subc((u32)(a >> 32), (u32)(b >> 32), b1, &b1);
-  const u32 t0 = __builtin_subc(d0, 0xFFFFFFFFu, 0u, &b2);  // d - EPS = d + p
-  const u32 t1 = __builtin_subc(d1, 0u, b2, &b2);
-  return b1 ? gl_mk(t0, t1) : gl_mk(d0, d1);
+  const u32 r0 = __builtin_addc(d0, 0u, b1, &k);
+  u32 kk;
+  const u32 r1 = __builtin_subc(__builtin_addc(d1, 0u, k, &kk), 0u, b1, &kk);
+  return gl_mk(r0, r1);
 }
 
 __host__ __device__ __forceinline__ u64 gl_neg(u64 a) { return a ? GL_P - a : 0; }
