@@ -74,22 +74,25 @@ __host__ __device__ __forceinline__ void gl_mul_limbs(u64 a, u64 b, u32 &c0, u32
 
 // c0 + c1 2^32 + c2 2^64 + c3 2^96  mod p
 //   = (c1:c0) - c3 + c2 (2^32 - 1)          (2^64 = 2^32 - 1, 2^96 = -1)
+// t = (c1:c0) - c3 (+ p on a borrow, as in gl_sub) is below 2^64, v = c2 EPS
+// is below 2^64 - 2^33 + 2, so t + v wraps past 2^64 at most once and the
+// wrapped sum plus EPS stays below p; as in gl_add, one conditional EPS
+// then canonicalises.
 __host__ __device__ __forceinline__ u64 gl_reduce_limbs(u32 c0, u32 c1, u32 c2, u32 c3) {
-  u32 e1, e2;
-  u32 t0 = __builtin_subc(c0, c3, 0u, &e1);           // t = (c1:c0) - c3
-  u32 t1 = __builtin_subc(c1, 0u, e1, &e1);
-  const u32 adj = e1 ? 0xFFFFFFFFu : 0u;               // borrow: t + p = t - EPS
-  t0 = __builtin_subc(t0, adj, 0u, &e2);
-  t1 = __builtin_subc(t1, 0u, e2, &e2);
+  u32 e1, k, kk;
+  const u32 d0 = __builtin_subc(c0, c3, 0u, &e1);
+  const u32 d1 = __builtin_subc(c1, 0u, e1, &e1);
+  const u32 t0 = __builtin_addc(d0, 0u, e1, &k);
+  const u32 t1 = __builtin_subc(__builtin_addc(d1, 0u, k, &kk), 0u, e1, &kk);
   u32 bb;
-  const u32 v0 = __builtin_subc(0u, c2, 0u, &bb);      // v = c2 * EPS = (c2 << 32) - c2
+  const u32 v0 = __builtin_subc(0u, c2, 0u, &bb);  // v = c2 EPS = (c2 << 32) - c2
   const u32 v1 = c2 - bb;
-  u32 ca, cb;
-  const u32 r0 = __builtin_addc(t0, v0, 0u, &ca);      // r = t + v
+  u32 ca;
+  const u32 r0 = __builtin_addc(t0, v0, 0u, &ca);
   const u32 r1 = __builtin_addc(t1, v1, ca, &ca);
-  const u32 s0 = __builtin_addc(r0, 0xFFFFFFFFu, 0u, &cb);
-  const u32 s1 = __builtin_addc(r1, 0u, cb, &cb);
-  return (ca | cb) ? gl_mk(s0, s1) : gl_mk(r0, r1);
+  const u64 r = gl_mk(r0, r1);
+  const u32 adj = (ca | (r >= GL_P)) ? 0xFFFFFFFFu : 0u;
+  return r + adj;
 }
 
 // (hi*2^64 + lo) mod p for any 128-bit value.
