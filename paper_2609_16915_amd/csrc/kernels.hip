@@ -258,8 +258,12 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
           R[k] = (RT)gl_round_top(d, s);
         }
       }
+      // levels from the least significant (t = L-1) up: each pass takes
+      // the balanced low digit of R and shifts it out, the last level is
+      // what remains (the sums over t are exact, so their order is free)
+      const RT half = (RT)1 << (beta - 1), mask = ((RT)1 << beta) - 1;
 #pragma unroll 1
-      for (int t = 0; t < L; ++t) {
+      for (int t = L - 1; t >= 0; --t) {
         gconst_u64 *g = G + (size_t)((u * L + t) * 2) * N;
         u64 g0[E], g1[E];
         if constexpr (PF) {
@@ -271,15 +275,22 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
         }
         // a3: digit polynomial of level t;  a4: forward transform (its first
         // stage in integer arithmetic while the digits are small)
+        RT d[E];
+#pragma unroll
+        for (int k = 0; k < E; ++k) {
+          if (t == 0) {
+            d[k] = R[k];
+          } else {
+            d[k] = ((R[k] + half) & mask) - half;
+            R[k] = (R[k] - d[k]) >> beta;
+          }
+        }
         u64 x[E];
         if (beta <= 14) {
-          RT d[E];
-#pragma unroll
-          for (int k = 0; k < E; ++k) d[k] = digit_of<L, RT>(R[k], beta, t);
           ntt_forward_small<S, RT>(d, x, lds, tid, tw);
         } else {
 #pragma unroll
-          for (int k = 0; k < E; ++k) x[k] = gl_from_i64((i64)digit_of<L, RT>(R[k], beta, t));
+          for (int k = 0; k < E; ++k) x[k] = gl_from_i64((i64)d[k]);
           ntt_forward<S>(x, lds, tid, tw);
         }
         // a5: multiply-accumulate with the two rows of GGSW_i[u][t]
