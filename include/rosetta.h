@@ -184,6 +184,30 @@ rosetta_status rosetta_ntt_inverse(const uint64_t *in, uint64_t *out, size_t cou
 rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *c, size_t count,
                                 uint32_t N, void *stream);
 
+/* Elementwise Goldilocks arithmetic with the device routines that every
+ * kernel above is built from (Sec. 2.2 works over Z_p; here p = 2^64 -
+ * 2^32 + 1), so that they can be checked on their own, edge values
+ * included.  out[i] = f(a[i], b[i], c[i]) mod p for op:
+ *   ROSETTA_FIELD_ADD      a + b
+ *   ROSETTA_FIELD_SUB      a - b
+ *   ROSETTA_FIELD_MUL      a * b
+ *   ROSETTA_FIELD_MUL_ADD  a * b + c
+ *   ROSETTA_FIELD_MUL_POW2 + e   a * 2^e   (0 <= e < 96; 2^96 = -1 mod p)
+ * a, b, c, out: device [count] u64.  Every input must be canonical (< p);
+ * the result is canonical.  b and c are not read (and may be NULL) when the
+ * op does not use them; out may alias an input exactly.  Errors:
+ * ROSETTA_ERR_PARAMS for an unknown op, ROSETTA_ERR_NULL for a missing
+ * pointer the op reads or writes. */
+enum {
+  ROSETTA_FIELD_ADD = 0,
+  ROSETTA_FIELD_SUB = 1,
+  ROSETTA_FIELD_MUL = 2,
+  ROSETTA_FIELD_MUL_ADD = 3,
+  ROSETTA_FIELD_MUL_POW2 = 256
+};
+rosetta_status rosetta_field_op(int op, const uint64_t *a, const uint64_t *b, const uint64_t *c,
+                                uint64_t *out, size_t count, void *stream);
+
 /* ---- lookup-protocol primitives (Sec. 3.2 "Cryptographic Lookup Protocol",
  * Steps 2-3 and Algorithm 1; Sec. 2.2.3 "RLWE Trace Computation") ---------
  *

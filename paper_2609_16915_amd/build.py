@@ -15,7 +15,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "librosetta.so")
-SOURCES = ["kernels.hip", "abi.cpp", "host_helpers.cpp", "seglut.cpp", "lookup.cpp"]
+SOURCES = ["kernels.hip", "keyswitch.hip", "abi.cpp", "host_helpers.cpp", "seglut.cpp",
+           "lookup.cpp"]
 ARCH = os.environ.get("ROSETTA_OFFLOAD_ARCH", "gfx950")
 
 
@@ -33,6 +34,19 @@ FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",
          f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
+# Device-code scheduling of the transform kernels (kernels.hip): LLVM's
+# iterative ILP scheduler interleaves the independent field products of the
+# transform passes (the default occupancy-first strategy runs them back to
+# back, and their carry chains then leave the VALU idle between dependent
+# instructions); the register budget, and with it the waves per SIMD, stays
+# the same.  keyswitch.hip keeps the default, which suits it better.
+TRANSFORM_FLAGS = ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]
+
+
+def _flags(src: str):
+    return FLAGS + (TRANSFORM_FLAGS if src == "kernels.hip" else [])
+
+
 def _filter(stderr: str) -> str:
     return "\n".join(l for l in (stderr or "").splitlines() if "packed-fp32-ops" not in l)
 
@@ -43,7 +57,7 @@ def build(verbose: bool = False) -> str:
     import tempfile
     with tempfile.TemporaryDirectory(prefix="rosetta_build_") as tmpdir:
         objs = [os.path.join(tmpdir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
-        cmds = [[hipcc(), *FLAGS, "-c", os.path.join(CSRC, s), "-o", o]
+        cmds = [[hipcc(), *_flags(s), "-c", os.path.join(CSRC, s), "-o", o]
                 for s, o in zip(SOURCES, objs)]
         if verbose:
             for c in cmds:

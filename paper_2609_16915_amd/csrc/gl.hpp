@@ -3,7 +3,10 @@
 // 2^64 = 2^32 - 1 (mod p), so a 128-bit value hi*2^64 + lo with
 // hi = h1*2^32 + h0 reduces to lo - h1 + h0*(2^32 - 1)  (since 2^96 = -1).
 // All functions take and return canonical values in [0, p).  The 64x64
-// product is built from four 32x32+64-bit multiply-adds.
+// product is built from four 32x32+64-bit multiply-adds.  On the device the
+// products, the multiply-accumulate and the power-of-two products use the
+// carry-out of v_mad_u64_u32 (see the gfx950 section below); the host
+// compiles the portable forms.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -100,10 +103,185 @@ __host__ __device__ __forceinline__ u64 gl_reduce128(u64 lo, u64 hi) {
   return gl_reduce_limbs((u32)lo, (u32)(lo >> 32), (u32)hi, (u32)(hi >> 32));
 }
 
+#if defined(__HIP_DEVICE_COMPILE__)
+// ---- gfx950 device forms ---------------------------------------------------
+// The compiler does not expose the carry-out of v_mad_u64_u32 (a wave64 lane
+// mask in an SGPR pair), and without it a 64-bit addend must be
+// zero-extended into an aligned register pair (moves) and an overflow
+// recovered by a compare.  The wrappers below are single instructions; the
+// mask logic between them compiles to scalar instructions.
+namespace isa {
+
+// a * b + c and its carry-out (bit 64 per lane)
+__device__ __forceinline__ u64 mad_c(u32 a, u32 b, u64 c, u64 &cy) {
+  u64 r;
+  asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(r), "=s"(cy) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+// a * (2^32 - 1) + c and its carry-out
+__device__ __forceinline__ u64 mad_eps_c(u32 a, u64 c, u64 &cy) {
+  u64 r;
+  asm("v_mad_u64_u32 %0, %1, %2, -1, %3" : "=v"(r), "=s"(cy) : "v"(a), "v"(c));
+  return r;
+}
+// a + b + (carry-in lane bit of ci); carry-out discarded
+__device__ __forceinline__ u32 add_ci(u32 a, u32 b, u64 ci) {
+  u32 r;
+  u64 co;
+  asm("v_addc_co_u32_e64 %0, %1, %2, %3, %4" : "=v"(r), "=s"(co) : "v"(a), "v"(b), "s"(ci));
+  return r;
+}
+// a + b + carry-in, with carry-out
+__device__ __forceinline__ u32 addc_c(u32 a, u32 b, u64 ci, u64 &co) {
+  u32 r;
+  asm("v_addc_co_u32_e64 %0, %1, %2, %3, %4" : "=v"(r), "=s"(co) : "v"(a), "v"(b), "s"(ci));
+  return r;
+}
+// a + b with carry-out
+__device__ __forceinline__ u32 add_c(u32 a, u32 b, u64 &co) {
+  u32 r;
+  asm("v_add_co_u32_e64 %0, %1, %2, %3" : "=v"(r), "=s"(co) : "v"(a), "v"(b));
+  return r;
+}
+// a + carry-in, carry-out discarded
+__device__ __forceinline__ u32 inc_ci(u32 a, u64 ci) {
+  u32 r;
+  u64 co;
+  asm("v_addc_co_u32_e64 %0, %1, %2, 0, %3" : "=v"(r), "=s"(co) : "v"(a), "s"(ci));
+  return r;
+}
+// a - b with borrow-out
+__device__ __forceinline__ u32 sub_c(u32 a, u32 b, u64 &bo) {
+  u32 r;
+  asm("v_sub_co_u32_e64 %0, %1, %2, %3" : "=v"(r), "=s"(bo) : "v"(a), "v"(b));
+  return r;
+}
+// a - borrow-in with borrow-out
+__device__ __forceinline__ u32 dec_bc(u32 a, u64 bi, u64 &bo) {
+  u32 r;
+  asm("v_subb_co_u32_e64 %0, %1, %2, 0, %3" : "=v"(r), "=s"(bo) : "v"(a), "s"(bi));
+  return r;
+}
+// lanes with r >= p
+__device__ __forceinline__ u64 ge_p(u64 r) {
+  u64 m;
+  asm("v_cmp_lt_u64_e64 %0, %1, %2" : "=s"(m) : "s"(GL_P - 1), "v"(r));
+  return m;
+}
+// m ? 2^32 - 1 : 0
+__device__ __forceinline__ u32 sel_eps(u64 m) {
+  u32 e;
+  asm("v_cndmask_b32_e64 %0, 0, -1, %1" : "=v"(e) : "s"(m));
+  return e;
+}
+// r + (m ? 2^32 - 1 : 0), i.e. r - p (mod 2^64) on the lanes of m
+__device__ __forceinline__ u64 add_eps_if(u64 r, u64 m) { return r + (u64)sel_eps(m); }
+
+}  // namespace isa
+
+// (c1:c0) + c2 (2^32 - 1) - c3 mod p, canonical.  t = (c1:c0) - c3, minus
+// EPS (plus p mod 2^64) on a borrow, which leaves t in [p - 2^32, p); then
+// R = c2 EPS + t with its carry: a carry leaves R + EPS below p (R is below
+// 2^64 - 2^33 + 1 after the wrap), no carry leaves R in [0, 2^64), so one
+// conditional EPS covers "carry or R >= p".
+__device__ __forceinline__ u64 gl_reduce_dev(u32 c0, u32 c1, u32 c2, u32 c3) {
+  u64 b0, b1, b2, b3;
+  const u32 d0 = isa::sub_c(c0, c3, b0);
+  const u32 d1 = isa::dec_bc(c1, b0, b1);
+  const u32 e = isa::sel_eps(b1);
+  const u32 t0 = isa::sub_c(d0, e, b2);
+  const u32 t1 = isa::dec_bc(d1, b2, b3);
+  u64 ca;
+  const u64 R = isa::mad_eps_c(c2, gl_mk(t0, t1), ca);
+  return isa::add_eps_if(R, ca | isa::ge_p(R));
+}
+
+// a b as limbs: M = a1 b0, S = a0 b1 + M (65 bits: carry cs),
+// P0 = a0 b0, P1 = a1 b1;  a b = P0 + 2^32 S + 2^64 P1, so
+// c1 = hi(P0) + lo(S), c2 = lo(P1) + hi(S) + carry, c3 = hi(P1) + carries.
+// c3 never overflows (a b < 2^128).
+__device__ __forceinline__ u64 gl_mul_dev(u64 a, u64 b) {
+  const u32 a0 = (u32)a, a1 = (u32)(a >> 32), b0 = (u32)b, b1 = (u32)(b >> 32);
+  u64 cs;
+  const u64 S = isa::mad_c(a0, b1, (u64)a1 * b0, cs);
+  const u64 P0 = (u64)a0 * b0;
+  const u64 P1 = (u64)a1 * b1;
+  u64 kc, kd;
+  const u32 c1 = isa::add_c((u32)(P0 >> 32), (u32)S, kc);
+  const u32 c2 = isa::addc_c((u32)P1, (u32)(S >> 32), kc, kd);
+  const u32 c3 = isa::inc_ci(isa::inc_ci((u32)(P1 >> 32), kd), cs);
+  return gl_reduce_dev((u32)P0, c1, c2, c3);
+}
+
+// a b + c: c enters the multiply-add of P0 (carry cc at weight 2^64, added
+// to c2 with its own carry into c3).
+__device__ __forceinline__ u64 gl_mul_add_dev(u64 a, u64 b, u64 c) {
+  const u32 a0 = (u32)a, a1 = (u32)(a >> 32), b0 = (u32)b, b1 = (u32)(b >> 32);
+  u64 cs, cc;
+  const u64 S = isa::mad_c(a0, b1, (u64)a1 * b0, cs);
+  const u64 P0 = isa::mad_c(a0, b0, c, cc);
+  const u64 P1 = (u64)a1 * b1;
+  u64 kc, kd, ke;
+  const u32 c1 = isa::add_c((u32)(P0 >> 32), (u32)S, kc);
+  const u32 c2a = isa::addc_c((u32)P1, (u32)(S >> 32), kc, kd);
+  const u32 c2 = isa::addc_c(c2a, 0u, cc, ke);
+  const u32 c3 = isa::inc_ci(isa::inc_ci(isa::inc_ci((u32)(P1 >> 32), kd), cs), ke);
+  return gl_reduce_dev((u32)P0, c1, c2, c3);
+}
+
+// x 2^E for 0 < E <= 32 as lo64 + c2 2^64 = lo64 + c2 EPS, c2 < 2^E; with
+// CANON false the result is only reduced below 2^64 (a wrap adds EPS, which
+// cannot wrap again since the wrapped sum is below 2^(32+E) <= 2^64 - EPS
+// for E < 32).
+template <int E, bool CANON>
+__device__ __forceinline__ u64 gl_shl_small_dev(u64 x) {
+  static_assert(E > 0 && E <= 32, "shift out of range");
+  const u32 c2 = (E == 32) ? (u32)(x >> 32) : (u32)(x >> (64 - E));
+  u64 ca;
+  const u64 R = isa::mad_eps_c(c2, x << E, ca);
+  if constexpr (CANON)
+    return isa::add_eps_if(R, ca | isa::ge_p(R));
+  else
+    return isa::add_eps_if(R, ca);
+}
+
+template <int E>
+__device__ __forceinline__ u64 gl_mul_pow2_dev(u64 x) {
+  static_assert(E >= 0 && E < 96, "exponent out of range");
+  if constexpr (E == 0) {
+    return x;
+  } else if constexpr (E <= 32) {
+    return gl_shl_small_dev<E, true>(x);
+  } else if constexpr (E < 64) {
+    // x 2^(E-32) below 2^64, then times 2^32 (whose product step accepts
+    // any 64-bit input: c2 = hi word, a wrap leaves the sum below p - EPS)
+    return gl_shl_small_dev<32, true>(gl_shl_small_dev<E - 32, false>(x));
+  } else {
+    // limbs c2 = lo(x) << f at 2^64 and h = x >> (32 - f) at 2^96 (the part
+    // above 2^128 = -2^32 included): x 2^E = c2 EPS - h, with c2 EPS < p
+    // and h < 2^63, so one conditional p after the subtraction is canonical
+    constexpr int f = E - 64;
+    const u32 c2 = (u32)x << f;
+    const u64 h = f ? (x >> (32 - f)) : (x >> 32);
+    const u64 R = (u64)c2 * 0xFFFFFFFFull;
+    u32 b1, k, kk;
+    const u32 d0 = __builtin_subc((u32)R, (u32)h, 0u, &b1);
+    const u32 d1 = __builtin_subc((u32)(R >> 32), (u32)(h >> 32), b1, &b1);
+    const u32 r0 = __builtin_addc(d0, 0u, b1, &k);
+    const u32 r1 = __builtin_subc(__builtin_addc(d1, 0u, k, &kk), 0u, b1, &kk);
+    return gl_mk(r0, r1);
+  }
+}
+#endif  // __HIP_DEVICE_COMPILE__
+
 __host__ __device__ __forceinline__ u64 gl_mul(u64 a, u64 b) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return gl_mul_dev(a, b);
+#else
   u32 c0, c1, c2, c3;
   gl_mul_limbs(a, b, c0, c1, c2, c3);
   return gl_reduce_limbs(c0, c1, c2, c3);
+#endif
 }
 
 // x * 2^E mod p for a compile-time 0 <= E < 96 (2^96 = -1 covers the rest):
@@ -111,6 +289,9 @@ __host__ __device__ __forceinline__ u64 gl_mul(u64 a, u64 b) {
 template <int E>
 __host__ __device__ __forceinline__ u64 gl_mul_pow2(u64 x) {
   static_assert(E >= 0 && E < 96, "exponent out of range");
+#if defined(__HIP_DEVICE_COMPILE__)
+  return gl_mul_pow2_dev<E>(x);
+#endif
   const u32 x0 = (u32)x, x1 = (u32)(x >> 32);
   if constexpr (E == 0) {
     return x;
@@ -135,6 +316,9 @@ __host__ __device__ __forceinline__ u64 gl_mul_pow2(u64 x) {
 // gl_mul_limbs (its low half with a0 b0, its high half with a0 b1), which
 // keeps every partial sum below 2^64; a b + c < p^2 + p < 2^128.
 __host__ __device__ __forceinline__ u64 gl_mul_add(u64 a, u64 b, u64 c) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return gl_mul_add_dev(a, b, c);
+#endif
   const u32 a0 = (u32)a, a1 = (u32)(a >> 32), b0 = (u32)b, b1 = (u32)(b >> 32);
   const u64 p00 = (u64)a0 * b0 + (u32)c;
   const u64 p01 = (u64)a0 * b1 + ((p00 >> 32) + (c >> 32));

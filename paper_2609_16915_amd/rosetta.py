@@ -73,6 +73,7 @@ SIGNATURES = {
     "rosetta_ntt_forward": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
     "rosetta_ntt_inverse": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
     "rosetta_poly_mul": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
+    "rosetta_field_op": (_ST, [C.c_int, _u64p, _u64p, _u64p, _u64p, C.c_size_t, C.c_void_p]),
     "rosetta_keygen": (_ST, [C.c_uint64, _pp, C.c_double, C.c_double, _u64p, _u64p, _u64p,
                              _u64p]),
     "rosetta_lwe_encrypt": (_ST, [C.c_uint64, _pp, C.c_double, _u64p, C.c_uint32, _u64p,
@@ -321,6 +322,20 @@ def poly_mul(a, b, N: int, out=None, stream=None):
     count = a.numel() // N
     out = empty(a.shape, a.device) if out is None else out
     _check(lib().rosetta_poly_mul(_dev(a, "a"), _dev(b, "b"), _dev(out, "c"), count, N,
+                                  _stream(stream)))
+    return out
+
+
+FIELD_ADD, FIELD_SUB, FIELD_MUL, FIELD_MUL_ADD, FIELD_MUL_POW2 = 0, 1, 2, 3, 256
+
+
+def field_op(op: int, a, b=None, c=None, out=None, stream=None):
+    """Elementwise Goldilocks arithmetic with the kernels' device routines
+    (op: FIELD_ADD, FIELD_SUB, FIELD_MUL, FIELD_MUL_ADD, FIELD_MUL_POW2 + e)."""
+    count = a.numel()
+    out = empty(a.shape, a.device) if out is None else out
+    _check(lib().rosetta_field_op(op, _dev(a, "a"), None if b is None else _dev(b, "b"),
+                                  None if c is None else _dev(c, "c"), _dev(out, "out"), count,
                                   _stream(stream)))
     return out
 

@@ -77,6 +77,14 @@ def test_null_and_empty_batches_touch_no_device(L):
     assert L.rosetta_ntt_forward(None, fake, 2, 256, None) == 1
     assert L.rosetta_ntt_forward(fake, fake, 2, 100, None) == 3
     assert L.rosetta_check_params(None) == 1
+    # field ops: unknown op, missing operands, empty
+    assert L.rosetta_field_op(4, fake, fake, fake, fake, 2, None) == 2
+    assert L.rosetta_field_op(256 + 96, fake, None, None, fake, 2, None) == 2
+    assert L.rosetta_field_op(-1, fake, fake, fake, fake, 2, None) == 2
+    assert L.rosetta_field_op(2, fake, None, None, fake, 2, None) == 1
+    assert L.rosetta_field_op(3, fake, fake, None, fake, 2, None) == 1
+    assert L.rosetta_field_op(256 + 48, None, None, None, fake, 2, None) == 1
+    assert L.rosetta_field_op(2, None, None, None, None, 0, None) == 0
 
 
 def test_alias_and_size_detection(L):

@@ -1,0 +1,93 @@
+"""GPU: the device field routines every kernel is built from, against exact
+integer arithmetic mod p = 2^64 - 2^32 + 1 (Python integers), on edge values
+(0, 1, p - 1, the limb boundaries 2^32 - 1, 2^32, 2^63 and their
+neighbours, values whose shifted limbs vanish) crossed with each other, and on
+seeded random values.  Bit-exact."""
+import itertools
+
+import numpy as np
+import pytest
+
+from gpu_helpers import require_gpu, say
+from paper_2609_16915_amd import rosetta as R
+
+pytestmark = pytest.mark.gpu
+P = 0xFFFFFFFF00000001
+
+
+def edge_values():
+    v = {0, 1, 2, 3, P - 1, P - 2, P - 3, (P - 1) // 2, (P + 1) // 2}
+    for b in (16, 31, 32, 33, 48, 63):
+        for d in (-2, -1, 0, 1, 2):
+            x = (1 << b) + d
+            if 0 <= x < P:
+                v.add(x)
+    for x in (0xFFFFFFFF, 0xFFFFFFFF00000000, 0xFFFFFFFEFFFFFFFF, 0xFFFFFFFF00000000 - 1,
+              0x8000000000000000, 0x8000000080000000, 0x00000000FFFF0000, 0xFFFF0000FFFF0000,
+              0x0000FFFF0000FFFF, 0x7FFFFFFF80000000):
+        if x < P:
+            v.add(x)
+    # x with x * 2^e landing on the 2^96 or 2^128 limb only, for the shifts
+    for e in (12, 24, 36, 48, 60, 72, 84):
+        for s in (96 - e, 128 - e, 64 - e):
+            if 0 <= s < 64:
+                v.add(1 << s)
+                v.add(((1 << s) * 3) % P)
+    return sorted(v)
+
+
+def pairs():
+    ev = edge_values()
+    rng = np.random.default_rng(7)
+    rnd = [int(x) for x in rng.integers(0, P, size=4000, dtype=np.uint64)]
+    a = [x for x, _ in itertools.product(ev, ev)] + rnd
+    b = [y for _, y in itertools.product(ev, ev)] + rnd[::-1]
+    c = [int(x) for x in rng.integers(0, P, size=len(a), dtype=np.uint64)]
+    c[: len(ev)] = ev
+    c[len(ev): 2 * len(ev)] = [P - 1] * len(ev)
+    return a, b, c
+
+
+@pytest.fixture(scope="module")
+def operands():
+    require_gpu()
+    a, b, c = pairs()
+    to = lambda xs: R.to_device(np.array(xs, dtype=np.uint64))
+    return a, b, c, to(a), to(b), to(c)
+
+
+@pytest.mark.parametrize("op,name,ref", [
+    (R.FIELD_ADD, "add", lambda a, b, c: (a + b) % P),
+    (R.FIELD_SUB, "sub", lambda a, b, c: (a - b) % P),
+    (R.FIELD_MUL, "mul", lambda a, b, c: a * b % P),
+    (R.FIELD_MUL_ADD, "mul_add", lambda a, b, c: (a * b + c) % P),
+])
+def test_field_binary_ops_exact(operands, op, name, ref):
+    a, b, c, da, db, dc = operands
+    say(f"[field] {name} on {len(a)} operand pairs")
+    got = R.to_host(R.field_op(op, da, db, dc))
+    want = np.array([ref(x, y, z) for x, y, z in zip(a, b, c)], dtype=np.uint64)
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, [(hex(a[i]), hex(b[i]), hex(int(got[i])), hex(int(want[i])))
+                           for i in bad[:5]]
+
+
+def test_field_pow2_every_exponent(operands):
+    a, _, _, da, _, _ = operands
+    say(f"[field] mul_pow2 e = 0..95 on {len(a)} values")
+    for e in range(96):
+        got = R.to_host(R.field_op(R.FIELD_MUL_POW2 + e, da))
+        t = pow(2, e, P)
+        want = np.array([x * t % P for x in a], dtype=np.uint64)
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, (e, [(hex(a[i]), hex(int(got[i])), hex(int(want[i])))
+                                   for i in bad[:5]])
+
+
+def test_field_ops_in_place(operands):
+    a, b, _, _, _, _ = operands
+    x = R.to_device(np.array(a, dtype=np.uint64))
+    y = R.to_device(np.array(b, dtype=np.uint64))
+    R.field_op(R.FIELD_MUL, x, y, out=x)
+    want = np.array([u * v % P for u, v in zip(a, b)], dtype=np.uint64)
+    assert np.array_equal(R.to_host(x), want)
