@@ -29,17 +29,17 @@ sys.path.insert(0, ROOT)
 
 # MI355X peaks.  The VALU issues 64 lanes of a full-rate 32-bit instruction
 # per clock per CU (4 SIMDs x 16 lanes): 256 CUs x 64 x 2.4 GHz = 39.3e12
-# lane-ops/s.  The library's Goldilocks multiplication (gl_mul) is 18
-# full-rate VALU instructions on gfx950: 4 v_mad_u64_u32, one 64-bit add and
-# 13 add/sub-with-carry, compare and select instructions for the reduction
-# (register moves that form 64-bit addends are not counted: a chain
-# microbenchmark of gl_mul runs at the rate this count implies).  That bounds
-# its rate at 39.3e12 / 18 = 2.18e12 modmul/s; the 4 multiply-adds alone
-# bound any 64x64-bit modular product built this way at 39.3e12 / 4 =
-# 9.8e12 modmul/s.
+# lane-ops/s.  The library's Goldilocks multiplication on the device is 17
+# full-rate VALU instructions on gfx950: the 128-bit product from 4
+# v_mad_u64_u32 and 4 add-with-carry, the reduction from 2 subtractions with
+# borrow, a conditional p (select + 2), one v_mad_u64_u32 folding the 2^64
+# limb with its carry-out, a compare, a select and a 64-bit add.  That
+# bounds its rate at 39.3e12 / 17 = 2.31e12 modmul/s; the 4 product
+# multiply-adds alone bound any 64x64-bit modular product built this way at
+# 39.3e12 / 4 = 9.8e12 modmul/s.
 HBM_PEAK_GBS = 8000.0
 CU, CLOCK_HZ, LANES = 256, 2.4e9, 64
-MODMUL_VALU_OPS = 18
+MODMUL_VALU_OPS = 17
 MODMUL_PEAK_T = CU * CLOCK_HZ * LANES / MODMUL_VALU_OPS / 1e12   # Tmodmul/s
 MULTIPLIER_BOUND_T = CU * CLOCK_HZ * LANES / 4 / 1e12
 PMC_PROFILE = os.path.join(ROOT, "profiles", "k_blind_rotate_llama3_8b_silu_pmc.md")

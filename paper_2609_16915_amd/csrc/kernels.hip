@@ -631,9 +631,14 @@ hipError_t launch_bsk_prepare(const uint64_t *bsk_std, uint64_t *bsk_dev,
   return hipGetLastError();
 }
 
-#ifndef BR_PREFETCH
-#define BR_PREFETCH 0
-#endif
+// Key rows loaded before each digit transform (PF): at N = 4096 the kernel
+// runs two waves per SIMD with registers to spare, and the early loads hide
+// their latency behind the transform (about 2 % there); at N <= 2048 the
+// extra 32 registers per thread cost more in spills than they save.
+template <class S>
+constexpr bool br_prefetch() {
+  return S::LOGN >= 12;
+}
 
 template <class S, int L>
 static hipError_t launch_br_levels(const uint64_t *lwe_in, const uint64_t *bsk_dev,
@@ -643,10 +648,10 @@ static hipError_t launch_br_levels(const uint64_t *lwe_in, const uint64_t *bsk_d
   const int n = (int)p.n, beta = (int)p.pbs_base_log;
   const size_t lds = br_lds_bytes<S>(n);
   if (L * beta <= 30)
-    ROSETTA_LAUNCH((k_blind_rotate<S, L, int32_t, BR_PREFETCH>), dim3(batch), dim3(S::T), lds,
+    ROSETTA_LAUNCH((k_blind_rotate<S, L, int32_t, br_prefetch<S>()>), dim3(batch), dim3(S::T), lds,
                    st, lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);
   else
-    ROSETTA_LAUNCH((k_blind_rotate<S, L, int64_t, BR_PREFETCH>), dim3(batch), dim3(S::T), lds,
+    ROSETTA_LAUNCH((k_blind_rotate<S, L, int64_t, br_prefetch<S>()>), dim3(batch), dim3(S::T), lds,
                    st, lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);
   return hipSuccess;
 }
