@@ -118,17 +118,18 @@ __device__ __forceinline__ u64 mad_c(u32 a, u32 b, u64 c, u64 &cy) {
   asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(r), "=s"(cy) : "v"(a), "v"(b), "v"(c));
   return r;
 }
+// a * b + c with signed 32-bit a, b and signed 64-bit c (exact when the
+// result fits in 64 bits)
+__device__ __forceinline__ int64_t mad_i64(int32_t a, int32_t b, int64_t c) {
+  int64_t r;
+  u64 cy;
+  asm("v_mad_i64_i32 %0, %1, %2, %3, %4" : "=v"(r), "=s"(cy) : "v"(a), "s"(b), "v"(c));
+  return r;
+}
 // a * (2^32 - 1) + c and its carry-out
 __device__ __forceinline__ u64 mad_eps_c(u32 a, u64 c, u64 &cy) {
   u64 r;
   asm("v_mad_u64_u32 %0, %1, %2, -1, %3" : "=v"(r), "=s"(cy) : "v"(a), "v"(c));
-  return r;
-}
-// a + b + (carry-in lane bit of ci); carry-out discarded
-__device__ __forceinline__ u32 add_ci(u32 a, u32 b, u64 ci) {
-  u32 r;
-  u64 co;
-  asm("v_addc_co_u32_e64 %0, %1, %2, %3, %4" : "=v"(r), "=s"(co) : "v"(a), "v"(b), "s"(ci));
   return r;
 }
 // a + b + carry-in, with carry-out

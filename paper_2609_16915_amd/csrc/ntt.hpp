@@ -182,20 +182,100 @@ __device__ __forceinline__ void ntt_inv_pass0(u64 (&x)[S::E]) {
   });
 }
 
-// Stage 0 of the forward transform on small signed inputs (|d| < 2^14),
-// in exact 64-bit integer arithmetic: zeta[1] = 2^48, so
-// d_k +- 2^48 d_k2 fits in 63 bits and needs only a sign fix.
-template <class S, typename RT>
-__device__ __forceinline__ void ntt_fwd_stage0_small(const RT (&d)[S::E], u64 (&x)[S::E]) {
-  static_assert(zeta_log2(1) == 48, "zeta[1] must be 2^48");
-  constexpr int half = S::E / 2;
-#pragma unroll
-  for (int k = 0; k < half; ++k) {
-    const i64 lo = (i64)d[k];
-    const i64 hi = (i64)d[k + half] * ((i64)1 << 48);
-    x[k] = gl_from_i64(lo + hi);
-    x[k + half] = gl_from_i64(lo - hi);
+// Stages 0 and 1 of the forward transform on small signed inputs
+// (|d| <= 2^13), in exact integer arithmetic.  Their twiddles are 16th roots
+// that are signed powers of two: zeta[1] = 2^48, zeta[2] = -2^24 and
+// zeta[3] = -2^72.  After the two stages every element is a signed sum of
+// four inputs, one at each weight 2^0, 2^24, 2^48, 2^72 (a pure sign and
+// index bookkeeping, computed at compile time by first_terms), and with
+// 2^72 = 2^40 - 2^8 (mod p) its value is
+//   L + 2^32 H,  L = s0 a + s24 2^24 b - s72 2^8 d,  H = s48 2^16 c + s72 2^8 d,
+// an exact integer of magnitude below 2^62; one sign fix makes it a field
+// element.
+struct FirstTerm {
+  int idx, sgn;  // input index and sign of the term at one weight
+};
+struct FirstElem {
+  FirstTerm w[4];  // weights 2^0, 2^24, 2^48, 2^72
+};
+template <int E>
+struct FirstTerms {
+  FirstElem el[E];
+};
+
+template <class S>
+constexpr FirstTerms<S::E> first_terms() {
+  static_assert(S::stage_end(0) >= 2, "the first pass must span two stages");
+  constexpr int E = S::E, lo = S::lo(0);
+  // terms as (input, weight exponent in units of 24 bits, sign)
+  int idx[E][4] = {}, ex[E][4] = {}, sg[E][4] = {}, n[E] = {};
+  for (int k = 0; k < E; ++k) {
+    idx[k][0] = k;
+    ex[k][0] = 0;
+    sg[k][0] = 1;
+    n[k] = 1;
   }
+  for (int s = 0; s < 2; ++s) {
+    const int sh = S::LOGN - s, b = sh - 1 - lo;
+    for (int k = 0; k < E; ++k) {
+      if (k & (1 << b)) continue;
+      const int k2 = k | (1 << b);
+      const int m = (1 << s) + (k >> (sh - lo));
+      const int em = zeta_log2(m) / 24;  // zeta[m] = 2^(24 em), em < 8
+      const int nu = n[k], nv = n[k2];
+      int ti[4], te[4], ts[4];
+      for (int i = 0; i < nv; ++i) {  // t = zeta[m] x[k2]; 2^96 = -1
+        int e = ex[k2][i] + em, g = sg[k2][i];
+        if (e >= 8) e -= 8;
+        if (e >= 4) {
+          e -= 4;
+          g = -g;
+        }
+        ti[i] = idx[k2][i];
+        te[i] = e;
+        ts[i] = g;
+      }
+      for (int i = 0; i < nv; ++i) {  // x[k2] = x[k] - t, x[k] = x[k] + t
+        idx[k2][i] = idx[k][i];
+        ex[k2][i] = ex[k][i];
+        sg[k2][i] = sg[k][i];
+      }
+      for (int i = 0; i < nv; ++i) {
+        idx[k][nu + i] = ti[i];
+        ex[k][nu + i] = te[i];
+        sg[k][nu + i] = ts[i];
+        idx[k2][nu + i] = ti[i];
+        ex[k2][nu + i] = te[i];
+        sg[k2][nu + i] = -ts[i];
+      }
+      n[k] = n[k2] = nu + nv;
+    }
+  }
+  FirstTerms<E> r{};
+  for (int k = 0; k < E; ++k)
+    for (int i = 0; i < 4; ++i) r.el[k].w[ex[k][i]] = FirstTerm{idx[k][i], sg[k][i]};
+  return r;
+}
+
+template <class S, typename RT>
+__device__ __forceinline__ void ntt_fwd_stages01_small(const RT (&d)[S::E], u64 (&x)[S::E]) {
+  constexpr FirstTerms<S::E> T = first_terms<S>();
+  static_for<0, S::E>([&](auto kc) {
+    constexpr FirstElem f = T.el[decltype(kc)::value];
+    const int32_t a = (int32_t)d[f.w[0].idx], b = (int32_t)d[f.w[1].idx];
+    const int32_t c = (int32_t)d[f.w[2].idx], e = (int32_t)d[f.w[3].idx];
+    const int32_t t = f.w[0].sgn * a - f.w[3].sgn * (e * 256);
+#if defined(__HIP_DEVICE_COMPILE__)
+    const int64_t L = isa::mad_i64(b, f.w[1].sgn * (1 << 24), (int64_t)t);
+#else
+    const int64_t L = (int64_t)b * (f.w[1].sgn * (1 << 24)) + t;
+#endif
+    const int32_t H = f.w[2].sgn * (c * 65536) + f.w[3].sgn * (e * 256);
+    const uint64_t X = (uint64_t)L + ((uint64_t)(uint32_t)H << 32);
+    // negative X: add p, i.e. subtract 2^32 - 1 modulo 2^64
+    const uint32_t neg = (uint32_t)((int32_t)(X >> 32) >> 31);
+    x[decltype(kc)::value] = X - (uint64_t)neg;
+  });
 }
 
 // Twisted radix-8 form of a three-stage pass (Q >= 1).  The thread's eight
@@ -449,12 +529,12 @@ __device__ __forceinline__ void ntt_forward(u64 (&x)[S::E], LdsBufs<S> &lds, int
 }
 
 // Forward transform of a polynomial with small signed coefficients d
-// (|d| < 2^14): stage 0 in integer arithmetic, then as ntt_forward.
+// (|d| <= 2^13): stages 0 and 1 in integer arithmetic, then as ntt_forward.
 template <class S, typename RT>
 __device__ __forceinline__ void ntt_forward_small(const RT (&d)[S::E], u64 (&x)[S::E],
                                                   LdsBufs<S> &lds, int tid, const u64 *tw) {
-  ntt_fwd_stage0_small<S, RT>(d, x);
-  ntt_fwd_pass0<S, 1>(x);
+  ntt_fwd_stages01_small<S, RT>(d, x);
+  ntt_fwd_pass0<S, 2>(x);
   if constexpr (S::PASSES > 1) {
     ntt_exchange<S, 0, 1>(x, lds, tid);
     ntt_fwd_from<S, 1>(x, lds, tid, tw);
