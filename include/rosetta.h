@@ -208,6 +208,17 @@ enum {
 rosetta_status rosetta_field_op(int op, const uint64_t *a, const uint64_t *b, const uint64_t *c,
                                 uint64_t *out, size_t count, void *stream);
 
+/* Throughput probe of the device modular multiplication (the roofline
+ * reference for the transform kernels): `threads` threads (256 per
+ * workgroup) each run 8 independent chains x <- x * w mod p for `iters`
+ * steps in registers, with x_j = (seed + 8 t + j + 1) mod p and
+ * w = (seed ^ (t * 0x9E3779B97F4A7C15)) mod p, or 3 where that is below 2;
+ * out[t] (device, [threads] u64) receives the XOR of the eight final values,
+ * x_j w^iters mod p, so that the work is checkable.  Errors: ROSETTA_ERR_NULL
+ * for a NULL out with threads > 0. */
+rosetta_status rosetta_modmul_chain(uint64_t seed, uint32_t threads, uint32_t iters,
+                                    uint64_t *out, void *stream);
+
 /* ---- lookup-protocol primitives (Sec. 3.2 "Cryptographic Lookup Protocol",
  * Steps 2-3 and Algorithm 1; Sec. 2.2.3 "RLWE Trace Computation") ---------
  *

@@ -422,6 +422,14 @@ rosetta_status rosetta_field_op(int op, const uint64_t *a, const uint64_t *b, co
   return e == hipSuccess ? ok() : hip_fail(e, "field_op launch");
 }
 
+rosetta_status rosetta_modmul_chain(uint64_t seed, uint32_t threads, uint32_t iters,
+                                    uint64_t *out, void *stream) {
+  if (threads == 0) return ok();
+  if (!out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  hipError_t e = launch_modmul_chain(seed, threads, iters, out, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "modmul_chain launch");
+}
+
 // ---- lookup-protocol primitives -----------------------------------------
 
 rosetta_status rosetta_blind_rotate_glwe(const uint64_t *lwe_in, const uint64_t *bsk_dev,

@@ -69,6 +69,8 @@ hipError_t launch_lwe_sum_groups(const uint64_t *in, uint64_t *out, size_t batch
 // op as in rosetta_field_op (validated by the caller)
 hipError_t launch_field_op(int op, const uint64_t *a, const uint64_t *b, const uint64_t *c,
                            uint64_t *out, size_t count, hipStream_t st);
+hipError_t launch_modmul_chain(uint64_t seed, uint32_t threads, uint32_t iters, uint64_t *out,
+                               hipStream_t st);
 hipError_t launch_keyswitch(const uint64_t *big, const uint64_t *ksk_dev, uint64_t *out,
                             size_t batch, const rosetta_params &p, hipStream_t st);
 hipError_t launch_ntt(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,

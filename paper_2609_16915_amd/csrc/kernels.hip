@@ -829,4 +829,31 @@ hipError_t launch_field_op(int op, const uint64_t *a, const uint64_t *b, const u
   return hipGetLastError();
 }
 
+// Eight independent product chains per thread, all in registers.
+__global__ void __launch_bounds__(256)
+k_modmul_chain(u64 seed, uint32_t threads, uint32_t iters, u64 *__restrict__ out) {
+  const uint32_t t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= threads) return;
+  u64 w = (seed ^ ((u64)t * 0x9E3779B97F4A7C15ull)) % GL_P;
+  if (w < 2) w = 3;
+  u64 x[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = (seed + 8ull * t + j + 1) % GL_P;
+  for (uint32_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = gl_mul(x[j], w);
+  }
+  u64 r = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r ^= x[j];
+  out[t] = r;
+}
+
+hipError_t launch_modmul_chain(uint64_t seed, uint32_t threads, uint32_t iters, uint64_t *out,
+                               hipStream_t st) {
+  hipLaunchKernelGGL(k_modmul_chain, dim3((threads + 255) / 256), dim3(256), 0, st, seed,
+                     threads, iters, out);
+  return hipGetLastError();
+}
+
 }  // namespace rosetta

@@ -74,6 +74,7 @@ SIGNATURES = {
     "rosetta_ntt_inverse": (_ST, [_u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
     "rosetta_poly_mul": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, C.c_uint32, C.c_void_p]),
     "rosetta_field_op": (_ST, [C.c_int, _u64p, _u64p, _u64p, _u64p, C.c_size_t, C.c_void_p]),
+    "rosetta_modmul_chain": (_ST, [C.c_uint64, C.c_uint32, C.c_uint32, _u64p, C.c_void_p]),
     "rosetta_keygen": (_ST, [C.c_uint64, _pp, C.c_double, C.c_double, _u64p, _u64p, _u64p,
                              _u64p]),
     "rosetta_lwe_encrypt": (_ST, [C.c_uint64, _pp, C.c_double, _u64p, C.c_uint32, _u64p,
@@ -337,6 +338,14 @@ def field_op(op: int, a, b=None, c=None, out=None, stream=None):
     _check(lib().rosetta_field_op(op, _dev(a, "a"), None if b is None else _dev(b, "b"),
                                   None if c is None else _dev(c, "c"), _dev(out, "out"), count,
                                   _stream(stream)))
+    return out
+
+
+def modmul_chain(seed: int, threads: int, iters: int, out=None, stream=None):
+    """Throughput probe: 8 register-resident product chains per thread
+    (see rosetta_modmul_chain); returns out[threads]."""
+    out = empty(threads) if out is None else out
+    _check(lib().rosetta_modmul_chain(seed, threads, iters, _dev(out, "out"), _stream(stream)))
     return out
 
 

@@ -85,6 +85,8 @@ def test_null_and_empty_batches_touch_no_device(L):
     assert L.rosetta_field_op(3, fake, fake, None, fake, 2, None) == 1
     assert L.rosetta_field_op(256 + 48, None, None, None, fake, 2, None) == 1
     assert L.rosetta_field_op(2, None, None, None, None, 0, None) == 0
+    assert L.rosetta_modmul_chain(1, 0, 10, None, None) == 0
+    assert L.rosetta_modmul_chain(1, 5, 10, None, None) == 1
 
 
 def test_alias_and_size_detection(L):

@@ -91,3 +91,16 @@ def test_field_ops_in_place(operands):
     R.field_op(R.FIELD_MUL, x, y, out=x)
     want = np.array([u * v % P for u, v in zip(a, b)], dtype=np.uint64)
     assert np.array_equal(R.to_host(x), want)
+
+
+def test_modmul_chain_probe_computes_the_powers():
+    require_gpu()
+    seed, threads, iters = 12345, 300, 37
+    got = R.to_host(R.modmul_chain(seed, threads, iters))
+    for t in (0, 1, 255, 256, 299):
+        w = (seed ^ ((t * 0x9E3779B97F4A7C15) % 2 ** 64)) % P
+        w = 3 if w < 2 else w
+        want = 0
+        for j in range(8):
+            want ^= (seed + 8 * t + j + 1) % P * pow(w, iters, P) % P
+        assert int(got[t]) == want, t
