@@ -100,12 +100,18 @@ def cpu_baseline(w, keys, cts, v, seconds_target: float):
     from oracle import oracle as O
     op = O.Params.make(**{k: x for k, x in w.params().items() if k != "k"})
     cores = min(os.cpu_count() or 1, int(os.environ.get("OMP_NUM_THREADS", "16") or 16))
-    # calibrate on one ciphertext, then size the sample to ~seconds_target
-    t0 = time.perf_counter()
-    O.pbs(op, cts[:1], keys["bsk"], keys["ksk"], v, O.NTT, 1)
-    one = time.perf_counter() - t0
-    sample = max(cores, int(seconds_target * cores / max(one, 1e-3)) // cores * cores)
-    sample = min(sample, cts.shape[0])
+    # two-point calibration with one and two rounds of `cores` ciphertexts:
+    # each call pays a fixed key transform K plus R per round; size the
+    # sample so that K + rounds * R is about seconds_target
+    def timed(count):
+        t0 = time.perf_counter()
+        O.pbs(op, cts[:count], keys["bsk"], keys["ksk"], v, O.NTT, cores)
+        return time.perf_counter() - t0
+    c1, c2 = timed(cores), timed(2 * cores)
+    per_round = max(c2 - c1, 1e-3)
+    fixed = max(c1 - per_round, 0.0)
+    rounds = max(1, int(round((seconds_target - fixed) / per_round)))
+    sample = min(rounds * cores, cts.shape[0])
     t0 = time.perf_counter()
     O.pbs(op, cts[:sample], keys["bsk"], keys["ksk"], v, O.NTT, cores)
     dt = time.perf_counter() - t0
