@@ -190,6 +190,17 @@ CORNERS = {
     # the largest ring, general first stage, 2 waves per SIMD
     "l4_b15_N4096": dict(n=24, N=4096, pbs_level=4, pbs_base_log=15, ks_level=3, ks_base_log=6,
                          msg_bits=3),
+    # small-digit first stages (integer stages 0-1) at the rings no workload uses
+    "l3_b8_N512": dict(n=20, N=512, pbs_level=3, pbs_base_log=8, ks_level=4, ks_base_log=4,
+                       msg_bits=2),
+    "l2_b14_N1024": dict(n=20, N=1024, pbs_level=2, pbs_base_log=14, ks_level=4, ks_base_log=4,
+                         msg_bits=2),
+    # the largest small digits (beta = 14) with a 64-bit rounded value, both rings
+    # whose first pass differs (N = 256: two stages; N = 4096: three)
+    "l4_b14_N4096": dict(n=8, N=4096, pbs_level=4, pbs_base_log=14, ks_level=3, ks_base_log=6,
+                         msg_bits=3),
+    "l3_b14_N256": dict(n=12, N=256, pbs_level=3, pbs_base_log=14, ks_level=3, ks_base_log=4,
+                        msg_bits=2),
 }
 
 
