@@ -46,11 +46,26 @@ PMC_PROFILE = os.path.join(ROOT, "profiles", "k_blind_rotate_llama3_8b_silu_pmc.
 KERNEL_SOURCES = ["gl.hpp", "ntt.hpp", "kernels.hip"]
 
 
+def kernel_source_digest() -> str:
+    """sha256 of the blind-rotation kernel sources (gl.hpp, ntt.hpp,
+    kernels.hip in that order) with comments and whitespace removed, so that
+    it changes with the code and not with its prose."""
+    import hashlib
+    import re
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_16915_amd", "csrc", f)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(re.sub(r"\s+", "", text).encode())
+    return h.hexdigest()
+
+
 def measured_traffic(workload: str, batch: int):
     """Calibrated HBM bytes per blind-rotation launch from the committed
     counter profile, or None unless that profile describes the current
-    kernel sources and this workload."""
-    import hashlib
+    kernel code and this workload."""
     import re
     from paper_2609_16915_amd import workloads as W
     if workload != W.HEADLINE or batch != W.get(W.HEADLINE).batch:
@@ -59,13 +74,9 @@ def measured_traffic(workload: str, batch: int):
         text = open(PMC_PROFILE).read()
     except OSError:
         return None
-    h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2609_16915_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    m_sha = re.search(r"kernel_source_sha256: ([0-9a-f]{64})", text)
+    m_sha = re.search(r"kernel_code_sha256: ([0-9a-f]{64})", text)
     m_tb = re.search(r"traffic_bytes_per_launch: ([0-9.eE+]+)", text)
-    if not m_sha or not m_tb or m_sha.group(1) != h.hexdigest():
+    if not m_sha or not m_tb or m_sha.group(1) != kernel_source_digest():
         return None
     return float(m_tb.group(1))
 

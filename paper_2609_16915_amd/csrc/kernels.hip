@@ -262,7 +262,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
           }
         }
         // a3: digit polynomial of level t;  a4: forward transform (its first
-        // stage in integer arithmetic while the digits are small)
+        // two stages in integer arithmetic while the digits are small)
         RT d[E];
 #pragma unroll
         for (int k = 0; k < E; ++k) {
