@@ -201,6 +201,7 @@ struct FirstElem {
 template <int E>
 struct FirstTerms {
   FirstElem el[E];
+  bool complete;  // every element has exactly one term at each weight
 };
 
 template <class S>
@@ -252,14 +253,22 @@ constexpr FirstTerms<S::E> first_terms() {
     }
   }
   FirstTerms<E> r{};
-  for (int k = 0; k < E; ++k)
-    for (int i = 0; i < 4; ++i) r.el[k].w[ex[k][i]] = FirstTerm{idx[k][i], sg[k][i]};
+  r.complete = true;
+  for (int k = 0; k < E; ++k) {
+    int seen = 0;
+    for (int i = 0; i < n[k]; ++i) {
+      seen |= 1 << ex[k][i];
+      r.el[k].w[ex[k][i]] = FirstTerm{idx[k][i], sg[k][i]};
+    }
+    r.complete = r.complete && n[k] == 4 && seen == 15;
+  }
   return r;
 }
 
 template <class S, typename RT>
 __device__ __forceinline__ void ntt_fwd_stages01_small(const RT (&d)[S::E], u64 (&x)[S::E]) {
   constexpr FirstTerms<S::E> T = first_terms<S>();
+  static_assert(T.complete, "two stages must give one term per weight");
   static_for<0, S::E>([&](auto kc) {
     constexpr FirstElem f = T.el[decltype(kc)::value];
     const int32_t a = (int32_t)d[f.w[0].idx], b = (int32_t)d[f.w[1].idx];
