@@ -127,17 +127,21 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
     const u64 psi = gl_pow(7, (GL_P - 1) / (2 * (u64)N));
     std::vector<u64> z(N);
     for (uint32_t m = 0; m < N; ++m) z[m] = gl_pow(psi, bitrev(m, logn));
-    // radix-8 powers for the passes after the first that span three stages
-    // (passes of 3 stages when N > 256; the first pass uses no table)
+    // passes after the first that span three stages (N >= 512) run in
+    // twisted radix-8 form: their table region [2^s0, 2^(s0+3)) (the
+    // twiddles of stages s0..s0+2, read by no other pass) becomes the
+    // powers q^1..q^7 of q = zeta[4 (2^s0 + b)], 7 words per block b
     if (logn >= 9) {
+      const std::vector<u64> z0 = z;
       for (int q = 1; 3 * q + 3 <= logn; ++q) {
-        const int s0 = 3 * q;
-        for (uint32_t b = 0; b < (1u << s0); ++b) {
-          const u64 qq = z[4 * ((1u << s0) + b)];
-          z.push_back(gl_pow(qq, 3));
-          z.push_back(gl_pow(qq, 5));
-          z.push_back(gl_pow(qq, 6));
-          z.push_back(gl_pow(qq, 7));
+        const uint32_t nb = 1u << (3 * q);
+        for (uint32_t b = 0; b < nb; ++b) {
+          const u64 qq = z0[4 * (nb + b)];
+          u64 pw = qq;
+          for (uint32_t i = 0; i < 7; ++i) {
+            z[nb + 7 * b + i] = pw;
+            pw = gl_mul(pw, qq);
+          }
         }
       }
     }

@@ -20,8 +20,8 @@ namespace rosetta {
 // ---------------------------------------------------------------------------
 
 // Dynamic LDS of the transform kernels: the twiddle area (TW_WORDS words:
-// zeta[N] then the radix-8 powers), then the exchange buffers (XCHG_WORDS,
-// see LdsBufs).
+// the zeta table with the twisted passes' block powers, see Ntt), then the
+// exchange buffers (XCHG_WORDS, see LdsBufs).
 extern __shared__ __align__(16) u64 lds_dyn[];
 
 template <class S>

@@ -70,20 +70,17 @@ struct Ntt {
     return (tid & ((1 << lo(q)) - 1)) + (k << lo(q)) + ((tid >> lo(q)) << (lo(q) + LE));
   }
   // Passes after the first that span three stages run in twisted radix-8
-  // form and need, per block of their first stage, the powers q^3, q^5,
-  // q^6, q^7 of q = zeta[4 m] (q, q^2, q^4 are zeta[4m], zeta[2m], zeta[m]).
+  // form and need, per block b of their first stage s0, the powers q^1..q^7
+  // of q = zeta[4 (2^s0 + b)].  The table region [2^s0, 2^(s0+3)) holds the
+  // twiddles of exactly those three stages and no other pass reads it, so
+  // for such a pass it stores q^1..q^7 of block b at 2^s0 + 7 b instead:
+  // 7 words per block fill it exactly, and the odd stride puts the blocks
+  // of a half wave on distinct LDS banks.
   __host__ __device__ static constexpr bool twisted(int q) {
     return q >= 1 && LE == 3 && stage_end(q) - stage_begin(q) == 3;
   }
-  __host__ __device__ static constexpr int tw8_base(int q) {
-    int b = 0;
-    for (int r = 1; r < q; ++r)
-      if (twisted(r)) b += 4 << stage_begin(r);
-    return b;
-  }
-  static constexpr int TW8_WORDS = tw8_base(PASSES);
-  // words of the LDS twiddle area: zeta[N] then the radix-8 powers
-  static constexpr int TW_WORDS = N + TW8_WORDS;
+  // words of the LDS twiddle area (the table above)
+  static constexpr int TW_WORDS = N;
   // In pass q each wave (64 threads) holds one contiguous block of
   // 2^(6+LE) indices when lo(q) <= 6 (the wave id then sets the top index
   // bits), or the whole transform when the workgroup is one wave.  An
@@ -304,15 +301,9 @@ template <class S, int Q>
 __device__ __forceinline__ void ntt_fwd_pass_twisted(u64 (&x)[S::E], int tid, const u64 *tw) {
   constexpr int lo = S::lo(Q), s0 = S::stage_begin(Q);
   const int b = tid >> lo;  // block at stage s0
-  const int m = (1 << s0) + b;
-  const u64 *t8 = tw + S::N + S::tw8_base(Q) + 4 * b;
-  x[1] = gl_mul(x[1], tw[4 * m]);
-  x[2] = gl_mul(x[2], tw[2 * m]);
-  x[3] = gl_mul(x[3], t8[0]);
-  x[4] = gl_mul(x[4], tw[m]);
-  x[5] = gl_mul(x[5], t8[1]);
-  x[6] = gl_mul(x[6], t8[2]);
-  x[7] = gl_mul(x[7], t8[3]);
+  const u64 *qp = tw + (1 << s0) + 7 * b;  // q^1 .. q^7
+#pragma unroll
+  for (int k = 1; k < 8; ++k) x[k] = gl_mul(x[k], qp[k - 1]);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const u64 u = x[k], v = x[k + 4];
@@ -352,8 +343,7 @@ template <class S, int Q>
 __device__ __forceinline__ void ntt_inv_pass_twisted(u64 (&x)[S::E], int tid, const u64 *tw) {
   constexpr int lo = S::lo(Q), s0 = S::stage_begin(Q);
   const int br = (1 << s0) - 1 - (tid >> lo);  // reflected block
-  const int mr = (1 << s0) + br;
-  const u64 *t8 = tw + S::N + S::tw8_base(Q) + 4 * br;
+  const u64 *qp = tw + (1 << s0) + 7 * br;  // powers of q_r = zeta[4 (2^s0 + br)]
   u64 z[8] = {x[7], x[6], x[4], x[5], x[0], x[1], x[2], x[3]};
   {
     u64 u = z[0], v = z[1];
@@ -389,13 +379,8 @@ __device__ __forceinline__ void ntt_inv_pass_twisted(u64 (&x)[S::E], int tid, co
     z[k + 4] = gl_sub(u, v);
   }
   x[0] = z[0];
-  x[1] = gl_mul(z[1], tw[4 * mr]);
-  x[2] = gl_mul(z[2], tw[2 * mr]);
-  x[3] = gl_mul(z[3], t8[0]);
-  x[4] = gl_mul(z[4], tw[mr]);
-  x[5] = gl_mul(z[5], t8[1]);
-  x[6] = gl_mul(z[6], t8[2]);
-  x[7] = gl_mul(z[7], t8[3]);
+#pragma unroll
+  for (int k = 1; k < 8; ++k) x[k] = gl_mul(z[k], qp[k - 1]);
 }
 
 // Forward stages of pass Q; `tw` is the LDS twiddle table.
@@ -557,7 +542,8 @@ __device__ __forceinline__ void ntt_inverse(u64 (&x)[S::E], LdsBufs<S> &lds, int
   ntt_inv_from<S, S::PASSES - 1>(x, lds, tid, tw);
 }
 
-// Copy the twiddle area (zeta[N] and the radix-8 powers, TW_WORDS words)
+// Copy the twiddle area (TW_WORDS words: zeta with the twisted passes'
+// regions holding their block powers)
 // into LDS (all threads of the workgroup).
 template <class S>
 __device__ __forceinline__ void load_twiddles(u64 *tw_lds, const u64 *__restrict__ zeta,
