@@ -131,6 +131,23 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
     // twisted radix-8 form: their table region [2^s0, 2^(s0+3)) (the
     // twiddles of stages s0..s0+2, read by no other pass) becomes the
     // powers q^1..q^7 of q = zeta[4 (2^s0 + b)], 7 words per block b
+    // the last pass (threads own E consecutive indices), when it is not
+    // twisted: each of its stages s stores block t nc + c (nc = E / 2^(logn -
+    // s) blocks per thread, T = N / E threads) at 2^s + c T + t
+    {
+      const int le = logn == 8 ? 2 : 3;  // elements per thread E = 2^le, as dispatched
+      const int passes = (logn + le - 1) / le, s0 = (passes - 1) * le;
+      const bool last_twisted = le == 3 && logn - s0 == 3;
+      if (!last_twisted) {
+        const uint32_t T = N >> le;
+        const std::vector<u64> z0 = z;
+        for (int s = s0; s < logn; ++s) {
+          const uint32_t nc = (1u << le) >> (logn - s);
+          for (uint32_t t = 0; t < T; ++t)
+            for (uint32_t c = 0; c < nc; ++c) z[(1u << s) + c * T + t] = z0[(1u << s) + t * nc + c];
+        }
+      }
+    }
     if (logn >= 9) {
       const std::vector<u64> z0 = z;
       for (int q = 1; 3 * q + 3 <= logn; ++q) {

@@ -79,7 +79,8 @@ struct Ntt {
   __host__ __device__ static constexpr bool twisted(int q) {
     return q >= 1 && LE == 3 && stage_end(q) - stage_begin(q) == 3;
   }
-  // words of the LDS twiddle area (the table above)
+  // words of the LDS twiddle area (the table above; the stages of a last
+  // pass that is not twisted are stored slot-major, see ntt_fwd_pass)
   static constexpr int TW_WORDS = N;
   // In pass q each wave (64 threads) holds one contiguous block of
   // 2^(6+LE) indices when lo(q) <= 6 (the wave id then sets the top index
@@ -383,7 +384,11 @@ __device__ __forceinline__ void ntt_inv_pass_twisted(u64 (&x)[S::E], int tid, co
   for (int k = 1; k < 8; ++k) x[k] = gl_mul(z[k], qp[k - 1]);
 }
 
-// Forward stages of pass Q; `tw` is the LDS twiddle table.
+// Forward stages of pass Q; `tw` is the LDS twiddle table.  In the last
+// pass (lo = 0) thread t holds indices E t .. E t + E - 1, so at stage s it
+// needs the nc = E / 2^(LOGN - s) consecutive blocks t nc .. t nc + nc - 1;
+// that stage's table region is stored slot-major there (block t nc + c at
+// 2^s + c T + t), so that a wave's reads of one slot are consecutive words.
 template <class S, int Q>
 __device__ __forceinline__ void ntt_fwd_pass(u64 (&x)[S::E], int tid, const u64 *tw) {
   constexpr int lo = S::lo(Q);
@@ -392,12 +397,12 @@ __device__ __forceinline__ void ntt_fwd_pass(u64 (&x)[S::E], int tid, const u64 
   for (int s = S::stage_begin(Q); s < S::stage_end(Q); ++s) {
     const int sh = S::LOGN - s;
     const int b = sh - 1 - lo;  // k-bit split by this stage
-    const u64 *zs = tw + (1 << s) + (jt >> sh);
+    const u64 *zs = lo == 0 ? tw + (1 << s) + tid : tw + (1 << s) + (jt >> sh);
 #pragma unroll
     for (int k = 0; k < S::E; ++k) {
       if (k & (1 << b)) continue;
       const int k2 = k | (1 << b);
-      const u64 w = zs[k >> (sh - lo)];
+      const u64 w = lo == 0 ? zs[(k >> sh) * S::T] : zs[k >> (sh - lo)];
       const u64 t = gl_mul(x[k2], w);
       x[k2] = gl_sub(x[k], t);
       x[k] = gl_add(x[k], t);
@@ -406,7 +411,9 @@ __device__ __forceinline__ void ntt_fwd_pass(u64 (&x)[S::E], int tid, const u64 
 }
 
 // Inverse (Gentleman-Sande) stages of pass Q, in reverse stage order:
-// (u, v) -> (u + v, (v - u) * zeta[2^(s+1) - 1 - b]).
+// (u, v) -> (u + v, (v - u) * zeta[2^(s+1) - 1 - b]).  In the last pass the
+// reflected block 2^s - 1 - (t nc + c) = (T - 1 - t) nc + (nc - 1 - c) is
+// read from the slot-major layout of ntt_fwd_pass.
 template <class S, int Q>
 __device__ __forceinline__ void ntt_inv_pass(u64 (&x)[S::E], int tid, const u64 *tw) {
   constexpr int lo = S::lo(Q);
@@ -415,12 +422,13 @@ __device__ __forceinline__ void ntt_inv_pass(u64 (&x)[S::E], int tid, const u64 
   for (int s = S::stage_end(Q) - 1; s >= S::stage_begin(Q); --s) {
     const int sh = S::LOGN - s;
     const int b = sh - 1 - lo;
-    const u64 *zs = tw + (2 << s) - 1 - (jt >> sh);
+    const int nc = S::E >> sh;
+    const u64 *zs = lo == 0 ? tw + (1 << s) + (S::T - 1 - tid) : tw + (2 << s) - 1 - (jt >> sh);
 #pragma unroll
     for (int k = 0; k < S::E; ++k) {
       if (k & (1 << b)) continue;
       const int k2 = k | (1 << b);
-      const u64 w = zs[-(k >> (sh - lo))];
+      const u64 w = lo == 0 ? zs[(nc - 1 - (k >> sh)) * S::T] : zs[-(k >> (sh - lo))];
       const u64 u = x[k], v = x[k2];
       x[k] = gl_add(u, v);
       x[k2] = gl_mul(gl_sub(v, u), w);
