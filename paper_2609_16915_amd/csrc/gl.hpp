@@ -44,8 +44,8 @@ __host__ __device__ __forceinline__ u64 gl_add(u64 a, u64 b) {
 
 // (a - b) mod p for canonical a, b: on a borrow add p, i.e. subtract EPS
 // mod 2^64, spelled as +borrow on the low word and -borrow on the high word
-// with the low word's carry.
-__host__ __device__ __forceinline__ u64 gl_sub(u64 a, u64 b) {
+// with the low word's carry.  (The device uses gl_sub_dev.)
+__host__ __device__ __forceinline__ u64 gl_sub_portable(u64 a, u64 b) {
   u32 b1, k;
   const u32 d0 = __builtin_subc((u32)a, (u32)b, 0u, &b1);
   const u32 d1 = __builtin_subc((u32)(a >> 32), (u32)(b >> 32), b1, &b1);
@@ -177,6 +177,35 @@ __device__ __forceinline__ u32 sel_eps(u64 m) {
 }
 // r + (m ? 2^32 - 1 : 0), i.e. r - p (mod 2^64) on the lanes of m
 __device__ __forceinline__ u64 add_eps_if(u64 r, u64 m) { return r + (u64)sel_eps(m); }
+// a - b - borrow-in, with borrow-out
+__device__ __forceinline__ u32 subb_c(u32 a, u32 b, u64 bi, u64 &bo) {
+  u32 r;
+  asm("v_subb_co_u32_e64 %0, %1, %2, %3, %4" : "=v"(r), "=s"(bo) : "v"(a), "v"(b), "s"(bi));
+  return r;
+}
+// a + carry-in, with carry-out
+__device__ __forceinline__ u32 inc_c(u32 a, u64 ci, u64 &co) {
+  u32 r;
+  asm("v_addc_co_u32_e64 %0, %1, %2, 0, %3" : "=v"(r), "=s"(co) : "v"(a), "s"(ci));
+  return r;
+}
+// a - borrow-in, borrow-out discarded
+__device__ __forceinline__ u32 dec_bi(u32 a, u64 bi) {
+  u32 r;
+  u64 bo;
+  asm("v_subb_co_u32_e64 %0, %1, %2, 0, %3" : "=v"(r), "=s"(bo) : "v"(a), "s"(bi));
+  return r;
+}
+// d - (2^32 - 1), i.e. d + p (mod 2^64), on the lanes of m, in two carry
+// instructions: the low word rises by one (carrying out where it was
+// 2^32 - 1) and the high word drops by one except where the low word
+// carried; the scalar unit forms that lane mask.
+__device__ __forceinline__ u64 sub_eps_if(u64 d, u64 m) {
+  u64 k;
+  const u32 lo = inc_c((u32)d, m, k);
+  const u32 hi = dec_bi((u32)(d >> 32), m & ~k);
+  return gl_mk(lo, hi);
+}
 
 }  // namespace isa
 
@@ -184,7 +213,9 @@ __device__ __forceinline__ u64 add_eps_if(u64 r, u64 m) { return r + (u64)sel_ep
 // EPS (plus p mod 2^64) on a borrow, which leaves t in [p - 2^32, p); then
 // R = c2 EPS + t with its carry: a carry leaves R + EPS below p (R is below
 // 2^64 - 2^33 + 1 after the wrap), no carry leaves R in [0, 2^64), so one
-// conditional EPS covers "carry or R >= p".
+// conditional EPS covers "carry or R >= p".  (The borrow correction keeps
+// the select form: sub_eps_if is one instruction shorter but puts a scalar
+// step on the product's dependent chain, which cost more than it saved.)
 __device__ __forceinline__ u64 gl_reduce_dev(u32 c0, u32 c1, u32 c2, u32 c3) {
   u64 b0, b1, b2, b3;
   const u32 d0 = isa::sub_c(c0, c3, b0);
@@ -265,15 +296,30 @@ __device__ __forceinline__ u64 gl_mul_pow2_dev(u64 x) {
     const u32 c2 = (u32)x << f;
     const u64 h = f ? (x >> (32 - f)) : (x >> 32);
     const u64 R = (u64)c2 * 0xFFFFFFFFull;
-    u32 b1, k, kk;
-    const u32 d0 = __builtin_subc((u32)R, (u32)h, 0u, &b1);
-    const u32 d1 = __builtin_subc((u32)(R >> 32), (u32)(h >> 32), b1, &b1);
-    const u32 r0 = __builtin_addc(d0, 0u, b1, &k);
-    const u32 r1 = __builtin_subc(__builtin_addc(d1, 0u, k, &kk), 0u, b1, &kk);
-    return gl_mk(r0, r1);
+    u64 b0, b1;
+    const u32 d0 = isa::sub_c((u32)R, (u32)h, b0);
+    const u32 d1 = isa::subb_c((u32)(R >> 32), (u32)(h >> 32), b0, b1);
+    return isa::sub_eps_if(gl_mk(d0, d1), b1);
   }
 }
+
+// (a - b) mod p for canonical a, b: as gl_sub_portable, with the
+// correction applied through carry-ins (4 instructions instead of 5).
+__device__ __forceinline__ u64 gl_sub_dev(u64 a, u64 b) {
+  u64 b0, b1;
+  const u32 d0 = isa::sub_c((u32)a, (u32)b, b0);
+  const u32 d1 = isa::subb_c((u32)(a >> 32), (u32)(b >> 32), b0, b1);
+  return isa::sub_eps_if(gl_mk(d0, d1), b1);
+}
 #endif  // __HIP_DEVICE_COMPILE__
+
+__host__ __device__ __forceinline__ u64 gl_sub(u64 a, u64 b) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return gl_sub_dev(a, b);
+#else
+  return gl_sub_portable(a, b);
+#endif
+}
 
 __host__ __device__ __forceinline__ u64 gl_mul(u64 a, u64 b) {
 #if defined(__HIP_DEVICE_COMPILE__)

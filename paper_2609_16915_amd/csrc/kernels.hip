@@ -9,6 +9,8 @@
 // served from L2 / the Infinity Cache to the others.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "gl.hpp"
 #include "internal.hpp"
 #include "ntt.hpp"
@@ -138,22 +140,6 @@ __device__ __forceinline__ u64 rotated_coef(const u64 *v, int j, int r) {
   return neg ? gl_neg(x) : x;
 }
 
-// Digit t (0 = most significant) of the balanced base-2^beta expansion of
-// the rounded value r (see gl_digit); L is the number of levels.
-template <int L, typename RT>
-__device__ __forceinline__ RT digit_of(RT r, int beta, int t) {
-  const RT half = (RT)1 << (beta - 1);
-  const RT mask = ((RT)1 << beta) - 1;
-  RT d = 0;
-#pragma unroll
-  for (int u = L - 1; u >= 1; --u) {
-    const RT du = ((r + half) & mask) - half;
-    if (u == t) d = du;
-    r = (r - du) >> beta;
-  }
-  return t == 0 ? r : d;
-}
-
 // One workgroup per ciphertext.  Per CMux step i:
 //   a2  D_u = X^(a~_i) ACC_u - ACC_u           (rotation through LDS)
 //   a3  digits of D_u, level t                 (registers)
@@ -249,7 +235,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
       // levels from the least significant (t = L-1) up: each pass takes
       // the balanced low digit of R and shifts it out, the last level is
       // what remains (the sums over t are exact, so their order is free)
-      const RT half = (RT)1 << (beta - 1), mask = ((RT)1 << beta) - 1;
+      const RT half = (RT)1 << (beta - 1);
 #pragma unroll 1
       for (int t = L - 1; t >= 0; --t) {
         gconst_u64 *g = G + (size_t)((u * L + t) * 2) * N;
@@ -264,13 +250,16 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
         // a3: digit polynomial of level t;  a4: forward transform (its first
         // two stages in integer arithmetic while the digits are small)
         RT d[E];
+        if (t == 0) {
 #pragma unroll
-        for (int k = 0; k < E; ++k) {
-          if (t == 0) {
-            d[k] = R[k];
-          } else {
-            d[k] = ((R[k] + half) & mask) - half;
-            R[k] = (R[k] - d[k]) >> beta;
+          for (int k = 0; k < E; ++k) d[k] = R[k];
+        } else {
+          // the low beta bits sign-extended, the rest carried up
+          const int dsh = (int)(8 * sizeof(RT)) - beta;
+#pragma unroll
+          for (int k = 0; k < E; ++k) {
+            d[k] = (RT)((std::make_unsigned_t<RT>)R[k] << dsh) >> dsh;
+            R[k] = (R[k] + half) >> beta;
           }
         }
         u64 x[E];
@@ -296,9 +285,9 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
         }
       }
     }
-    // a6: back to coefficients, accumulate (one loop body for both
-    // components keeps a single copy of the inverse transform)
-#pragma unroll 1
+    // a6: back to coefficients, accumulate (unrolled: with c a compile-time
+    // index the accumulator updates need no per-element selection)
+#pragma unroll
     for (int c = 0; c < 2; ++c) {
       u64 y[E];
 #pragma unroll
@@ -421,17 +410,28 @@ k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restric
 #pragma unroll
     for (int k = 0; k < E; ++k) Y0[k] = Y1[k] = 0;
     gconst_u64 *G = as_global(autk) + (size_t)(kr - 1) * round_words + tid;
+    // levels from the least significant up, as in the blind rotation
+    const i64 half = (i64)1 << (beta - 1);
 #pragma unroll 1
-    for (int t = 0; t < L; ++t) {
+    for (int t = L - 1; t >= 0; --t) {
+      i64 d[E];
+      if (t == 0) {
+#pragma unroll
+        for (int k = 0; k < E; ++k) d[k] = R[k];
+      } else {
+        const int dsh = 64 - beta;
+#pragma unroll
+        for (int k = 0; k < E; ++k) {
+          d[k] = (i64)((u64)R[k] << dsh) >> dsh;
+          R[k] = (R[k] + half) >> beta;
+        }
+      }
       u64 x[E];
       if (beta <= 14) {
-        i64 d[E];
-#pragma unroll
-        for (int k = 0; k < E; ++k) d[k] = digit_of<L, i64>(R[k], beta, t);
         ntt_forward_small<S, i64>(d, x, lds, tid, tw);
       } else {
 #pragma unroll
-        for (int k = 0; k < E; ++k) x[k] = gl_from_i64(digit_of<L, i64>(R[k], beta, t));
+        for (int k = 0; k < E; ++k) x[k] = gl_from_i64(d[k]);
         ntt_forward<S>(x, lds, tid, tw);
       }
       gconst_u64 *g = G + (size_t)(t * 2) * N;
@@ -441,7 +441,7 @@ k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restric
         Y1[k] = gl_mul_add(x[k], g[N + k * T], Y1[k]);
       }
     }
-#pragma unroll 1
+#pragma unroll
     for (int c = 0; c < 2; ++c) {
       u64 y[E];
 #pragma unroll
