@@ -193,9 +193,14 @@ rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *
  *   ROSETTA_FIELD_MUL      a * b
  *   ROSETTA_FIELD_MUL_ADD  a * b + c
  *   ROSETTA_FIELD_MUL_POW2 + e   a * 2^e   (0 <= e < 96; 2^96 = -1 mod p)
- * a, b, c, out: device [count] u64.  Every input must be canonical (< p);
- * the result is canonical.  b and c are not read (and may be NULL) when the
- * op does not use them; out may alias an input exactly.  Errors:
+ *   ROSETTA_FIELD_ROUND_TOP + s  (1 <= s <= 63) the rounding that opens the
+ *       gadget decomposition of the blind rotation (Sec. 2.2, PBS
+ *       paragraph): floor((a_c + 2^(s-1)) / 2^s) for the centred
+ *       representative a_c of a in (-p/2, p/2], as a two's-complement int64;
+ *       a = p is also accepted (as 0)
+ * a, b, c, out: device [count] u64.  Every input must be canonical (< p)
+ * unless stated; the result is canonical.  b and c are not read (and may be
+ * NULL) when the op does not use them; out may alias an input exactly.  Errors:
  * ROSETTA_ERR_PARAMS for an unknown op, ROSETTA_ERR_NULL for a missing
  * pointer the op reads or writes. */
 enum {
@@ -203,7 +208,8 @@ enum {
   ROSETTA_FIELD_SUB = 1,
   ROSETTA_FIELD_MUL = 2,
   ROSETTA_FIELD_MUL_ADD = 3,
-  ROSETTA_FIELD_MUL_POW2 = 256
+  ROSETTA_FIELD_MUL_POW2 = 256,
+  ROSETTA_FIELD_ROUND_TOP = 512
 };
 rosetta_status rosetta_field_op(int op, const uint64_t *a, const uint64_t *b, const uint64_t *c,
                                 uint64_t *out, size_t count, void *stream);

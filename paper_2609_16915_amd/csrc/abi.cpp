@@ -434,10 +434,12 @@ rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *
 rosetta_status rosetta_field_op(int op, const uint64_t *a, const uint64_t *b, const uint64_t *c,
                                 uint64_t *out, size_t count, void *stream) {
   const bool pow2 = op >= ROSETTA_FIELD_MUL_POW2 && op < ROSETTA_FIELD_MUL_POW2 + 96;
-  if (!pow2 && (op < ROSETTA_FIELD_ADD || op > ROSETTA_FIELD_MUL_ADD))
+  const bool round = op > ROSETTA_FIELD_ROUND_TOP && op < ROSETTA_FIELD_ROUND_TOP + 64;
+  const bool unary = pow2 || round;
+  if (!unary && (op < ROSETTA_FIELD_ADD || op > ROSETTA_FIELD_MUL_ADD))
     return fail(ROSETTA_ERR_PARAMS, "unknown field op %d", op);
   if (count == 0) return ok();
-  if (!a || !out || (!pow2 && !b) || (op == ROSETTA_FIELD_MUL_ADD && !c))
+  if (!a || !out || (!unary && !b) || (op == ROSETTA_FIELD_MUL_ADD && !c))
     return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
   hipError_t e = launch_field_op(op, a, b, c, out, count, (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "field_op launch");

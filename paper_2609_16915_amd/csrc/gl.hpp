@@ -419,6 +419,19 @@ __host__ __device__ __forceinline__ i64 gl_round_top(u64 a, int s) {
   return (ac >> s) + ((ac >> (s - 1)) & 1);
 }
 
+// gl_round_top for 34 <= s <= 63 from the high word alone, a 32-bit result.
+// The centred value's high word is hi(a), or hi(a - p) = hi(a + EPS) =
+// hi(a) + (lo(a) != 0) above (p - 1) / 2; with y = a_c >> (s - 1) =
+// hi(a_c) >> (s - 33), floor((a_c + 2^(s-1)) / 2^s) = (y + 1) >> 1, and
+// |y| < 2^30 keeps y + 1 from overflowing (at s = 33 it could).  Also exact
+// for a = p (the centred value 0).
+__host__ __device__ __forceinline__ int32_t gl_round_top32(u64 a, int s) {
+  const u32 lo = (u32)a, hi = (u32)(a >> 32);
+  const bool upper = a > (GL_P - 1) / 2;
+  const int32_t h = (int32_t)(hi + (u32)(upper && lo != 0));
+  return ((h >> (s - 33)) + 1) >> 1;
+}
+
 __host__ __device__ __forceinline__ i64 gl_digit(i64 r, int levels, int beta, int t) {
   const i64 half = (i64)1 << (beta - 1);
   const i64 mask = ((i64)1 << beta) - 1;

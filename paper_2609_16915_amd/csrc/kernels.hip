@@ -228,8 +228,13 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
           const int j = tid + T * k;
           const bool neg = (j < ar) != flip;
           const u64 v = buf[(j - ar) & (N - 1)];
-          const u64 d = gl_sub(neg ? gl_neg(v) : v, cur[k]);
-          R[k] = (RT)gl_round_top(d, s);
+          // -v as p - v: p itself for v = 0 is a valid minuend of gl_sub,
+          // and the rounding maps it to 0 as it does 0
+          const u64 d = gl_sub(neg ? GL_P - v : v, cur[k]);
+          if constexpr (sizeof(RT) == 4)
+            R[k] = gl_round_top32(d, s);  // s = 64 - l beta >= 34 here
+          else
+            R[k] = gl_round_top(d, s);
         }
       }
       // levels from the least significant (t = L-1) up: each pass takes
@@ -790,6 +795,16 @@ k_field_op(const u64 *__restrict__ a, const u64 *__restrict__ b, const u64 *__re
   }
 }
 
+// The decomposition's rounding of a at s, as the transform kernels compute
+// it (the 32-bit high-word form from s = 34 up), sign-extended.
+__global__ void __launch_bounds__(256)
+k_field_round(const u64 *__restrict__ a, u64 *__restrict__ out, size_t count, int s) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= count) return;
+  const i64 r = s >= 34 ? (i64)gl_round_top32(a[i], s) : gl_round_top(a[i], s);
+  out[i] = (u64)r;
+}
+
 template <int E>
 static hipError_t launch_field_pow2(int e, const u64 *a, u64 *out, size_t count, dim3 grid,
                                     hipStream_t st) {
@@ -824,6 +839,11 @@ hipError_t launch_field_op(int op, const uint64_t *a, const uint64_t *b, const u
                          out, count);
       break;
     default:
+      if (op > ROSETTA_FIELD_ROUND_TOP && op < ROSETTA_FIELD_ROUND_TOP + 64) {
+        hipLaunchKernelGGL(k_field_round, grid, dim3(256), 0, st, a, out, count,
+                           op - ROSETTA_FIELD_ROUND_TOP);
+        break;
+      }
       return launch_field_pow2<0>(op - ROSETTA_FIELD_MUL_POW2, a, out, count, grid, st);
   }
   return hipGetLastError();

@@ -84,6 +84,10 @@ def test_null_and_empty_batches_touch_no_device(L):
     assert L.rosetta_field_op(2, fake, None, None, fake, 2, None) == 1
     assert L.rosetta_field_op(3, fake, fake, None, fake, 2, None) == 1
     assert L.rosetta_field_op(256 + 48, None, None, None, fake, 2, None) == 1
+    assert L.rosetta_field_op(512, fake, None, None, fake, 2, None) == 2  # s = 0
+    assert L.rosetta_field_op(512 + 64, fake, None, None, fake, 2, None) == 2
+    assert L.rosetta_field_op(512 + 34, None, None, None, fake, 2, None) == 1
+    assert L.rosetta_field_op(512 + 34, fake, None, None, fake, 0, None) == 0
     assert L.rosetta_field_op(2, None, None, None, None, 0, None) == 0
     assert L.rosetta_modmul_chain(1, 0, 10, None, None) == 0
     assert L.rosetta_modmul_chain(1, 5, 10, None, None) == 1

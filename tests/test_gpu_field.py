@@ -84,6 +84,28 @@ def test_field_pow2_every_exponent(operands):
                                    for i in bad[:5]])
 
 
+def test_field_round_top_every_shift(operands):
+    # the rounding that opens the gadget decomposition, in both device forms
+    # (64-bit below s = 34, high word from s = 34 up), on the edge values,
+    # p itself (the minuend form of -0 in the blind rotation), values just
+    # around the centring boundary and whole multiples of 2^32 above it
+    a, _, _, _, _, _ = operands
+    h = (P - 1) // 2
+    extra = [P, h - 1, h, h + 1, h + 2, P - (1 << 32), P - (1 << 32) - 1,
+             0xFFFFFFFE00000000, 0x8000000100000000, 0x8000000000000001,
+             0x7FFFFFFF80000000, 0x7FFFFFFFFFFFFFFF, 0x7FFFFFFF00000000]
+    vals = list(a) + extra
+    dv = R.to_device(np.array(vals, dtype=np.uint64))
+    say(f"[field] round_top s = 1..63 on {len(vals)} values")
+    for s in range(1, 64):
+        got = R.to_host(R.field_op(R.FIELD_ROUND_TOP + s, dv)).view(np.int64)
+        want = np.array([((x - P if x > h else x) + (1 << (s - 1))) >> s for x in vals],
+                        dtype=np.int64)
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, (s, [(hex(vals[i]), int(got[i]), int(want[i]))
+                                   for i in bad[:5]])
+
+
 def test_field_ops_in_place(operands):
     a, b, _, _, _, _ = operands
     x = R.to_device(np.array(a, dtype=np.uint64))
