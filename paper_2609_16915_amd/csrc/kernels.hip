@@ -131,6 +131,22 @@ constexpr int br_waves_per_eu() {
   return S::LOGN >= 12 ? 2 : BR_WAVES_PER_EU;
 }
 
+// Rows of one GGSW read through a raw buffer descriptor: a wave-uniform
+// base, the lane's byte offset in a vector register and the row's byte
+// offset in a scalar register, so that the address arithmetic of the key
+// stream runs on the scalar unit.  Word 3 of the descriptor is the gfx9
+// raw-buffer setting (32-bit data format); num_records only bounds the
+// lane offset, which stays far below it.
+struct KeyRows {
+  __amdgpu_buffer_rsrc_t r;
+  __device__ __forceinline__ explicit KeyRows(const u64 *base)
+      : r(__builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, 0x7FFFFFFF, 0x00020000)) {}
+  __device__ __forceinline__ u64 load(int lane_byte, int row_byte) const {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, lane_byte, row_byte, 0);
+    return ((u64)v[1] << 32) | v[0];
+  }
+};
+
 // Coefficient j of X^r * v (negacyclic), 0 <= r < 2N.
 template <int N>
 __device__ __forceinline__ u64 rotated_coef(const u64 *v, int j, int r) {
@@ -209,7 +225,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
     u64 Y0[E], Y1[E];
 #pragma unroll
     for (int k = 0; k < E; ++k) Y0[k] = Y1[k] = 0;
-    gconst_u64 *G = as_global(bsk) + (size_t)i * ggsw_words + tid;
+    const KeyRows G(bsk + (size_t)i * ggsw_words);
 
 #pragma unroll 1
     for (int u = 0; u < 2; ++u) {
@@ -243,13 +259,13 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
       const RT half = (RT)1 << (beta - 1);
 #pragma unroll 1
       for (int t = L - 1; t >= 0; --t) {
-        gconst_u64 *g = G + (size_t)((u * L + t) * 2) * N;
+        const int row = (u * L + t) * 2 * N * 8;  // byte offset of GGSW_i[u][t][0]
         u64 g0[E], g1[E];
         if constexpr (PF) {
 #pragma unroll
           for (int k = 0; k < E; ++k) {
-            g0[k] = g[k * T];
-            g1[k] = g[N + k * T];
+            g0[k] = G.load(tid * 8, row + k * T * 8);
+            g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
           }
         }
         // a3: digit polynomial of level t;  a4: forward transform (its first
@@ -279,8 +295,8 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
         if constexpr (!PF) {
 #pragma unroll
           for (int k = 0; k < E; ++k) {
-            g0[k] = g[k * T];
-            g1[k] = g[N + k * T];
+            g0[k] = G.load(tid * 8, row + k * T * 8);
+            g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
           }
         }
 #pragma unroll
