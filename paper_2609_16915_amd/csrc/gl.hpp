@@ -44,7 +44,9 @@ __host__ __device__ __forceinline__ u64 gl_add(u64 a, u64 b) {
 
 // (a - b) mod p for canonical a, b: on a borrow add p, i.e. subtract EPS
 // mod 2^64, spelled as +borrow on the low word and -borrow on the high word
-// with the low word's carry.  (The device uses gl_sub_dev.)
+// with the low word's carry.  (The device uses gl_sub_dev.)  Any a < 2^64
+// with canonical b also works: a borrow means a < b < p, and without one
+// a - b is below 2^64 and congruent (canonical when a is).
 __host__ __device__ __forceinline__ u64 gl_sub_portable(u64 a, u64 b) {
   u32 b1, k;
   const u32 d0 = __builtin_subc((u32)a, (u32)b, 0u, &b1);
@@ -318,6 +320,28 @@ __host__ __device__ __forceinline__ u64 gl_sub(u64 a, u64 b) {
   return gl_sub_dev(a, b);
 #else
   return gl_sub_portable(a, b);
+#endif
+}
+
+// a + b up to a multiple of p, for any a < 2^64 and canonical b: the result
+// is below 2^64 and congruent to a + b, not necessarily below p.  A wrap
+// past 2^64 adds EPS, and cannot wrap again: a + b - 2^64 < p, so the sum
+// stays below p + EPS = 2^64.  One compare fewer than gl_add; gl_sub (any
+// minuend, canonical subtrahend), gl_mul, gl_mul_add and gl_mul_pow2 all
+// accept such values.
+__host__ __device__ __forceinline__ u64 gl_add_weak(u64 a, u64 b) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  // the wrap's EPS through a multiply-add of the 0/1 carry (the sum is
+  // already a register pair, so no zero-extended addend is needed)
+  u64 c0, c1, cy;
+  const u32 s0 = isa::add_c((u32)a, (u32)b, c0);
+  const u32 s1 = isa::addc_c((u32)(a >> 32), (u32)(b >> 32), c0, c1);
+  u32 w;
+  asm("v_cndmask_b32_e64 %0, 0, 1, %1" : "=v"(w) : "s"(c1));
+  return isa::mad_eps_c(w, gl_mk(s0, s1), cy);
+#else
+  const u64 s = a + b;
+  return s < a ? s + GL_EPS : s;
 #endif
 }
 

@@ -806,6 +806,8 @@ k_field_op(const u64 *__restrict__ a, const u64 *__restrict__ b, const u64 *__re
     out[i] = gl_mul(a[i], b[i]);
   } else if constexpr (OP == ROSETTA_FIELD_MUL_ADD) {
     out[i] = gl_mul_add(a[i], b[i], c[i]);
+  } else if constexpr (OP == ROSETTA_FIELD_ADD_WEAK) {
+    out[i] = gl_add_weak(a[i], b[i]);
   } else {
     out[i] = gl_mul_pow2<OP - ROSETTA_FIELD_MUL_POW2>(a[i]);
   }
@@ -852,6 +854,10 @@ hipError_t launch_field_op(int op, const uint64_t *a, const uint64_t *b, const u
       break;
     case ROSETTA_FIELD_MUL_ADD:
       hipLaunchKernelGGL(k_field_op<ROSETTA_FIELD_MUL_ADD>, grid, dim3(256), 0, st, a, b, c,
+                         out, count);
+      break;
+    case ROSETTA_FIELD_ADD_WEAK:
+      hipLaunchKernelGGL(k_field_op<ROSETTA_FIELD_ADD_WEAK>, grid, dim3(256), 0, st, a, b, c,
                          out, count);
       break;
     default:

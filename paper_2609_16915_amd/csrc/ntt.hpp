@@ -128,9 +128,23 @@ __host__ __device__ constexpr bool small_root_negative() {
   return zeta_log2(M) >= 96;
 }
 
+// Sums of the forward butterflies.  A weak forward transform (W) feeds only
+// products (the key multiply-accumulate), so its values need only stay below
+// 2^64 and congruent: a sum whose second operand is canonical (a product, a
+// shift, or a value kept canonical for that purpose) takes gl_add_weak, and
+// every difference has a canonical subtrahend, which gl_sub accepts with any
+// minuend.  Products and shifts accept any input and return canonical values.
+template <bool W>
+__device__ __forceinline__ u64 fwd_sum(u64 a, u64 b) {
+  if constexpr (W)
+    return gl_add_weak(a, b);
+  else
+    return gl_add(a, b);
+}
+
 // Pass 0 of the forward transform (all twiddles compile-time powers of
 // two), starting at stage FIRST.
-template <class S, int FIRST>
+template <class S, int FIRST, bool W = false>
 __device__ __forceinline__ void ntt_fwd_pass0(u64 (&x)[S::E]) {
   constexpr int lo = S::lo(0);
   static_for<FIRST, S::stage_end(0)>([&](auto sc) {
@@ -146,9 +160,9 @@ __device__ __forceinline__ void ntt_fwd_pass0(u64 (&x)[S::E]) {
         const u64 u = x[k];
         if constexpr (small_root_negative<m>()) {  // w = -|w|
           x[k] = gl_sub(u, t);
-          x[k2] = gl_add(u, t);
+          x[k2] = fwd_sum<W>(u, t);
         } else {
-          x[k] = gl_add(u, t);
+          x[k] = fwd_sum<W>(u, t);
           x[k2] = gl_sub(u, t);
         }
       }
@@ -298,7 +312,11 @@ __device__ __forceinline__ void ntt_fwd_stages01_small(const RT (&d)[S::E], u64 
 // factor w^-k is absorbed by feeding the inverse 8-point transform its
 // inputs rotated by one frequency (slots 7,6,4,5,0,1,2,3), after which the
 // untwist multiplies by powers of zeta[4 m_r].
-template <class S, int Q>
+//
+// Weak form (W, see fwd_sum): only x[0] may arrive non-canonical; the sums
+// that later serve as the second operand of a twiddle-1 butterfly (x[1],
+// x[2], x[3] after the first stage, x[1] after the second) stay canonical.
+template <class S, int Q, bool W = false>
 __device__ __forceinline__ void ntt_fwd_pass_twisted(u64 (&x)[S::E], int tid, const u64 *tw) {
   constexpr int lo = S::lo(Q), s0 = S::stage_begin(Q);
   const int b = tid >> lo;  // block at stage s0
@@ -308,35 +326,35 @@ __device__ __forceinline__ void ntt_fwd_pass_twisted(u64 (&x)[S::E], int tid, co
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const u64 u = x[k], v = x[k + 4];
-    x[k] = gl_add(u, v);
+    x[k] = k == 0 ? fwd_sum<W>(u, v) : gl_add(u, v);
     x[k + 4] = gl_sub(u, v);
   }
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     u64 u = x[k], v = x[k + 2];
-    x[k] = gl_add(u, v);
+    x[k] = k == 0 ? fwd_sum<W>(u, v) : gl_add(u, v);
     x[k + 2] = gl_sub(u, v);
     u = x[k + 4];
     v = gl_mul_pow2<48>(x[k + 6]);  // i
-    x[k + 4] = gl_add(u, v);
+    x[k + 4] = fwd_sum<W>(u, v);
     x[k + 6] = gl_sub(u, v);
   }
   {
     u64 u = x[0], v = x[1];
-    x[0] = gl_add(u, v);
+    x[0] = fwd_sum<W>(u, v);
     x[1] = gl_sub(u, v);
     u = x[2];
     v = gl_mul_pow2<48>(x[3]);  // i
-    x[2] = gl_add(u, v);
+    x[2] = fwd_sum<W>(u, v);
     x[3] = gl_sub(u, v);
     u = x[4];
     v = gl_mul_pow2<24>(x[5]);  // w = -2^24
     x[4] = gl_sub(u, v);
-    x[5] = gl_add(u, v);
+    x[5] = fwd_sum<W>(u, v);
     u = x[6];
     v = gl_mul_pow2<72>(x[7]);  // w^3 = -2^72
     x[6] = gl_sub(u, v);
-    x[7] = gl_add(u, v);
+    x[7] = fwd_sum<W>(u, v);
   }
 }
 
@@ -389,7 +407,7 @@ __device__ __forceinline__ void ntt_inv_pass_twisted(u64 (&x)[S::E], int tid, co
 // needs the nc = E / 2^(LOGN - s) consecutive blocks t nc .. t nc + nc - 1;
 // that stage's table region is stored slot-major there (block t nc + c at
 // 2^s + c T + t), so that a wave's reads of one slot are consecutive words.
-template <class S, int Q>
+template <class S, int Q, bool W = false>
 __device__ __forceinline__ void ntt_fwd_pass(u64 (&x)[S::E], int tid, const u64 *tw) {
   constexpr int lo = S::lo(Q);
   const int jt = S::idx(Q, tid, 0);
@@ -405,7 +423,7 @@ __device__ __forceinline__ void ntt_fwd_pass(u64 (&x)[S::E], int tid, const u64 
       const u64 w = lo == 0 ? zs[(k >> sh) * S::T] : zs[k >> (sh - lo)];
       const u64 t = gl_mul(x[k2], w);
       x[k2] = gl_sub(x[k], t);
-      x[k] = gl_add(x[k], t);
+      x[k] = fwd_sum<W>(x[k], t);
     }
   }
 }
@@ -492,18 +510,18 @@ __device__ __forceinline__ void ntt_exchange(u64 (&x)[S::E], LdsBufs<S> &lds, in
   }
 }
 
-template <class S, int Q>
+template <class S, int Q, bool W = false>
 __device__ __forceinline__ void ntt_fwd_from(u64 (&x)[S::E], LdsBufs<S> &lds, int tid,
                                              const u64 *tw) {
   if constexpr (Q == 0)
-    ntt_fwd_pass0<S, 0>(x);
+    ntt_fwd_pass0<S, 0, W>(x);
   else if constexpr (S::twisted(Q))
-    ntt_fwd_pass_twisted<S, Q>(x, tid, tw);
+    ntt_fwd_pass_twisted<S, Q, W>(x, tid, tw);
   else
-    ntt_fwd_pass<S, Q>(x, tid, tw);
+    ntt_fwd_pass<S, Q, W>(x, tid, tw);
   if constexpr (Q + 1 < S::PASSES) {
     ntt_exchange<S, Q, Q + 1>(x, lds, tid);
-    ntt_fwd_from<S, Q + 1>(x, lds, tid, tw);
+    ntt_fwd_from<S, Q + 1, W>(x, lds, tid, tw);
   }
 }
 
@@ -531,15 +549,17 @@ __device__ __forceinline__ void ntt_forward(u64 (&x)[S::E], LdsBufs<S> &lds, int
 }
 
 // Forward transform of a polynomial with small signed coefficients d
-// (|d| <= 2^13): stages 0 and 1 in integer arithmetic, then as ntt_forward.
+// (|d| <= 2^13): stages 0 and 1 in integer arithmetic, then as ntt_forward
+// in the weak form (fwd_sum): each output is below 2^64 and congruent to
+// the transform, for callers that only multiply it (gl_mul_add).
 template <class S, typename RT>
 __device__ __forceinline__ void ntt_forward_small(const RT (&d)[S::E], u64 (&x)[S::E],
                                                   LdsBufs<S> &lds, int tid, const u64 *tw) {
   ntt_fwd_stages01_small<S, RT>(d, x);
-  ntt_fwd_pass0<S, 2>(x);
+  ntt_fwd_pass0<S, 2, true>(x);
   if constexpr (S::PASSES > 1) {
     ntt_exchange<S, 0, 1>(x, lds, tid);
-    ntt_fwd_from<S, 1>(x, lds, tid, tw);
+    ntt_fwd_from<S, 1, true>(x, lds, tid, tw);
   }
 }
 

@@ -72,6 +72,24 @@ def test_field_binary_ops_exact(operands, op, name, ref):
                            for i in bad[:5]]
 
 
+def test_field_add_weak_contract(operands):
+    # first operand anywhere below 2^64 (the values at and above p included),
+    # second canonical: the result must be congruent to a + b mod p
+    _, b, _, _, _, _ = operands
+    high = [P, P + 1, P + 2, (1 << 64) - 1, (1 << 64) - 2, (1 << 64) - (1 << 32),
+            P + (1 << 31), (1 << 64) - 3]
+    rng = np.random.default_rng(11)
+    a = [high[i % len(high)] if i % 3 == 0 else int(x)
+         for i, x in enumerate(rng.integers(0, 1 << 64, size=len(b), dtype=np.uint64))]
+    bb = list(b)
+    bb[: len(high)] = [P - 1] * len(high)
+    say(f"[field] add_weak on {len(a)} pairs")
+    got = R.to_host(R.field_op(R.FIELD_ADD_WEAK, R.to_device(np.array(a, dtype=np.uint64)),
+                               R.to_device(np.array(bb, dtype=np.uint64))))
+    bad = [i for i in range(len(a)) if int(got[i]) % P != (a[i] + bb[i]) % P]
+    assert not bad, [(hex(a[i]), hex(bb[i]), hex(int(got[i]))) for i in bad[:5]]
+
+
 def test_field_pow2_every_exponent(operands):
     a, _, _, da, _, _ = operands
     say(f"[field] mul_pow2 e = 0..95 on {len(a)} values")
