@@ -4,6 +4,7 @@
 // in kernels.hip.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -127,31 +128,34 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
     const u64 psi = gl_pow(7, (GL_P - 1) / (2 * (u64)N));
     std::vector<u64> z(N);
     for (uint32_t m = 0; m < N; ++m) z[m] = gl_pow(psi, bitrev(m, logn));
-    // passes after the first that span three stages (N >= 512) run in
-    // twisted radix-8 form: their table region [2^s0, 2^(s0+3)) (the
-    // twiddles of stages s0..s0+2, read by no other pass) becomes the
-    // powers q^1..q^7 of q = zeta[4 (2^s0 + b)], 7 words per block b
-    // the last pass (threads own E consecutive indices), when it is not
-    // twisted: each of its stages s stores block t nc + c (nc = E / 2^(logn -
-    // s) blocks per thread, T = N / E threads) at 2^s + c T + t
+    // The pass structure of the kernels' transform (E = 2^le elements per
+    // thread, pass 0 spanning f stages, every later pass le: ntt_le and
+    // ntt_first).  Passes after the first that span three stages run in twisted
+    // radix-8 form: their table region [2^s0, 2^(s0+3)) (the twiddles of
+    // stages s0..s0+2, read by no other pass) becomes the powers q^1..q^7
+    // of q = zeta[4 (2^s0 + b)], 7 words per block b.  The last pass
+    // (threads own E consecutive indices), when it is not twisted: each of
+    // its stages s stores block t nc + c (nc = E / 2^(logn - s) blocks per
+    // thread, T = N / E threads) at 2^s + c T + t.
     {
-      const int le = logn == 8 ? 2 : 3;  // elements per thread E = 2^le, as dispatched
-      const int passes = (logn + le - 1) / le, s0 = (passes - 1) * le;
-      const bool last_twisted = le == 3 && logn - s0 == 3;
+      const int le = ntt_le(logn), f = ntt_first(logn);
+      std::vector<int> begin;  // first stage of each pass
+      for (int s = 0; s < logn; s += begin.size() == 1 ? f : le) begin.push_back(s);
+      const std::vector<u64> z0 = z;
+      const int s_last = begin.back();
+      const bool last_twisted = begin.size() > 1 && le == 3 && logn - s_last == 3;
       if (!last_twisted) {
         const uint32_t T = N >> le;
-        const std::vector<u64> z0 = z;
-        for (int s = s0; s < logn; ++s) {
+        for (int s = s_last; s < logn; ++s) {
           const uint32_t nc = (1u << le) >> (logn - s);
           for (uint32_t t = 0; t < T; ++t)
             for (uint32_t c = 0; c < nc; ++c) z[(1u << s) + c * T + t] = z0[(1u << s) + t * nc + c];
         }
       }
-    }
-    if (logn >= 9) {
-      const std::vector<u64> z0 = z;
-      for (int q = 1; 3 * q + 3 <= logn; ++q) {
-        const uint32_t nb = 1u << (3 * q);
+      for (size_t q = 1; q < begin.size(); ++q) {
+        const int s0 = begin[q];
+        if (le != 3 || std::min(logn, s0 + 3) - s0 != 3) continue;
+        const uint32_t nb = 1u << s0;
         for (uint32_t b = 0; b < nb; ++b) {
           const u64 qq = z0[4 * (nb + b)];
           u64 pw = qq;

@@ -15,11 +15,18 @@ namespace rosetta {
 // rotation amounts are staged in LDS).
 constexpr uint32_t MAX_LWE_N = 2048;
 
+// Shape of the transform the kernels use at N = 2^logn: E = 2^ntt_le(logn)
+// elements per thread, pass 0 spanning ntt_first(logn) stages and every
+// later pass ntt_le(logn) (Ntt in ntt.hpp).  The twiddle table (abi.cpp)
+// is laid out for exactly this shape.
+constexpr int ntt_le(int logn) { return logn == 8 ? 2 : 3; }
+constexpr int ntt_first(int logn) { return logn == 11 ? 2 : ntt_le(logn); }
+
 // Per-device, per-N transform tables (device pointers) and N^-1.
 struct Tables {
-  // zeta[m] = psi^rev(m) for m < N (zeta[0] = 1), followed by the radix-8
-  // powers q^3, q^5, q^6, q^7 (q = zeta[4m]) of every block m of each
-  // twisted pass (see ntt.hpp)
+  // N words: zeta[m] = psi^rev(m) (zeta[0] = 1), with the regions of the
+  // twisted passes holding their block powers and the stages of a last
+  // pass that is not twisted stored slot-major (see ntt.hpp)
   const uint64_t *zeta;
   uint64_t ninv;
 };

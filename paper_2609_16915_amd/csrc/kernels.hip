@@ -611,14 +611,14 @@ __global__ void k_lwe_sum_groups(const u64 *__restrict__ in, u64 *__restrict__ o
 // Launchers
 // ---------------------------------------------------------------------------
 
-#define ROSETTA_DISPATCH_N(LOGN_VAR, ...)                  \
-  switch (LOGN_VAR) {                                      \
-    case 8: { using S = Ntt<8, 2>; __VA_ARGS__; } break;   \
-    case 9: { using S = Ntt<9, 3>; __VA_ARGS__; } break;   \
-    case 10: { using S = Ntt<10, 3>; __VA_ARGS__; } break; \
-    case 11: { using S = Ntt<11, 3>; __VA_ARGS__; } break; \
-    case 12: { using S = Ntt<12, 3>; __VA_ARGS__; } break; \
-    default: return hipErrorInvalidValue;                  \
+#define ROSETTA_DISPATCH_N(LOGN_VAR, ...)                                             \
+  switch (LOGN_VAR) {                                                                 \
+    case 8: { using S = Ntt<8, ntt_le(8), ntt_first(8)>; __VA_ARGS__; } break;        \
+    case 9: { using S = Ntt<9, ntt_le(9), ntt_first(9)>; __VA_ARGS__; } break;        \
+    case 10: { using S = Ntt<10, ntt_le(10), ntt_first(10)>; __VA_ARGS__; } break;    \
+    case 11: { using S = Ntt<11, ntt_le(11), ntt_first(11)>; __VA_ARGS__; } break;    \
+    case 12: { using S = Ntt<12, ntt_le(12), ntt_first(12)>; __VA_ARGS__; } break;    \
+    default: return hipErrorInvalidValue;                                             \
   }
 
 static int ilog2(uint32_t N) {

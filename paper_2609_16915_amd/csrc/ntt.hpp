@@ -12,14 +12,16 @@
 // directions and the sign is absorbed by computing (v - u) * zeta instead of
 // (u - v) * zeta^-1.
 //
-// Stages are grouped into passes of LE stages.  During pass q a thread holds
-// the E elements whose index bits [lo_q, lo_q + LE) vary, lo_q =
-// max(0, LOGN - (q+1) LE); the thread id fills the remaining bits in order:
+// Stages are grouped into passes: pass 0 takes the first F <= LE stages, every
+// later pass the next LE (the last one what remains).  During pass q >= 1 a
+// thread holds the E elements whose index bits [lo_q, lo_q + LE) vary, lo_q =
+// max(0, LOGN - (end of the pass's stages)); the thread id fills the
+// remaining bits in order:
 //   j = (tid mod 2^lo) + (k << lo) + ((tid >> lo) << (lo + LE)).
+// Pass 0 is the natural layout j = tid + T*k (lo_0 = LOGN - LE).
 // Butterflies inside a pass are register-only; between passes the workgroup
 // transposes through LDS (one write, one barrier, one read), alternating
-// between two buffers so that one barrier per transpose suffices.  Pass 0
-// is the natural layout j = tid + T*k.
+// between two buffers so that one barrier per transpose suffices.
 //
 // LDS word addresses of the transposes go through a linear XOR swizzle
 // (bit b < 5 of the address is flipped by the parity of j & SWZ_MASK[b],
@@ -49,21 +51,23 @@ __host__ __device__ constexpr int swz(int j) {
   return a;
 }
 
-template <int LOGN_, int LE_>
+template <int LOGN_, int LE_, int F_ = LE_>
 struct Ntt {
+  static_assert(F_ >= 1 && F_ <= LE_, "the first pass spans 1..LE stages");
   static constexpr int LOGN = LOGN_;
   static constexpr int LE = LE_;
+  static constexpr int F = F_;  // stages of pass 0
   static constexpr int N = 1 << LOGN;
   static constexpr int E = 1 << LE;
   static constexpr int T = N / E;
-  static constexpr int PASSES = (LOGN + LE - 1) / LE;
+  static constexpr int PASSES = 1 + (LOGN - F + LE - 1) / LE;
 
-  __host__ __device__ static constexpr int lo(int q) {
-    return (LOGN - (q + 1) * LE) > 0 ? (LOGN - (q + 1) * LE) : 0;
-  }
-  __host__ __device__ static constexpr int stage_begin(int q) { return q * LE; }
+  __host__ __device__ static constexpr int stage_begin(int q) { return q == 0 ? 0 : F + (q - 1) * LE; }
   __host__ __device__ static constexpr int stage_end(int q) {
-    return (q + 1) * LE < LOGN ? (q + 1) * LE : LOGN;
+    return F + q * LE < LOGN ? F + q * LE : LOGN;
+  }
+  __host__ __device__ static constexpr int lo(int q) {
+    return q == 0 ? LOGN - LE : (LOGN - stage_end(q) > 0 ? LOGN - stage_end(q) : 0);
   }
   // index held by element k of thread tid during pass q
   __host__ __device__ static constexpr int idx(int q, int tid, int k) {
@@ -78,6 +82,14 @@ struct Ntt {
   // of a half wave on distinct LDS banks.
   __host__ __device__ static constexpr bool twisted(int q) {
     return q >= 1 && LE == 3 && stage_end(q) - stage_begin(q) == 3;
+  }
+  // A twisted pass whose first stage is s0 <= 2 has q = zeta[4 (2^s0 + b)]
+  // among the 64th roots of unity, which are powers of two; when, in
+  // addition, lo >= 6, the block b = tid >> lo is the wave's index, so the
+  // wave can branch (uniformly) to a copy of the pass in which the powers
+  // q^k are compile-time shifts instead of products.
+  __host__ __device__ static constexpr bool shift_twist(int q) {
+    return twisted(q) && stage_begin(q) <= 2 && lo(q) >= 6;
   }
   // words of the LDS twiddle area (the table above; the stages of a last
   // pass that is not twisted are stored slot-major, see ntt_fwd_pass)
@@ -128,6 +140,29 @@ __host__ __device__ constexpr bool small_root_negative() {
   return zeta_log2(M) >= 96;
 }
 
+// zeta[m] for m < 32 is a 64th root of unity: with 7^((p-1)/64) = 2^39 it
+// equals 2^(39 rev5(m) mod 192) for every N >= 32 (rev5 the 5-bit reversal;
+// below 8 this is zeta_log2).
+__host__ __device__ constexpr int rev5(int m) {
+  return ((m & 1) << 4) | ((m & 2) << 2) | (m & 4) | ((m >> 2) & 2) | ((m >> 4) & 1);
+}
+__host__ __device__ constexpr int zeta_log2_64(int m) { return (39 * rev5(m)) % 192; }
+__host__ __device__ constexpr bool zeta_logs_agree() {
+  for (int m = 0; m < 8; ++m)
+    if (zeta_log2_64(m) != zeta_log2(m)) return false;
+  return true;
+}
+static_assert(zeta_logs_agree(), "the two closed forms of the small roots disagree");
+
+// x * (+-2^E) for a compile-time E mod 192 (2^96 = -1): the magnitude as a
+// shift; the sign is the caller's (sign_pow2).
+template <int E>
+__device__ __forceinline__ u64 mul_pow2_mag(u64 x) {
+  return gl_mul_pow2<(E % 192 >= 96 ? E % 192 - 96 : E % 192)>(x);
+}
+__host__ __device__ constexpr int sign_pow2(int e) { return e % 192 >= 96 ? -1 : 1; }
+
+
 // Sums of the forward butterflies.  A weak forward transform (W) feeds only
 // products (the key multiply-accumulate), so its values need only stay below
 // 2^64 and congruent: a sum whose second operand is canonical (a product, a
@@ -140,6 +175,24 @@ __device__ __forceinline__ u64 fwd_sum(u64 a, u64 b) {
     return gl_add_weak(a, b);
   else
     return gl_add(a, b);
+}
+
+// Butterfly on signed operands A = SA a, B = SB b (signs known at compile
+// time, a and b the stored values): a <- A + B, b <- A - B, both returned
+// with the sign SA, which costs nothing: for SA != SB the sum and the
+// difference of the stored values trade places.  The subtrahend is always
+// b.  CF: the first result must be canonical (a and b canonical); a sum in
+// any other place may be weak (W, see fwd_sum).
+template <int SA, int SB, bool W, bool CF>
+__device__ __forceinline__ void signed_bfly(u64 &a, u64 &b) {
+  const u64 u = a, v = b;
+  if constexpr (SA == SB) {
+    a = CF ? gl_add(u, v) : fwd_sum<W>(u, v);
+    b = gl_sub(u, v);
+  } else {
+    a = gl_sub(u, v);
+    b = fwd_sum<W>(u, v);
+  }
 }
 
 // Pass 0 of the forward transform (all twiddles compile-time powers of
@@ -358,12 +411,17 @@ __device__ __forceinline__ void ntt_fwd_pass_twisted(u64 (&x)[S::E], int tid, co
   }
 }
 
-template <class S, int Q>
-__device__ __forceinline__ void ntt_inv_pass_twisted(u64 (&x)[S::E], int tid, const u64 *tw) {
-  constexpr int lo = S::lo(Q), s0 = S::stage_begin(Q);
-  const int br = (1 << s0) - 1 - (tid >> lo);  // reflected block
-  const u64 *qp = tw + (1 << s0) + 7 * br;  // powers of q_r = zeta[4 (2^s0 + br)]
-  u64 z[8] = {x[7], x[6], x[4], x[5], x[0], x[1], x[2], x[3]};
+// The 8-point inverse transform of a twisted inverse pass, on the inputs
+// rotated by one frequency (see ntt_fwd_pass_twisted), into z.
+__device__ __forceinline__ void ntt_inv_dft8(const u64 (&x)[8], u64 (&z)[8]) {
+  z[0] = x[7];
+  z[1] = x[6];
+  z[2] = x[4];
+  z[3] = x[5];
+  z[4] = x[0];
+  z[5] = x[1];
+  z[6] = x[2];
+  z[7] = x[3];
   {
     u64 u = z[0], v = z[1];
     z[0] = gl_add(u, v);
@@ -397,9 +455,102 @@ __device__ __forceinline__ void ntt_inv_pass_twisted(u64 (&x)[S::E], int tid, co
     z[k] = gl_add(u, v);
     z[k + 4] = gl_sub(u, v);
   }
+}
+
+template <class S, int Q>
+__device__ __forceinline__ void ntt_inv_pass_twisted(u64 (&x)[S::E], int tid, const u64 *tw) {
+  constexpr int lo = S::lo(Q), s0 = S::stage_begin(Q);
+  const int br = (1 << s0) - 1 - (tid >> lo);  // reflected block
+  const u64 *qp = tw + (1 << s0) + 7 * br;  // powers of q_r = zeta[4 (2^s0 + br)]
+  u64 z[8];
+  ntt_inv_dft8(x, z);
   x[0] = z[0];
 #pragma unroll
   for (int k = 1; k < 8; ++k) x[k] = gl_mul(z[k], qp[k - 1]);
+}
+
+// Twisted pass Q for the block B at its first stage when q = zeta[4 (2^s0 +
+// B)] is a power of two (Ntt::shift_twist): the twist y_k = q^k x_k is a
+// shift by |q^k|, and the signs of the q^k ride through the 8-point
+// transform in signed_bfly, so that every output leaves with the sign of
+// y_0 = x_0, positive, at no cost.  Weak and canonical sums sit where
+// ntt_fwd_pass_twisted has them (CF marks the canonical ones).
+template <class S, int Q, bool W, int B>
+__device__ __forceinline__ void ntt_fwd_pass_shift_twist(u64 (&x)[S::E]) {
+  constexpr int eq = zeta_log2_64(4 * ((1 << S::stage_begin(Q)) + B));
+  constexpr int s1 = sign_pow2(eq), s2 = sign_pow2(2 * eq), s3 = sign_pow2(3 * eq),
+                s4 = sign_pow2(4 * eq), s5 = sign_pow2(5 * eq), s6 = sign_pow2(6 * eq),
+                s7 = sign_pow2(7 * eq);
+  x[1] = mul_pow2_mag<eq>(x[1]);
+  x[2] = mul_pow2_mag<2 * eq>(x[2]);
+  x[3] = mul_pow2_mag<3 * eq>(x[3]);
+  x[4] = mul_pow2_mag<4 * eq>(x[4]);
+  x[5] = mul_pow2_mag<5 * eq>(x[5]);
+  x[6] = mul_pow2_mag<6 * eq>(x[6]);
+  x[7] = mul_pow2_mag<7 * eq>(x[7]);
+  // stage A; afterwards x[j] and x[j + 4] carry the sign of y_j
+  signed_bfly<1, s4, W, false>(x[0], x[4]);
+  signed_bfly<s1, s5, W, true>(x[1], x[5]);
+  signed_bfly<s2, s6, W, true>(x[2], x[6]);
+  signed_bfly<s3, s7, W, true>(x[3], x[7]);
+  // stage B (i = 2^48); afterwards x[0], x[2], x[4], x[6] are positive and
+  // x[1], x[3], x[5], x[7] carry s1
+  signed_bfly<1, s2, W, false>(x[0], x[2]);
+  signed_bfly<s1, s3, W, true>(x[1], x[3]);
+  x[6] = gl_mul_pow2<48>(x[6]);
+  signed_bfly<1, s2, W, false>(x[4], x[6]);
+  x[7] = gl_mul_pow2<48>(x[7]);
+  signed_bfly<s1, s3, W, false>(x[5], x[7]);
+  // stage C (i, w = -2^24, w^3 = -2^72)
+  signed_bfly<1, s1, W, false>(x[0], x[1]);
+  x[3] = gl_mul_pow2<48>(x[3]);
+  signed_bfly<1, s1, W, false>(x[2], x[3]);
+  x[5] = gl_mul_pow2<24>(x[5]);
+  signed_bfly<1, -s1, W, false>(x[4], x[5]);
+  x[7] = gl_mul_pow2<72>(x[7]);
+  signed_bfly<1, -s1, W, false>(x[6], x[7]);
+}
+
+// The inverse of ntt_fwd_pass_shift_twist for block B: the 8-point inverse
+// of ntt_inv_pass_twisted, then the untwist by the powers of q_r =
+// zeta[4 (2^s0 + 2^s0 - 1 - B)] as shifts, negated (gl_neg) where q_r^k is.
+template <class S, int Q, int B>
+__device__ __forceinline__ void ntt_inv_pass_shift_twist(u64 (&x)[S::E]) {
+  constexpr int s0 = S::stage_begin(Q);
+  constexpr int er = zeta_log2_64(4 * ((1 << s0) + (1 << s0) - 1 - B));
+  u64 z[8];
+  ntt_inv_dft8(x, z);
+  x[0] = z[0];
+  static_for<1, 8>([&](auto kc) {
+    constexpr int k = decltype(kc)::value;
+    const u64 r = mul_pow2_mag<k * er>(z[k]);
+    x[k] = sign_pow2(k * er) < 0 ? gl_neg(r) : r;
+  });
+}
+
+// Dispatch of a shift-twisted pass to the copy of the wave's block b
+// (wave-uniform, so the branches are scalar).
+template <class S, int Q, bool W, int B = 0>
+__device__ __forceinline__ void ntt_fwd_shift_twist_block(u64 (&x)[S::E], int b) {
+  if constexpr (B + 1 < (1 << S::stage_begin(Q))) {
+    if (b == B)
+      ntt_fwd_pass_shift_twist<S, Q, W, B>(x);
+    else
+      ntt_fwd_shift_twist_block<S, Q, W, B + 1>(x, b);
+  } else {
+    ntt_fwd_pass_shift_twist<S, Q, W, B>(x);
+  }
+}
+template <class S, int Q, int B = 0>
+__device__ __forceinline__ void ntt_inv_shift_twist_block(u64 (&x)[S::E], int b) {
+  if constexpr (B + 1 < (1 << S::stage_begin(Q))) {
+    if (b == B)
+      ntt_inv_pass_shift_twist<S, Q, B>(x);
+    else
+      ntt_inv_shift_twist_block<S, Q, B + 1>(x, b);
+  } else {
+    ntt_inv_pass_shift_twist<S, Q, B>(x);
+  }
 }
 
 // Forward stages of pass Q; `tw` is the LDS twiddle table.  In the last
@@ -515,6 +666,8 @@ __device__ __forceinline__ void ntt_fwd_from(u64 (&x)[S::E], LdsBufs<S> &lds, in
                                              const u64 *tw) {
   if constexpr (Q == 0)
     ntt_fwd_pass0<S, 0, W>(x);
+  else if constexpr (S::shift_twist(Q))
+    ntt_fwd_shift_twist_block<S, Q, W>(x, __builtin_amdgcn_readfirstlane(tid >> S::lo(Q)));
   else if constexpr (S::twisted(Q))
     ntt_fwd_pass_twisted<S, Q, W>(x, tid, tw);
   else
@@ -530,6 +683,8 @@ __device__ __forceinline__ void ntt_inv_from(u64 (&x)[S::E], LdsBufs<S> &lds, in
                                              const u64 *tw) {
   if constexpr (Q == 0)
     ntt_inv_pass0<S>(x);
+  else if constexpr (S::shift_twist(Q))
+    ntt_inv_shift_twist_block<S, Q>(x, __builtin_amdgcn_readfirstlane(tid >> S::lo(Q)));
   else if constexpr (S::twisted(Q))
     ntt_inv_pass_twisted<S, Q>(x, tid, tw);
   else
