@@ -91,8 +91,10 @@ struct Ntt {
   __host__ __device__ static constexpr bool shift_twist(int q) {
     return twisted(q) && stage_begin(q) <= 2 && lo(q) >= 6;
   }
-  // words of the LDS twiddle area (the table above; the stages of a last
-  // pass that is not twisted are stored slot-major, see ntt_fwd_pass)
+  // words of the LDS twiddle area (the table above, with the regions of the
+  // twisted passes as described there and the stages of a last pass that is
+  // not twisted stored slot-major, see ntt_fwd_pass; the shift-twisted
+  // passes read none of it)
   static constexpr int TW_WORDS = N;
   // In pass q each wave (64 threads) holds one contiguous block of
   // 2^(6+LE) indices when lo(q) <= 6 (the wave id then sets the top index
@@ -122,7 +124,7 @@ __device__ __forceinline__ void static_for(F &&f) {
 
 // zeta[m] for m < 8 is a 16th root of unity, and with psi = 7^((p-1)/2N)
 // it equals 2^((156 * rev3(m)) mod 192) for every N, 7^((p-1)/16) being
-// 2^156.  Pass 0 (stages 0..LE-1 <= 2) uses only these, so its twiddle
+// 2^156.  Pass 0 (stages 0..F-1, F <= 3) uses only these, so its twiddle
 // products are shifts (gl_mul_pow2) and need no table.
 __host__ __device__ constexpr int rev3(int m) {
   return ((m & 1) << 2) | (m & 2) | ((m >> 2) & 1);
