@@ -195,6 +195,9 @@ rosetta_status rosetta_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *
  *   ROSETTA_FIELD_ADD_WEAK a + b for any a < 2^64 and canonical b, as the
  *       digit transforms of the blind rotation add: a result below 2^64 and
  *       congruent to a + b mod p, not necessarily canonical
+ *   ROSETTA_FIELD_MUL_ADD_WEAK  a * b + c for any a, c < 2^64 and canonical
+ *       b, as the blind rotation's key multiply-accumulate runs: below 2^64
+ *       and congruent, not necessarily canonical
  *   ROSETTA_FIELD_MUL_POW2 + e   a * 2^e   (0 <= e < 96; 2^96 = -1 mod p)
  *   ROSETTA_FIELD_ROUND_TOP + s  (1 <= s <= 63) the rounding that opens the
  *       gadget decomposition of the blind rotation (Sec. 2.2, PBS
@@ -212,6 +215,7 @@ enum {
   ROSETTA_FIELD_MUL = 2,
   ROSETTA_FIELD_MUL_ADD = 3,
   ROSETTA_FIELD_ADD_WEAK = 4,
+  ROSETTA_FIELD_MUL_ADD_WEAK = 5,
   ROSETTA_FIELD_MUL_POW2 = 256,
   ROSETTA_FIELD_ROUND_TOP = 512
 };

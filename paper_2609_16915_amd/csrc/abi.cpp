@@ -440,10 +440,11 @@ rosetta_status rosetta_field_op(int op, const uint64_t *a, const uint64_t *b, co
   const bool pow2 = op >= ROSETTA_FIELD_MUL_POW2 && op < ROSETTA_FIELD_MUL_POW2 + 96;
   const bool round = op > ROSETTA_FIELD_ROUND_TOP && op < ROSETTA_FIELD_ROUND_TOP + 64;
   const bool unary = pow2 || round;
-  if (!unary && (op < ROSETTA_FIELD_ADD || op > ROSETTA_FIELD_ADD_WEAK))
+  if (!unary && (op < ROSETTA_FIELD_ADD || op > ROSETTA_FIELD_MUL_ADD_WEAK))
     return fail(ROSETTA_ERR_PARAMS, "unknown field op %d", op);
   if (count == 0) return ok();
-  if (!a || !out || (!unary && !b) || (op == ROSETTA_FIELD_MUL_ADD && !c))
+  const bool reads_c = op == ROSETTA_FIELD_MUL_ADD || op == ROSETTA_FIELD_MUL_ADD_WEAK;
+  if (!a || !out || (!unary && !b) || (reads_c && !c))
     return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
   hipError_t e = launch_field_op(op, a, b, c, out, count, (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "field_op launch");

@@ -218,6 +218,9 @@ __device__ __forceinline__ u64 sub_eps_if(u64 d, u64 m) {
 // conditional EPS covers "carry or R >= p".  (The borrow correction keeps
 // the select form: sub_eps_if is one instruction shorter but puts a scalar
 // step on the product's dependent chain, which cost more than it saved.)
+// With CANON false only the carry is corrected: the result is below 2^64
+// and congruent, not necessarily below p.
+template <bool CANON = true>
 __device__ __forceinline__ u64 gl_reduce_dev(u32 c0, u32 c1, u32 c2, u32 c3) {
   u64 b0, b1, b2, b3;
   const u32 d0 = isa::sub_c(c0, c3, b0);
@@ -227,7 +230,10 @@ __device__ __forceinline__ u64 gl_reduce_dev(u32 c0, u32 c1, u32 c2, u32 c3) {
   const u32 t1 = isa::dec_bc(d1, b2, b3);
   u64 ca;
   const u64 R = isa::mad_eps_c(c2, gl_mk(t0, t1), ca);
-  return isa::add_eps_if(R, ca | isa::ge_p(R));
+  if constexpr (CANON)
+    return isa::add_eps_if(R, ca | isa::ge_p(R));
+  else
+    return isa::add_eps_if(R, ca);
 }
 
 // a b as limbs: M = a1 b0, S = a0 b1 + M (65 bits: carry cs),
@@ -248,7 +254,9 @@ __device__ __forceinline__ u64 gl_mul_dev(u64 a, u64 b) {
 }
 
 // a b + c: c enters the multiply-add of P0 (carry cc at weight 2^64, added
-// to c2 with its own carry into c3).
+// to c2 with its own carry into c3).  Any a, c < 2^64 with canonical b keep
+// a b + c below 2^128; CANON false leaves the result weak (gl_reduce_dev).
+template <bool CANON = true>
 __device__ __forceinline__ u64 gl_mul_add_dev(u64 a, u64 b, u64 c) {
   const u32 a0 = (u32)a, a1 = (u32)(a >> 32), b0 = (u32)b, b1 = (u32)(b >> 32);
   u64 cs, cc;
@@ -260,7 +268,7 @@ __device__ __forceinline__ u64 gl_mul_add_dev(u64 a, u64 b, u64 c) {
   const u32 c2a = isa::addc_c((u32)P1, (u32)(S >> 32), kc, kd);
   const u32 c2 = isa::addc_c(c2a, 0u, cc, ke);
   const u32 c3 = isa::inc_ci(isa::inc_ci(isa::inc_ci((u32)(P1 >> 32), kd), cs), ke);
-  return gl_reduce_dev((u32)P0, c1, c2, c3);
+  return gl_reduce_dev<CANON>((u32)P0, c1, c2, c3);
 }
 
 // x 2^E for 0 < E <= 32 as lo64 + c2 2^64 = lo64 + c2 EPS, c2 < 2^E; with
@@ -396,6 +404,27 @@ __host__ __device__ __forceinline__ u64 gl_mul_add(u64 a, u64 b, u64 c) {
   const u64 p10 = (u64)a1 * b0 + (u32)p01;
   const u64 p11 = (u64)a1 * b1 + ((p01 >> 32) + (p10 >> 32));
   return gl_reduce_limbs((u32)p00, (u32)p10, (u32)p11, (u32)(p11 >> 32));
+}
+
+// a b + c up to a multiple of p, for any a, c < 2^64 and canonical b: below
+// 2^64 and congruent (the running sums of the key multiply-accumulate,
+// which only feed further such sums until gl_canon).
+__host__ __device__ __forceinline__ u64 gl_mul_add_weak(u64 a, u64 b, u64 c) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return gl_mul_add_dev<false>(a, b, c);
+#else
+  return gl_mul_add(a, b, c);
+#endif
+}
+
+// The canonical representative of any x < 2^64 (x - p = x + EPS mod 2^64
+// when x >= p).
+__host__ __device__ __forceinline__ u64 gl_canon(u64 x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return isa::add_eps_if(x, isa::ge_p(x));
+#else
+  return x >= GL_P ? x - GL_P : x;
+#endif
 }
 
 __host__ __device__ inline u64 gl_pow(u64 a, u64 e) {

@@ -299,10 +299,11 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
             g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
           }
         }
+        // (running sums weak until the inverse transform takes them)
 #pragma unroll
         for (int k = 0; k < E; ++k) {
-          Y0[k] = gl_mul_add(x[k], g0[k], Y0[k]);
-          Y1[k] = gl_mul_add(x[k], g1[k], Y1[k]);
+          Y0[k] = gl_mul_add_weak(x[k], g0[k], Y0[k]);
+          Y1[k] = gl_mul_add_weak(x[k], g1[k], Y1[k]);
         }
       }
     }
@@ -312,7 +313,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
     for (int c = 0; c < 2; ++c) {
       u64 y[E];
 #pragma unroll
-      for (int k = 0; k < E; ++k) y[k] = c ? Y1[k] : Y0[k];
+      for (int k = 0; k < E; ++k) y[k] = gl_canon(c ? Y1[k] : Y0[k]);
       ntt_inverse<S>(y, lds, tid, tw);
 #pragma unroll
       for (int k = 0; k < E; ++k) {
@@ -458,15 +459,15 @@ k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restric
       gconst_u64 *g = G + (size_t)(t * 2) * N;
 #pragma unroll
       for (int k = 0; k < E; ++k) {
-        Y0[k] = gl_mul_add(x[k], g[k * T], Y0[k]);
-        Y1[k] = gl_mul_add(x[k], g[N + k * T], Y1[k]);
+        Y0[k] = gl_mul_add_weak(x[k], g[k * T], Y0[k]);
+        Y1[k] = gl_mul_add_weak(x[k], g[N + k * T], Y1[k]);
       }
     }
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       u64 y[E];
 #pragma unroll
-      for (int k = 0; k < E; ++k) y[k] = c ? Y1[k] : Y0[k];
+      for (int k = 0; k < E; ++k) y[k] = gl_canon(c ? Y1[k] : Y0[k]);
       ntt_inverse<S>(y, lds, tid, tw);
 #pragma unroll
       for (int k = 0; k < E; ++k) {
@@ -808,6 +809,8 @@ k_field_op(const u64 *__restrict__ a, const u64 *__restrict__ b, const u64 *__re
     out[i] = gl_mul_add(a[i], b[i], c[i]);
   } else if constexpr (OP == ROSETTA_FIELD_ADD_WEAK) {
     out[i] = gl_add_weak(a[i], b[i]);
+  } else if constexpr (OP == ROSETTA_FIELD_MUL_ADD_WEAK) {
+    out[i] = gl_mul_add_weak(a[i], b[i], c[i]);
   } else {
     out[i] = gl_mul_pow2<OP - ROSETTA_FIELD_MUL_POW2>(a[i]);
   }
@@ -859,6 +862,10 @@ hipError_t launch_field_op(int op, const uint64_t *a, const uint64_t *b, const u
     case ROSETTA_FIELD_ADD_WEAK:
       hipLaunchKernelGGL(k_field_op<ROSETTA_FIELD_ADD_WEAK>, grid, dim3(256), 0, st, a, b, c,
                          out, count);
+      break;
+    case ROSETTA_FIELD_MUL_ADD_WEAK:
+      hipLaunchKernelGGL(k_field_op<ROSETTA_FIELD_MUL_ADD_WEAK>, grid, dim3(256), 0, st, a, b,
+                         c, out, count);
       break;
     default:
       if (op > ROSETTA_FIELD_ROUND_TOP && op < ROSETTA_FIELD_ROUND_TOP + 64) {

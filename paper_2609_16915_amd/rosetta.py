@@ -328,14 +328,14 @@ def poly_mul(a, b, N: int, out=None, stream=None):
 
 
 FIELD_ADD, FIELD_SUB, FIELD_MUL, FIELD_MUL_ADD, FIELD_ADD_WEAK = 0, 1, 2, 3, 4
-FIELD_MUL_POW2, FIELD_ROUND_TOP = 256, 512
+FIELD_MUL_ADD_WEAK, FIELD_MUL_POW2, FIELD_ROUND_TOP = 5, 256, 512
 
 
 def field_op(op: int, a, b=None, c=None, out=None, stream=None):
     """Elementwise Goldilocks arithmetic with the kernels' device routines
     (op: FIELD_ADD, FIELD_SUB, FIELD_MUL, FIELD_MUL_ADD, FIELD_ADD_WEAK,
-    FIELD_MUL_POW2 + e, FIELD_ROUND_TOP + s; the last returns int64 values
-    as uint64)."""
+    FIELD_MUL_ADD_WEAK, FIELD_MUL_POW2 + e, FIELD_ROUND_TOP + s; the last
+    returns int64 values as uint64)."""
     count = a.numel()
     out = empty(a.shape, a.device) if out is None else out
     _check(lib().rosetta_field_op(op, _dev(a, "a"), None if b is None else _dev(b, "b"),

@@ -78,8 +78,9 @@ def test_null_and_empty_batches_touch_no_device(L):
     assert L.rosetta_ntt_forward(fake, fake, 2, 100, None) == 3
     assert L.rosetta_check_params(None) == 1
     # field ops: unknown op, missing operands, empty
-    assert L.rosetta_field_op(5, fake, fake, fake, fake, 2, None) == 2
+    assert L.rosetta_field_op(6, fake, fake, fake, fake, 2, None) == 2
     assert L.rosetta_field_op(4, fake, None, None, fake, 2, None) == 1
+    assert L.rosetta_field_op(5, fake, fake, None, fake, 2, None) == 1
     assert L.rosetta_field_op(256 + 96, fake, None, None, fake, 2, None) == 2
     assert L.rosetta_field_op(-1, fake, fake, fake, fake, 2, None) == 2
     assert L.rosetta_field_op(2, fake, None, None, fake, 2, None) == 1

@@ -90,6 +90,26 @@ def test_field_add_weak_contract(operands):
     assert not bad, [(hex(a[i]), hex(bb[i]), hex(int(got[i]))) for i in bad[:5]]
 
 
+def test_field_mul_add_weak_contract(operands):
+    # first factor and addend anywhere below 2^64, second factor canonical:
+    # the result must be congruent to a * b + c mod p
+    _, b, _, _, _, _ = operands
+    high = [P, P + 1, (1 << 64) - 1, (1 << 64) - (1 << 32), P + (1 << 31)]
+    rng = np.random.default_rng(13)
+    n = len(b)
+    a = [high[i % len(high)] if i % 4 == 0 else int(x)
+         for i, x in enumerate(rng.integers(0, 1 << 64, size=n, dtype=np.uint64))]
+    c = [high[i % len(high)] if i % 3 == 0 else int(x)
+         for i, x in enumerate(rng.integers(0, 1 << 64, size=n, dtype=np.uint64))]
+    bb = list(b)
+    bb[: len(high)] = [P - 1] * len(high)
+    say(f"[field] mul_add_weak on {n} triples")
+    to = lambda xs: R.to_device(np.array(xs, dtype=np.uint64))
+    got = R.to_host(R.field_op(R.FIELD_MUL_ADD_WEAK, to(a), to(bb), to(c)))
+    bad = [i for i in range(n) if int(got[i]) % P != (a[i] * bb[i] + c[i]) % P]
+    assert not bad, [(hex(a[i]), hex(bb[i]), hex(c[i]), hex(int(got[i]))) for i in bad[:5]]
+
+
 def test_field_pow2_every_exponent(operands):
     a, _, _, da, _, _ = operands
     say(f"[field] mul_pow2 e = 0..95 on {len(a)} values")
