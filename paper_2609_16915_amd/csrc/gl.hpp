@@ -2,11 +2,15 @@
 //
 // 2^64 = 2^32 - 1 (mod p), so a 128-bit value hi*2^64 + lo with
 // hi = h1*2^32 + h0 reduces to lo - h1 + h0*(2^32 - 1)  (since 2^96 = -1).
-// All functions take and return canonical values in [0, p).  The 64x64
-// product is built from four 32x32+64-bit multiply-adds.  On the device the
-// products, the multiply-accumulate and the power-of-two products use the
-// carry-out of v_mad_u64_u32 (see the gfx950 section below); the host
-// compiles the portable forms.
+// Functions take and return canonical values in [0, p) unless stated: the
+// products and power-of-two products accept any 64-bit input, and the
+// "weak" forms (gl_add_weak, gl_mul_add_weak) return a value below 2^64
+// that is only congruent, for chains that end in a product or in gl_canon.
+// The 64x64 product is built from four 32x32+64-bit multiply-adds.  On the
+// device the products, the multiply-accumulate, the power-of-two products
+// and the subtraction use the carry-out of v_mad_u64_u32 and explicit
+// carry chains (see the gfx950 section below); the host compiles the
+// portable forms.
 #pragma once
 
 #include <hip/hip_runtime.h>
