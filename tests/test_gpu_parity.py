@@ -201,6 +201,13 @@ CORNERS = {
                          msg_bits=3),
     "l3_b14_N256": dict(n=12, N=256, pbs_level=3, pbs_base_log=14, ks_level=3, ks_base_log=4,
                         msg_bits=2),
+    # the headline ring (two-stage first pass, shift-twisted second pass) with
+    # the general first stages (beta > 14) and a 64-bit rounded value
+    "l2_b16_N2048": dict(n=16, N=2048, pbs_level=2, pbs_base_log=16, ks_level=3, ks_base_log=6,
+                         msg_bits=2),
+    # the headline ring with the largest small digits and a 64-bit rounded value
+    "l3_b14_N2048": dict(n=12, N=2048, pbs_level=3, pbs_base_log=14, ks_level=3, ks_base_log=6,
+                         msg_bits=2),
 }
 
 
