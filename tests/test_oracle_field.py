@@ -66,6 +66,24 @@ def test_seven_generates_and_roots(O):
     assert w64 in {pow(8, e, P) for e in range(1, 64, 2)}
 
 
+def _rev(x, bits):
+    return int(format(x, f"0{bits}b")[::-1], 2)
+
+
+@pytest.mark.parametrize("logn", [8, 10, 11, 12])
+def test_small_twiddles_are_powers_of_two(O, logn):
+    # The transforms replace their first twiddles by shifts: zeta[m] =
+    # psi^rev(m) equals 2^(156 rev3(m) mod 192) for m < 8 and 2^(39 rev5(m)
+    # mod 192) for m < 32, at every N (7^((p-1)/16) = 2^156, 7^((p-1)/64) =
+    # 2^39), with psi the oracle's primitive 2N-th root.
+    psi = O.root_2n(1 << logn)
+    for m in range(32):
+        z = O.pow_(psi, _rev(m, logn))
+        assert z == pow(2, (39 * _rev(m, 5)) % 192, P), m
+        if m < 8:
+            assert z == pow(2, (156 * _rev(m, 3)) % 192, P), m
+
+
 # ----------------------------------------------------------------- ring ---
 
 def horner(coeffs, z):
