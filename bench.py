@@ -352,8 +352,8 @@ def main():
     hbm_bytes = (w.bsk_words() + w.ksk_words()) * 8 + w.batch * 2 * (w.n + 1) * 8 + w.N * 8
 
     result = {
-        "metric": "PBS/s (bootstraps per second) at N=2048, batch 14336; roofline fraction "
-                  "of the blind-rotation kernel",
+        "metric": f"PBS/sec (bootstraps/s) at N={w.N} batch {w.batch}; "
+                  "% of int64-VALU / HBM roofline",
         "value": round(value, 2), "unit": "PBS/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3),
         "ms_per_step_events": {"median": round(float(np.median(step_ms)), 3),
