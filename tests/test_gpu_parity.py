@@ -44,6 +44,29 @@ def test_ntt_forward_inverse_vs_oracle(O, torch_dev, N):
     assert np.array_equal(R.to_host(t), fwd)
 
 
+@pytest.mark.parametrize("N", [256, 1024, 2048, 4096])
+def test_ntt_edge_inputs_vs_oracle(O, torch_dev, N):
+    # structured inputs whose butterflies meet 0, p - 1 and equal operands:
+    # constants, single spikes at the block boundaries of each pass, and
+    # alternating extremes
+    rows = [[0] * N, [P - 1] * N, [1] * N]
+    for j in (0, 1, N // 8, N // 2 - 1, N // 2, N - 1):
+        r = [0] * N
+        r[j] = P - 1
+        rows.append(r)
+    rows.append([P - 1 if j % 2 else 0 for j in range(N)])
+    rows.append([(P - 1) // 2 + (j % 3) for j in range(N)])
+    a = np.array(rows, dtype=np.uint64)
+    assert int(a[1, 0]) == P - 1
+    say(f"[ntt edges] N={N} rows={len(rows)}")
+    fwd = R.to_host(R.ntt_forward(R.to_device(a), N))
+    L = N.bit_length() - 1
+    perm = np.array([bitrev(j, L) for j in range(N)])
+    for c in range(a.shape[0]):
+        assert np.array_equal(fwd[c], O.ntt_forward(a[c])[perm]), c
+    assert np.array_equal(R.to_host(R.ntt_inverse(R.to_device(fwd), N)), a)
+
+
 @pytest.mark.parametrize("N", [256, 512, 2048, 4096])
 def test_poly_mul_vs_oracle(O, torch_dev, N):
     rng = np.random.default_rng(100 + N)
