@@ -99,8 +99,13 @@ const char *rosetta_last_error(void);
 rosetta_status rosetta_check_params(const rosetta_params *params);
 
 /* Sizes in 64-bit words.  The standard and the device (prepared) layouts of
- * the bootstrapping key have the same size, n*2*l*2*N.  The prepared
- * key-switching key holds the N*l_ks*(n+1) key words plus n+1 column sums. */
+ * the bootstrapping key have the same size, n*2*l*2*N.  The standard
+ * key-switching key is N*l_ks*(n+1) words.  Its prepared layout depends on
+ * the parameters: where the key switch runs on the int8 matrix cores
+ * (beta_ks <= 7, l_ks*beta_ks <= 30, N a multiple of 32 and
+ * N*l_ks*2^(beta_ks-1)*128 < 2^31) it is the key's 8 signed byte planes,
+ * ceil((n+1)/32) * (N*l_ks/32) * 1024 words; otherwise the key words plus
+ * n+1 column sums. */
 size_t rosetta_bsk_words(const rosetta_params *params);
 size_t rosetta_ksk_words(const rosetta_params *params);
 size_t rosetta_ksk_device_words(const rosetta_params *params);
@@ -113,9 +118,12 @@ size_t rosetta_ksk_device_words(const rosetta_params *params);
 rosetta_status rosetta_bsk_prepare(const uint64_t *bsk_std_dev, uint64_t *bsk_dev,
                                    const rosetta_params *params, void *stream);
 
-/* Key-switching-key preparation: copies the standard layout into `ksk_dev`
- * (rosetta_ksk_device_words words, device, must not overlap) and appends the
- * column sums used by the key-switch kernel. */
+/* Key-switching-key preparation (once per key, not part of a PBS): writes the prepared layout of the standard key `ksk_std_dev` into
+ * `ksk_dev` (rosetta_ksk_device_words words, device, must not overlap):
+ * the signed byte planes of every key word (each word w replaced by w or
+ * w - p, whichever 8 balanced base-256 digits represent) in the operand
+ * order of the matrix-core kernel, or the key copied with its column sums
+ * appended for the VALU kernel. */
 rosetta_status rosetta_ksk_prepare(const uint64_t *ksk_std_dev, uint64_t *ksk_dev,
                                    const rosetta_params *params, void *stream);
 

@@ -248,7 +248,8 @@ size_t rosetta_ksk_words(const rosetta_params *p) {
 }
 
 size_t rosetta_ksk_device_words(const rosetta_params *p) {
-  return p ? rosetta_ksk_words(p) + (p->n + 1) : 0;
+  if (!p) return 0;
+  return ks_on_matrix_cores(*p) ? ks_matrix_key_words(*p) : rosetta_ksk_words(p) + (p->n + 1);
 }
 
 rosetta_status rosetta_bsk_prepare(const uint64_t *bsk_std_dev, uint64_t *bsk_dev,

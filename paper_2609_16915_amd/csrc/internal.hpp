@@ -80,6 +80,25 @@ hipError_t launch_modmul_chain(uint64_t seed, uint32_t threads, uint32_t iters, 
                                hipStream_t st);
 hipError_t launch_keyswitch(const uint64_t *big, const uint64_t *ksk_dev, uint64_t *out,
                             size_t batch, const rosetta_params &p, hipStream_t st);
+
+// The key switch is one integer matrix product over the batch (digits x
+// key), run on the int8 matrix cores when the signed digits fit a byte
+// (|d| <= 2^(beta_ks-1) <= 64), the rounded value 31 bits (l_ks beta_ks
+// <= 30), N is a multiple of 32 (whole 32-deep k blocks), and no int32 sum
+// of N l_ks digit x key-byte products can overflow (N l_ks 2^(beta_ks-1)
+// 128 < 2^31).  Otherwise the VALU kernel runs.  The prepared key's layout
+// follows the choice (launch_ksk_prepare).
+inline bool ks_on_matrix_cores(const rosetta_params &p) {
+  if (p.ks_base_log < 1 || p.ks_base_log > 7 || p.ks_level < 1) return false;
+  if (p.ks_level * p.ks_base_log > 30 || p.N % 32 != 0) return false;
+  const uint64_t bound = (uint64_t)p.N * p.ks_level * (1ull << (p.ks_base_log - 1)) * 128;
+  return bound < (1ull << 31);
+}
+// Words of the byte-plane key: ceil((n+1)/32) column blocks x N l_ks / 32
+// k blocks x 1024 words (16 operand fragments of 64 lanes x 8 bytes).
+inline size_t ks_matrix_key_words(const rosetta_params &p) {
+  return (size_t)((p.n + 1 + 31) / 32) * ((size_t)p.N * p.ks_level / 32) * 1024;
+}
 hipError_t launch_ntt(const uint64_t *in, uint64_t *out, size_t count, uint32_t N,
                       const Tables &tb, bool inverse, hipStream_t st);
 hipError_t launch_poly_mul(const uint64_t *a, const uint64_t *b, uint64_t *c, size_t count,

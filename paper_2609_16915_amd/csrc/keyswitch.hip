@@ -108,6 +108,167 @@ k_keyswitch(const u64 *__restrict__ big, const u64 *__restrict__ ksk, u64 *__res
 }
 
 // ---------------------------------------------------------------------------
+// Key switching on the int8 matrix cores
+// ---------------------------------------------------------------------------
+
+// Over a batch the key switch is one integer matrix product: digits
+// D[b][kappa] (batch x N l_ks) times key K[kappa][c] ((N l_ks) x (n+1)),
+// kappa = t N + j for digit level t of input coefficient j (any order of
+// the contraction index gives the same sum).  Each key word K in [0, p) is
+// replaced by V = K or K - p, whichever lies in the range of 8 balanced
+// base-256 digits [-128 S, 127 S], S = (2^64 - 1) / 255; V = sum_m 256^m k_m
+// with k_m in [-128, 127], so D K = sum_m 256^m (D k_m) (mod p) with eight
+// exact int8 x int8 -> int32 products.  X = V + 128 S lies in [0, 2^64) and
+// its plain base-256 digits are k_m + 128, so byte m of X with its top bit
+// flipped is k_m as a signed byte; X is K + 128 S, plus 2^32 - 1 (= -p mod
+// 2^64) when V = K - p.
+//
+// Byte-plane layout, in 8-byte words: word ((cb KB + kb) 16 + 2 m + cc) 64
+// + lane holds, in byte i, k_m[kappa][c] with kappa = 32 kb + 8 (lane / 16)
+// + i and c = 32 cb + 16 cc + lane % 16 (0 past the last column): exactly
+// the B operand of a 16 x 16 x 32 int8 product (lane l supplies rows
+// 8 (l / 16) .. + 7 of column l % 16) for the column tile cc of column
+// block cb, plane m, k block kb (KB = N l_ks / 32 of them).
+constexpr u64 KS_S128 = 0x8080808080808080ull;   // 128 S
+constexpr u64 KS_S127 = 0x7F7F7F7F7F7F7F7Full;   // 127 S
+
+__global__ void k_ksk_planes(const u64 *__restrict__ ksk, u64 *__restrict__ planes, int N,
+                             int lks, int cols, size_t words) {
+  const size_t w = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (w >= words) return;
+  const int lane = (int)(w & 63);
+  const size_t f = w >> 6;                 // (cb KB + kb) 16 + 2 m + cc
+  const int cc = (int)(f & 1), m = (int)((f >> 1) & 7);
+  const size_t blk = f >> 4;               // cb KB + kb
+  const size_t KB = (size_t)N * lks / 32;
+  const int kb = (int)(blk % KB), cb = (int)(blk / KB);
+  const int c = 32 * cb + 16 * cc + lane % 16;
+  u64 word = 0;
+  for (int i = 0; i < 8; ++i) {
+    const int kappa = 32 * kb + 8 * (lane / 16) + i;
+    const int t = kappa / N, j = kappa % N;
+    const u64 K = c < cols ? ksk[((size_t)j * lks + t) * cols + c] : 0;
+    const u64 X = K + KS_S128 + (K <= KS_S127 ? 0 : GL_EPS);
+    word |= (((X >> (8 * m)) & 0xFF) ^ 0x80) << (8 * i);
+  }
+  planes[w] = word;
+}
+
+typedef int32_t ks_v4i __attribute__((ext_vector_type(4)));
+
+// out[b][c] = (c == n ? b'_b : 0) - sum_kappa D[b][kappa] K[kappa][c].
+// Workgroup = 4 waves on one 32-column block (the same key fragments,
+// shared through the cache), each wave on its own 32 ciphertexts: two
+// 16-ciphertext row tiles x two 16-column tiles x 8 byte planes of int32
+// accumulators.  Per 32 input coefficients a lane rounds its 8 coefficients
+// of each row tile and peels their l_ks balanced digits from the bottom
+// (the A operand of level t: row l % 16, coefficients 8 (l / 16) .. + 7);
+// each level is 32 products.  The planes are recombined exactly: with
+// |acc| < 2^31, lo = sum_{m<4} 256^m acc_m and hi = sum_{m>=4} 256^(m-4)
+// acc_m are below 2^56 in magnitude, and the sum is lo + 2^32 hi mod p.
+// No barriers: a wave with no ciphertexts exits at once (every column
+// block holds at least one column).
+constexpr int KSM_WAVES = 4;
+
+template <int LKS>
+__global__ void __launch_bounds__(64 * KSM_WAVES) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_keyswitch_mfma(const u64 *__restrict__ big, const u64 *__restrict__ planes,
+                 u64 *__restrict__ out, size_t batch, int n, int N, int beta) {
+  const int wv = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int cb = blockIdx.y;
+  const int cols = n + 1;
+  const size_t b0 = ((size_t)blockIdx.x * KSM_WAVES + wv) * 32;
+  if (b0 >= batch) return;
+  const int s = 64 - LKS * beta;
+  const int32_t h = 1 << (beta - 1), mask = (1 << beta) - 1;
+  const int KB = N * LKS / 32, NB = N / 32;
+  const u64 *bp = planes + (size_t)cb * KB * 1024 + l;
+
+  const u64 *arow[2];
+  bool aok[2];
+#pragma unroll
+  for (int bt = 0; bt < 2; ++bt) {
+    const size_t q = b0 + 16 * bt + (l & 15);
+    aok[bt] = q < batch;
+    arow[bt] = big + (aok[bt] ? q : 0) * (size_t)(N + 1) + 8 * (l >> 4);
+  }
+  ks_v4i acc[2][2][8];
+#pragma unroll
+  for (int bt = 0; bt < 2; ++bt)
+#pragma unroll
+    for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+      for (int m = 0; m < 8; ++m) acc[bt][cc][m] = ks_v4i{0, 0, 0, 0};
+
+  for (int jb = 0; jb < NB; ++jb) {
+    int32_t r[2][8];
+#pragma unroll
+    for (int bt = 0; bt < 2; ++bt)
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        r[bt][i] = gl_round_top32(aok[bt] ? arow[bt][32 * jb + i] : 0, s);
+#pragma unroll 1
+    for (int t = LKS - 1; t >= 0; --t) {
+      long a[2];
+#pragma unroll
+      for (int bt = 0; bt < 2; ++bt) {
+        u32 w0 = 0, w1 = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          int32_t d = r[bt][i];
+          if (t > 0) {
+            d = ((d + h) & mask) - h;
+            r[bt][i] = (r[bt][i] - d) >> beta;
+          }
+          const u32 byte = (u32)d & 0xFFu;
+          if (i < 4) w0 |= byte << (8 * i);
+          else w1 |= byte << (8 * (i - 4));
+        }
+        a[bt] = (long)gl_mk(w0, w1);
+      }
+      const u64 *kp = bp + (size_t)(t * NB + jb) * 1024;
+      long bf[8][2];
+#pragma unroll
+      for (int m = 0; m < 8; ++m)
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) bf[m][cc] = (long)kp[(2 * m + cc) * 64];
+#pragma unroll
+      for (int m = 0; m < 8; ++m)
+#pragma unroll
+        for (int bt = 0; bt < 2; ++bt)
+#pragma unroll
+          for (int cc = 0; cc < 2; ++cc)
+            acc[bt][cc][m] =
+                __builtin_amdgcn_mfma_i32_16x16x32_i8(a[bt], bf[m][cc], acc[bt][cc][m], 0, 0, 0);
+    }
+  }
+
+#pragma unroll
+  for (int bt = 0; bt < 2; ++bt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const size_t q = b0 + 16 * bt + 4 * (l >> 4) + i;
+      if (q >= batch) continue;
+      const u64 body = big[q * (size_t)(N + 1) + N];
+#pragma unroll
+      for (int cc = 0; cc < 2; ++cc) {
+        const int c = 32 * cb + 16 * cc + (l & 15);
+        if (c >= cols) continue;
+        int64_t lo = 0, hi = 0;
+#pragma unroll
+        for (int m = 3; m >= 0; --m) {
+          lo = lo * 256 + acc[bt][cc][m][i];
+          hi = hi * 256 + acc[bt][cc][m + 4][i];
+        }
+        const u64 lop = (u64)lo + (lo < 0 ? GL_P : 0);
+        const u64 hi_p = (u64)hi + (hi < 0 ? GL_P : 0);
+        const u64 sum = gl_add(lop, gl_mul_pow2<32>(hi_p));
+        out[q * (size_t)cols + c] = gl_sub(c == n ? body : 0, sum);
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 
@@ -115,6 +276,12 @@ hipError_t launch_ksk_prepare(const uint64_t *ksk_std, uint64_t *ksk_dev,
                               const rosetta_params &p, hipStream_t st) {
   const size_t rows = (size_t)p.N * p.ks_level;
   const int cols = (int)p.n + 1;
+  if (ks_on_matrix_cores(p)) {
+    const size_t words = ks_matrix_key_words(p);
+    hipLaunchKernelGGL(k_ksk_planes, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, st,
+                       ksk_std, ksk_dev, (int)p.N, (int)p.ks_level, cols, words);
+    return hipGetLastError();
+  }
   hipError_t e = hipMemcpyAsync(ksk_dev, ksk_std, rows * cols * sizeof(u64),
                                 hipMemcpyDeviceToDevice, st);
   if (e != hipSuccess) return e;
@@ -126,6 +293,30 @@ hipError_t launch_ksk_prepare(const uint64_t *ksk_std, uint64_t *ksk_dev,
 
 hipError_t launch_keyswitch(const uint64_t *big, const uint64_t *ksk_dev, uint64_t *out,
                             size_t batch, const rosetta_params &p, hipStream_t st) {
+  if (ks_on_matrix_cores(p)) {
+    const dim3 grid((unsigned)((batch + 32 * KSM_WAVES - 1) / (32 * KSM_WAVES)),
+                    (p.n + 1 + 31) / 32);
+    const int n = (int)p.n, N = (int)p.N, beta = (int)p.ks_base_log;
+#define ROSETTA_KSM_CASE(LK)                                                               \
+  case LK:                                                                                 \
+    hipLaunchKernelGGL(k_keyswitch_mfma<LK>, grid, dim3(64 * KSM_WAVES), 0, st, big, ksk_dev, \
+                       out, batch, n, N, beta);                                            \
+    break;
+    switch (p.ks_level) {
+      ROSETTA_KSM_CASE(1)
+      ROSETTA_KSM_CASE(2)
+      ROSETTA_KSM_CASE(3)
+      ROSETTA_KSM_CASE(4)
+      ROSETTA_KSM_CASE(5)
+      ROSETTA_KSM_CASE(6)
+      ROSETTA_KSM_CASE(7)
+      ROSETTA_KSM_CASE(8)
+      default:
+        return hipErrorInvalidValue;
+    }
+#undef ROSETTA_KSM_CASE
+    return hipGetLastError();
+  }
   const dim3 grid((unsigned)((batch + KS_BT - 1) / KS_BT), (p.n + 1 + KS_TPB - 1) / KS_TPB);
   const int n = (int)p.n, N = (int)p.N, beta = (int)p.ks_base_log;
 #define ROSETTA_KS_CASE(LK)                                                                 \

@@ -147,6 +147,53 @@ def test_library_keys_give_same_result(O, torch_dev):
     assert np.array_equal(R.to_host(bsk2), R.to_host(bsk))
 
 
+# ----------------------------------------------------------- key switch ---
+
+# (n, N, l_ks, beta_ks): the headline shape and its largest LWE dimension
+# (2049 columns: a last column block of one column) on the int8 matrix
+# cores, and two shapes the VALU kernel takes (beta_ks = 8 digits do not
+# fit a signed byte; l_ks beta_ks = 32 does not fit the 31-bit rounding)
+KS_SHAPES = {"mfma_n1024": (1024, 2048, 6, 3), "mfma_n2048": (2048, 2048, 6, 3),
+             "mfma_l8_b3_n742": (742, 2048, 8, 3), "valu_b8": (1024, 2048, 2, 8),
+             "valu_l4_b8_n63": (63, 1024, 4, 8)}
+S127 = 0x7F7F7F7F7F7F7F7F    # largest word whose 8 balanced base-256 digits fit
+
+
+@pytest.mark.parametrize("name", list(KS_SHAPES))
+def test_keyswitch_vs_oracle(O, torch_dev, name):
+    # any key words (the key switch is linear): uniform ones with planted
+    # extremes of the byte-plane encoding; inputs with rounding boundaries
+    # and a batch ragged against 16-, 32- and 128-ciphertext tiles
+    n, N, lks, beta = KS_SHAPES[name]
+    prm = dict(n=n, k=1, N=N, pbs_level=2, pbs_base_log=8, ks_level=lks, ks_base_log=beta,
+               msg_bits=2)
+    op = O.Params.make(**prm)
+    rng = np.random.default_rng(n + N + lks)
+    ksk = rng.integers(0, P, (N * lks, n + 1), dtype=np.uint64)
+    edges = [0, 1, P - 1, P - 2, S127 - 1, S127, S127 + 1, 1 << 63, P - (1 << 63) - 1,
+             P - (1 << 63), (1 << 32) - 1, 1 << 32]
+    flat = ksk.reshape(-1)
+    pos = rng.choice(flat.size, size=4000, replace=False)
+    flat[pos] = np.array(edges, dtype=np.uint64)[np.arange(pos.size) % len(edges)]
+    ksk[0, :] = P - 1
+    ksk[:, n] = P - 1
+    batch = 131
+    big = rng.integers(0, P, (batch, N + 1), dtype=np.uint64)
+    s = 64 - lks * beta
+    half = [(P - 1) // 2, (P + 1) // 2, 0, P - 1, 1 << (s - 1), (1 << (s - 1)) - 1,
+            P - (1 << (s - 1)), 3 << (s - 1)]
+    big[0, :] = P - 1
+    big[1, : len(half)] = half
+    big[2, :] = (P - 1) // 2
+    say(f"[keyswitch {name}] GPU")
+    out = R.to_host(R.keyswitch(R.to_device(big), R.ksk_prepare(R.to_device(ksk), prm), prm))
+    picks = [0, 1, 2, 15, 16, 17, 31, 32, 63, 127, 128, 130]   # edge rows, tile boundaries
+    say(f"[keyswitch {name}] oracle on {len(picks)} of {batch}")
+    assert np.all(out < np.uint64(P))
+    for q in picks:
+        assert np.array_equal(out[q], O.keyswitch(op, big[q], ksk)), q
+
+
 # ------------------------------------------------- workloads, full size ---
 
 FULL = ["gpt2_gelu", "tinyllama_silu", "llama3_8b_silu", "llama3_8b_softmax_exp",
