@@ -42,6 +42,7 @@ CU, CLOCK_HZ, LANES = 256, 2.4e9, 64
 MODMUL_VALU_OPS = 17
 MODMUL_PEAK_T = CU * CLOCK_HZ * LANES / MODMUL_VALU_OPS / 1e12   # Tmodmul/s
 MULTIPLIER_BOUND_T = CU * CLOCK_HZ * LANES / 4 / 1e12
+INT8_PEAK_P = 5.0   # MI355X dense int8 matrix-core peak, POP/s (no sparsity)
 PMC_PROFILE = os.path.join(ROOT, "profiles", "k_blind_rotate_llama3_8b_silu_pmc.md")
 KERNEL_SOURCES = ["gl.hpp", "ntt.hpp", "kernels.hip"]
 
@@ -350,6 +351,17 @@ def main():
                 "modmul_probe": round(probe_t, 4),
                 "frac_of_modmul_probe": round(achieved_t / probe_t, 4)}
     hbm_bytes = (w.bsk_words() + w.ksk_words()) * 8 + w.batch * 2 * (w.n + 1) * 8 + w.N * 8
+    # the key switch on the int8 matrix cores (the condition rosetta.h states
+    # for its byte-plane key): 8 byte-plane products of 2 ops per digit MAC
+    ks_mfma = (1 <= w.ks_base_log <= 7 and w.ks_level * w.ks_base_log <= 30 and w.N % 32 == 0
+               and w.N * w.ks_level * (1 << (w.ks_base_log - 1)) * 128 < (1 << 31))
+    ks_ops = 2 * 8 * w.batch * w.N * w.ks_level * (w.n + 1)
+    roofline_ks = ({"bound": "mfma", "kernel": "k_keyswitch_mfma", "dtype": "i8",
+                    "achieved": round(ks_ops / (ks_ms * 1e-3) / 1e15, 4),
+                    "peak": INT8_PEAK_P, "unit": "POP/s",
+                    "frac": round(ks_ops / (ks_ms * 1e-3) / 1e15 / INT8_PEAK_P, 4),
+                    "per_launch_ops": ks_ops, "launch_ms": round(ks_ms, 3)}
+                   if ks_mfma else None)
 
     result = {
         "metric": f"PBS/sec (bootstraps/s) at N={w.N} batch {w.batch}; "
@@ -369,6 +381,7 @@ def main():
         "hbm_algorithmic_frac": round(hbm_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 6),
         "checks": {"split_equals_pbs_batch": same, "decrypt_equals_table_rate": round(ok_rate, 5)},
         "roofline": roofline,
+        "roofline_keyswitch": roofline_ks,
     }
     if args.lookup_steps > 0:
         log("[bench] lookup select (blind rotation of ciphertext test polynomials + trace)")

@@ -118,8 +118,9 @@ size_t rosetta_ksk_device_words(const rosetta_params *params);
 rosetta_status rosetta_bsk_prepare(const uint64_t *bsk_std_dev, uint64_t *bsk_dev,
                                    const rosetta_params *params, void *stream);
 
-/* Key-switching-key preparation (once per key, not part of a PBS): writes the prepared layout of the standard key `ksk_std_dev` into
- * `ksk_dev` (rosetta_ksk_device_words words, device, must not overlap):
+/* Key-switching-key preparation (once per key, not part of a PBS): writes
+ * the prepared layout of the standard key `ksk_std_dev` into `ksk_dev`
+ * (rosetta_ksk_device_words words, device, must not overlap):
  * the signed byte planes of every key word (each word w replaced by w or
  * w - p, whichever 8 balanced base-256 digits represent) in the operand
  * order of the matrix-core kernel, or the key copied with its column sums

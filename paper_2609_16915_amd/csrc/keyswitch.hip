@@ -123,12 +123,14 @@ k_keyswitch(const u64 *__restrict__ big, const u64 *__restrict__ ksk, u64 *__res
 // flipped is k_m as a signed byte; X is K + 128 S, plus 2^32 - 1 (= -p mod
 // 2^64) when V = K - p.
 //
-// Byte-plane layout, in 8-byte words: word ((cb KB + kb) 16 + 2 m + cc) 64
-// + lane holds, in byte i, k_m[kappa][c] with kappa = 32 kb + 8 (lane / 16)
-// + i and c = 32 cb + 16 cc + lane % 16 (0 past the last column): exactly
-// the B operand of a 16 x 16 x 32 int8 product (lane l supplies rows
-// 8 (l / 16) .. + 7 of column l % 16) for the column tile cc of column
-// block cb, plane m, k block kb (KB = N l_ks / 32 of them).
+// Byte-plane layout, in 8-byte words: word ((cb KB + kb) 8 + m) 128
+// + 2 lane + cc holds, in byte i, k_m[kappa][c] with kappa = 32 kb +
+// 8 (lane / 16) + i and c = 32 cb + 16 cc + lane % 16 (0 past the last
+// column): the B operand of a 16 x 16 x 32 int8 product (lane l supplies
+// rows 8 (l / 16) .. + 7 of column l % 16) for column tile cc of column
+// block cb, plane m, k block kb (KB = N l_ks / 32 of them).  The 1024
+// words of one (cb, kb) are contiguous, and a lane's two column tiles are
+// adjacent.
 constexpr u64 KS_S128 = 0x8080808080808080ull;   // 128 S
 constexpr u64 KS_S127 = 0x7F7F7F7F7F7F7F7Full;   // 127 S
 
@@ -136,10 +138,8 @@ __global__ void k_ksk_planes(const u64 *__restrict__ ksk, u64 *__restrict__ plan
                              int lks, int cols, size_t words) {
   const size_t w = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (w >= words) return;
-  const int lane = (int)(w & 63);
-  const size_t f = w >> 6;                 // (cb KB + kb) 16 + 2 m + cc
-  const int cc = (int)(f & 1), m = (int)((f >> 1) & 7);
-  const size_t blk = f >> 4;               // cb KB + kb
+  const int cc = (int)(w & 1), lane = (int)((w >> 1) & 63), m = (int)((w >> 7) & 7);
+  const size_t blk = w >> 10;              // cb KB + kb
   const size_t KB = (size_t)N * lks / 32;
   const int kb = (int)(blk % KB), cb = (int)(blk / KB);
   const int c = 32 * cb + 16 * cc + lane % 16;
@@ -157,32 +157,38 @@ __global__ void k_ksk_planes(const u64 *__restrict__ ksk, u64 *__restrict__ plan
 typedef int32_t ks_v4i __attribute__((ext_vector_type(4)));
 
 // out[b][c] = (c == n ? b'_b : 0) - sum_kappa D[b][kappa] K[kappa][c].
-// Workgroup = 4 waves on one 32-column block (the same key fragments,
-// shared through the cache), each wave on its own 32 ciphertexts: two
-// 16-ciphertext row tiles x two 16-column tiles x 8 byte planes of int32
-// accumulators.  Per 32 input coefficients a lane rounds its 8 coefficients
-// of each row tile and peels their l_ks balanced digits from the bottom
-// (the A operand of level t: row l % 16, coefficients 8 (l / 16) .. + 7);
-// each level is 32 products.  The planes are recombined exactly: with
-// |acc| < 2^31, lo = sum_{m<4} 256^m acc_m and hi = sum_{m>=4} 256^(m-4)
-// acc_m are below 2^56 in magnitude, and the sum is lo + 2^32 hi mod p.
-// No barriers: a wave with no ciphertexts exits at once (every column
-// block holds at least one column).
+// Workgroup = 4 waves on one 32-column block, each wave on its own 32
+// ciphertexts: two 16-ciphertext row tiles x two 16-column tiles x 8 byte
+// planes of int32 accumulators.  The contraction runs over k blocks in the
+// order (32-coefficient chunk, level from the bottom); the workgroup
+// stages each k block's 8 KB of key fragments in LDS (double-buffered, one
+// barrier per k block, the next block's global loads in flight during the
+// current one's products), so the key is fetched once per 128 ciphertexts.
+// At a chunk's first level a lane rounds its 8 coefficients of each row
+// tile; every level peels one balanced digit from the bottom (the A operand
+// of level t: row l % 16, coefficients 8 (l / 16) .. + 7) and issues 32
+// products.  The planes are recombined exactly: with |acc| < 2^31,
+// lo = sum_{m<4} 256^m acc_m and hi = sum_{m>=4} 256^(m-4) acc_m are below
+// 2^56 in magnitude, and the sum is lo + 2^32 hi mod p.  A wave with no
+// ciphertexts still takes part in the staging and the barriers.
 constexpr int KSM_WAVES = 4;
 
 template <int LKS>
 __global__ void __launch_bounds__(64 * KSM_WAVES) __attribute__((amdgpu_waves_per_eu(2, 2)))
 k_keyswitch_mfma(const u64 *__restrict__ big, const u64 *__restrict__ planes,
                  u64 *__restrict__ out, size_t batch, int n, int N, int beta) {
-  const int wv = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __shared__ __attribute__((aligned(16))) u64 kbuf[2][1024];
+  const int tid = threadIdx.x;
+  const int wv = tid >> 6, l = tid & 63;
   const int cb = blockIdx.y;
   const int cols = n + 1;
   const size_t b0 = ((size_t)blockIdx.x * KSM_WAVES + wv) * 32;
-  if (b0 >= batch) return;
+  const bool active = b0 < batch;
   const int s = 64 - LKS * beta;
   const int32_t h = 1 << (beta - 1), mask = (1 << beta) - 1;
-  const int KB = N * LKS / 32, NB = N / 32;
-  const u64 *bp = planes + (size_t)cb * KB * 1024 + l;
+  const int NB = N / 32, KB = NB * LKS;
+  // this thread's 32 bytes of each k block's 8 KB
+  const ulonglong2 *gsrc = (const ulonglong2 *)(planes + (size_t)cb * KB * 1024) + 2 * tid;
 
   const u64 *arow[2];
   bool aok[2];
@@ -200,15 +206,34 @@ k_keyswitch_mfma(const u64 *__restrict__ big, const u64 *__restrict__ planes,
 #pragma unroll
       for (int m = 0; m < 8; ++m) acc[bt][cc][m] = ks_v4i{0, 0, 0, 0};
 
-  for (int jb = 0; jb < NB; ++jb) {
-    int32_t r[2][8];
-#pragma unroll
-    for (int bt = 0; bt < 2; ++bt)
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        r[bt][i] = gl_round_top32(aok[bt] ? arow[bt][32 * jb + i] : 0, s);
+  {
+    const ulonglong2 g0 = gsrc[(size_t)(LKS - 1) * NB * 512], g1 = gsrc[(size_t)(LKS - 1) * NB * 512 + 1];
+    ((ulonglong2 *)kbuf[0])[2 * tid] = g0;
+    ((ulonglong2 *)kbuf[0])[2 * tid + 1] = g1;
+  }
+  __syncthreads();
+
+  int32_t r[2][8];
+  const int total = NB * LKS;
 #pragma unroll 1
-    for (int t = LKS - 1; t >= 0; --t) {
+  for (int it = 0; it < total; ++it) {
+    const int jb = it / LKS, t = LKS - 1 - (it - jb * LKS);
+    // next k block: (jb, t - 1), or (jb + 1, LKS - 1)
+    ulonglong2 p0, p1;
+    const bool more = it + 1 < total;
+    if (more) {
+      const int kn = t > 0 ? (t - 1) * NB + jb : (LKS - 1) * NB + jb + 1;
+      p0 = gsrc[(size_t)kn * 512];
+      p1 = gsrc[(size_t)kn * 512 + 1];
+    }
+    if (active) {
+      if (t == LKS - 1) {
+#pragma unroll
+        for (int bt = 0; bt < 2; ++bt)
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            r[bt][i] = gl_round_top32(aok[bt] ? arow[bt][32 * jb + i] : 0, s);
+      }
       long a[2];
 #pragma unroll
       for (int bt = 0; bt < 2; ++bt) {
@@ -226,22 +251,24 @@ k_keyswitch_mfma(const u64 *__restrict__ big, const u64 *__restrict__ planes,
         }
         a[bt] = (long)gl_mk(w0, w1);
       }
-      const u64 *kp = bp + (size_t)(t * NB + jb) * 1024;
-      long bf[8][2];
+      const ulonglong2 *kb2 = (const ulonglong2 *)kbuf[it & 1] + l;
 #pragma unroll
-      for (int m = 0; m < 8; ++m)
+      for (int m = 0; m < 8; ++m) {
+        const ulonglong2 f = kb2[64 * m];
 #pragma unroll
-        for (int cc = 0; cc < 2; ++cc) bf[m][cc] = (long)kp[(2 * m + cc) * 64];
-#pragma unroll
-      for (int m = 0; m < 8; ++m)
-#pragma unroll
-        for (int bt = 0; bt < 2; ++bt)
-#pragma unroll
-          for (int cc = 0; cc < 2; ++cc)
-            acc[bt][cc][m] =
-                __builtin_amdgcn_mfma_i32_16x16x32_i8(a[bt], bf[m][cc], acc[bt][cc][m], 0, 0, 0);
+        for (int bt = 0; bt < 2; ++bt) {
+          acc[bt][0][m] = __builtin_amdgcn_mfma_i32_16x16x32_i8(a[bt], (long)f.x, acc[bt][0][m], 0, 0, 0);
+          acc[bt][1][m] = __builtin_amdgcn_mfma_i32_16x16x32_i8(a[bt], (long)f.y, acc[bt][1][m], 0, 0, 0);
+        }
+      }
     }
+    if (more) {
+      ((ulonglong2 *)kbuf[(it + 1) & 1])[2 * tid] = p0;
+      ((ulonglong2 *)kbuf[(it + 1) & 1])[2 * tid + 1] = p1;
+    }
+    __syncthreads();
   }
+  if (!active) return;
 
 #pragma unroll
   for (int bt = 0; bt < 2; ++bt)
