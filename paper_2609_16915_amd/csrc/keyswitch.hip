@@ -165,11 +165,12 @@ typedef int32_t ks_v4i __attribute__((ext_vector_type(4)));
 // barrier per k block, the next block's global loads in flight during the
 // current one's products), so the key is fetched once per 128 ciphertexts.
 // At a chunk's first level a lane rounds its 8 coefficients of each row
-// tile; every level peels one balanced digit from the bottom (the A operand
-// of level t: row l % 16, coefficients 8 (l / 16) .. + 7) and issues 32
-// products.  The planes are recombined exactly: with |acc| < 2^31,
-// lo = sum_{m<4} 256^m acc_m and hi = sum_{m>=4} 256^(m-4) acc_m are below
-// 2^56 in magnitude, and the sum is lo + 2^32 hi mod p.  A wave with no
+// tile (loaded one chunk ahead) and issues the next chunk's loads; every
+// level peels one balanced digit from the bottom (the A operand of level
+// t: row l % 16, coefficients 8 (l / 16) .. + 7) and issues 32 products.
+// The planes are recombined exactly: with |acc| < 2^31, lo = sum_{m<4}
+// 256^m acc_m and hi = sum_{m>=4} 256^(m-4) acc_m are below 2^56 in
+// magnitude, and the sum is lo + 2^32 hi mod p.  A wave with no
 // ciphertexts still takes part in the staging and the barriers.
 constexpr int KSM_WAVES = 4;
 
@@ -213,6 +214,13 @@ k_keyswitch_mfma(const u64 *__restrict__ big, const u64 *__restrict__ planes,
   }
   __syncthreads();
 
+  // raw coefficients of the next chunk, loaded a whole chunk (l_ks k
+  // blocks) before they are rounded
+  u64 cn[2][8];
+#pragma unroll
+  for (int bt = 0; bt < 2; ++bt)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cn[bt][i] = (active && aok[bt]) ? arow[bt][i] : 0;
   int32_t r[2][8];
   const int total = NB * LKS;
 #pragma unroll 1
@@ -231,8 +239,13 @@ k_keyswitch_mfma(const u64 *__restrict__ big, const u64 *__restrict__ planes,
 #pragma unroll
         for (int bt = 0; bt < 2; ++bt)
 #pragma unroll
-          for (int i = 0; i < 8; ++i)
-            r[bt][i] = gl_round_top32(aok[bt] ? arow[bt][32 * jb + i] : 0, s);
+          for (int i = 0; i < 8; ++i) r[bt][i] = gl_round_top32(cn[bt][i], s);
+        if (jb + 1 < NB) {
+#pragma unroll
+          for (int bt = 0; bt < 2; ++bt)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) cn[bt][i] = aok[bt] ? arow[bt][32 * (jb + 1) + i] : 0;
+        }
       }
       long a[2];
 #pragma unroll

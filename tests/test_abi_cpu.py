@@ -49,6 +49,34 @@ def P(**kw):
     return R.Params.from_dict(base)
 
 
+@pytest.mark.parametrize("kw,matrix", [
+    ({}, True),                                                   # 3 x 4 bits, N = 256
+    ({"n": 1024, "N": 2048, "ks_level": 6, "ks_base_log": 3}, True),   # headline shape
+    ({"n": 1024, "N": 4096, "ks_level": 6, "ks_base_log": 3}, True),
+    ({"ks_level": 2, "ks_base_log": 7}, True),                    # digits up to 64
+    ({"ks_level": 2, "ks_base_log": 8}, False),                   # a digit of 128
+    ({"ks_level": 5, "ks_base_log": 6}, True),                    # 30-bit rounded value
+    ({"ks_level": 4, "ks_base_log": 8}, False),                   # 32-bit rounded value
+    # the largest digit sums a valid set allows (N = 4096, 4 x 7 bits) stay
+    # at 2^27, inside the int32 bound the dispatch also checks
+    ({"N": 4096, "ks_level": 4, "ks_base_log": 7}, True),
+    ({"n": 2048, "N": 2048, "ks_level": 2, "ks_base_log": 8}, False),
+])
+def test_ksk_device_words_follow_the_documented_layouts(L, kw, matrix):
+    # the prepared key-switching key is the byte-plane layout exactly when
+    # the header's matrix-core condition holds, else key words + column sums
+    p = P(**kw)
+    n, N, lks, b = p.n, p.N, p.ks_level, p.ks_base_log
+    cond = (1 <= b <= 7 and lks * b <= 30 and N % 32 == 0
+            and N * lks * (1 << (b - 1)) * 128 < (1 << 31))
+    assert cond == matrix
+    plane_words = -(-(n + 1) // 32) * (N * lks // 32) * 1024
+    std_words = N * lks * (n + 1)
+    assert L.rosetta_ksk_words(C.byref(p)) == std_words
+    assert L.rosetta_ksk_device_words(C.byref(p)) == (plane_words if matrix
+                                                      else std_words + n + 1)
+
+
 @pytest.mark.parametrize("kw,status", [
     ({}, 0),
     ({"k": 2}, 3),

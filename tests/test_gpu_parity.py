@@ -151,10 +151,13 @@ def test_library_keys_give_same_result(O, torch_dev):
 
 # (n, N, l_ks, beta_ks): the headline shape and its largest LWE dimension
 # (2049 columns: a last column block of one column) on the int8 matrix
-# cores, and two shapes the VALU kernel takes (beta_ks = 8 digits do not
-# fit a signed byte; l_ks beta_ks = 32 does not fit the 31-bit rounding)
+# cores, the largest digits they take (7 bits: |d| up to 64) at the
+# largest ring, and two shapes the VALU kernel takes (beta_ks = 8 digits
+# do not fit a signed byte; l_ks beta_ks = 32 does not fit the 31-bit
+# rounding)
 KS_SHAPES = {"mfma_n1024": (1024, 2048, 6, 3), "mfma_n2048": (2048, 2048, 6, 3),
-             "mfma_l8_b3_n742": (742, 2048, 8, 3), "valu_b8": (1024, 2048, 2, 8),
+             "mfma_l8_b3_n742": (742, 2048, 8, 3), "mfma_l4_b7_N4096": (1024, 4096, 4, 7),
+             "valu_b8": (1024, 2048, 2, 8),
              "valu_l4_b8_n63": (63, 1024, 4, 8)}
 S127 = 0x7F7F7F7F7F7F7F7F    # largest word whose 8 balanced base-256 digits fit
 
