@@ -1,10 +1,12 @@
-// Key switching kernels (step a8) and the preparation of their key.
+// Key switching kernels (step a8) and the preparation of their key: the
+// int8 matrix-core kernel for parameter sets whose digits fit a signed byte
+// (ks_on_matrix_cores), the VALU kernel for the others.
 //
 // Kept apart from kernels.hip because they are compiled with the compiler's
-// default instruction scheduling: the key switch is a stream of independent
-// 32x32-bit multiply-accumulates into 64-bit accumulators, which the
-// default occupancy-first schedule already interleaves, while the transform
-// kernels are built with the ILP-first one.
+// default instruction scheduling: both are streams of independent
+// multiply-accumulates (matrix products, or 32x32-bit products into 64-bit
+// accumulators), which the default occupancy-first schedule already
+// interleaves, while the transform kernels are built with the ILP-first one.
 #include <hip/hip_runtime.h>
 
 #include "gl.hpp"
@@ -172,6 +174,9 @@ typedef int32_t ks_v4i __attribute__((ext_vector_type(4)));
 // 256^m acc_m and hi = sum_{m>=4} 256^(m-4) acc_m are below 2^56 in
 // magnitude, and the sum is lo + 2^32 hi mod p.  A wave with no
 // ciphertexts still takes part in the staging and the barriers.
+// Two waves per SIMD: the register cap of 256 holds the 128 accumulators,
+// the key fragments and the prefetched coefficients without spills (left
+// to itself the compiler takes 256 + 128 registers and one wave).
 constexpr int KSM_WAVES = 4;
 
 template <int LKS>
