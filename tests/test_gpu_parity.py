@@ -197,6 +197,34 @@ def test_keyswitch_vs_oracle(O, torch_dev, name):
         assert np.array_equal(out[q], O.keyswitch(op, big[q], ksk)), q
 
 
+def test_keyswitch_rows_independent_of_batch_tiling(O, torch_dev):
+    # the headline key-switch shape: each output row depends on its own input
+    # row only, so a batch of 257 (two full 128-ciphertext workgroups and one
+    # with a single live row) must equal the same rows switched in pieces of
+    # 1, 31, 33, 64 and 128 (every position within a 16-, 32- and 128-row
+    # tile, and workgroups with idle waves); batches of 1 and 32 and a
+    # sample of the rest against the oracle
+    n, N, lks, beta = 1024, 2048, 6, 3
+    prm = dict(n=n, k=1, N=N, pbs_level=3, pbs_base_log=8, ks_level=lks, ks_base_log=beta,
+               msg_bits=2)
+    op = O.Params.make(**prm)
+    rng = np.random.default_rng(257)
+    ksk = rng.integers(0, P, (N * lks, n + 1), dtype=np.uint64)
+    big = rng.integers(0, P, (257, N + 1), dtype=np.uint64)
+    d_ksk = R.ksk_prepare(R.to_device(ksk), prm)
+    say("[keyswitch tiling] GPU batch 257 and its pieces")
+    whole = R.to_host(R.keyswitch(R.to_device(big), d_ksk, prm))
+    parts, at = [], 0
+    for size in (1, 31, 33, 64, 128):
+        parts.append(R.to_host(R.keyswitch(R.to_device(big[at:at + size]), d_ksk, prm)))
+        at += size
+    assert at == 257
+    assert np.array_equal(np.concatenate(parts), whole)
+    say("[keyswitch tiling] oracle")
+    for q in [0, 1, 2, 31, 32, 100, 127, 128, 255, 256]:
+        assert np.array_equal(whole[q], O.keyswitch(op, big[q], ksk)), q
+
+
 # ------------------------------------------------- workloads, full size ---
 
 FULL = ["gpt2_gelu", "tinyllama_silu", "llama3_8b_silu", "llama3_8b_softmax_exp",
