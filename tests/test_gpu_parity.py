@@ -309,6 +309,10 @@ CORNERS = {
     # the headline ring with the largest small digits and a 64-bit rounded value
     "l3_b14_N2048": dict(n=12, N=2048, pbs_level=3, pbs_base_log=14, ks_level=3, ks_base_log=6,
                          msg_bits=2),
+    # the largest LWE dimension on the largest ring (the most LDS a blind
+    # rotation takes: 132 KiB), with the headline key switch
+    "n2048_N4096": dict(n=2048, N=4096, pbs_level=3, pbs_base_log=8, ks_level=6,
+                        ks_base_log=3, msg_bits=2),
 }
 
 
