@@ -174,6 +174,7 @@ typedef int32_t ks_v4i __attribute__((ext_vector_type(4)));
 // 256^m acc_m and hi = sum_{m>=4} 256^(m-4) acc_m are below 2^56 in
 // magnitude, and the sum is lo + 2^32 hi mod p.  A wave with no
 // ciphertexts still takes part in the staging and the barriers.
+//
 // Two waves per SIMD: the register cap of 256 holds the 128 accumulators,
 // the key fragments and the prefetched coefficients without spills (left
 // to itself the compiler takes 256 + 128 registers and one wave).

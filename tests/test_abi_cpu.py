@@ -77,6 +77,30 @@ def test_ksk_device_words_follow_the_documented_layouts(L, kw, matrix):
                                                       else std_words + n + 1)
 
 
+def test_byte_plane_identity_of_the_key_switch():
+    # the arithmetic the matrix-core key switch rests on, checked in exact
+    # integers: for every word K in [0, p), V = K or K - p lies in the range
+    # of 8 balanced base-256 digits [-128 S, 127 S] (S = (2^64 - 1) / 255),
+    # X = V + 128 S = K + 128 S (+ 2^32 - 1 when V = K - p) mod 2^64, and the
+    # bytes of X with the top bit flipped, read as signed, are those digits
+    p = 0xFFFFFFFF00000001
+    S = (2 ** 64 - 1) // 255
+    rng = np.random.default_rng(11)
+    words = [0, 1, 2, p - 1, p - 2, 127 * S - 1, 127 * S, 127 * S + 1, 2 ** 63 - 1, 2 ** 63,
+             p - 2 ** 63 - 1, p - 2 ** 63, 2 ** 32 - 1, 2 ** 32]
+    words += [int(x) for x in rng.integers(0, p, 20000, dtype=np.uint64)]
+    for K in words:
+        V = K if K <= 127 * S else K - p
+        assert -128 * S <= V <= 127 * S
+        X = (K + 128 * S + (0 if K <= 127 * S else 2 ** 32 - 1)) % 2 ** 64
+        assert X == V + 128 * S
+        digits = [((X >> (8 * m)) & 0xFF) ^ 0x80 for m in range(8)]
+        digits = [d - 256 if d >= 128 else d for d in digits]
+        assert all(-128 <= d <= 127 for d in digits)
+        assert sum(d * 256 ** m for m, d in enumerate(digits)) == V
+        assert V % p == K
+
+
 @pytest.mark.parametrize("kw,status", [
     ({}, 0),
     ({"k": 2}, 3),
