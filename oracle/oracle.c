@@ -49,10 +49,19 @@
  *   blind rot.  trivial input gives (0, X^-b~ v) exactly; the paper's
  *               N = 4 example (LUT 6,7,3,5; m = 2 -> 3)
  *   PBS         decrypt(PBS(Enc m)) = T[m] for every m (3-bit and 4-bit
- *               spaces); tier 1 = tier 2 bit for bit
+ *               spaces); tier 1 = tier 2 bit for bit, which pins only the
+ *               external product, since both tiers run the same loop
+ *               (or_br_loop), extraction and key switching
+ *   shared loop the independent pure-Python coding oracle/mini.py (tier 0:
+ *               its own modulus switch, accumulator start, CMux loop,
+ *               decomposition, Kronecker-substitution products, extraction
+ *               and key switching) equals tier 1 bit for bit on the whole
+ *               tiny workload, the paper's N = 4 example and noisy sets at
+ *               N = 16..64 (tests/test_oracle_mini.py)
  * The exact noise bits of a bootstrapped ciphertext are fixed by the
- * conventions above (loop order, CMux form, rounding rules) and are checked
- * only through these component pins and tier agreement.
+ * conventions above (loop order, CMux form, rounding rules); beyond the
+ * sizes tier 0 runs, they are checked through these component pins and
+ * the agreement of the codings.
  *
  * Lookup-protocol primitives (end of file; tests/test_oracle_lookup.py):
  *   automorphism  evaluation at z^d for every root z; group law; ring map;
