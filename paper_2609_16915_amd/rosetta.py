@@ -195,6 +195,28 @@ def _stream(stream) -> int:
     return stream.cuda_stream
 
 
+def _words(t) -> int:
+    """Element count of a tensor (or numpy array)."""
+    return int(t.numel()) if hasattr(t, "numel") else int(t.size)
+
+
+def _expect(t, name: str, words: int):
+    """Raise ValueError unless `t` holds exactly `words` elements.  Runs before
+    any library call, so that a buffer of the wrong size never reaches a
+    kernel (which would read or write out of its bounds)."""
+    got = _words(t)
+    if got != words:
+        raise ValueError(f"{name} holds {got} words, the call needs {words}")
+
+
+def _batch_of(t, name: str, row: int, allow_empty: bool = True) -> int:
+    """Rows of `row` words in `t`; ValueError if the size is not a multiple."""
+    got = _words(t)
+    if got % row or (got == 0 and not allow_empty):
+        raise ValueError(f"{name} holds {got} words, not a whole number of {row}-word rows")
+    return got // row
+
+
 def empty(words, device="cuda"):
     torch = _torch()
     return torch.empty(words, dtype=torch.uint64, device=device)
@@ -228,8 +250,10 @@ def check_params(params):
 
 def bsk_prepare(bsk_std, params, out=None, stream=None):
     p = _params(params)
+    _expect(bsk_std, "bsk_std", bsk_words(p))
     if out is None:
         out = empty(bsk_words(p), bsk_std.device)
+    _expect(out, "bsk_dev", bsk_words(p))
     _check(lib().rosetta_bsk_prepare(_dev(bsk_std, "bsk_std"), _dev(out, "bsk_dev"), C.byref(p),
                                      _stream(stream)))
     return out
@@ -237,18 +261,30 @@ def bsk_prepare(bsk_std, params, out=None, stream=None):
 
 def ksk_prepare(ksk_std, params, out=None, stream=None):
     p = _params(params)
+    _expect(ksk_std, "ksk_std", ksk_words(p))
     if out is None:
         out = empty(ksk_device_words(p), ksk_std.device)
+    _expect(out, "ksk_dev", ksk_device_words(p))
     _check(lib().rosetta_ksk_prepare(_dev(ksk_std, "ksk_std"), _dev(out, "ksk_dev"), C.byref(p),
                                      _stream(stream)))
     return out
 
 
+def _check_pbs_args(p, lwe_in, bsk_dev, ksk_dev, lut) -> int:
+    """Sizes of the PBS inputs against the parameters; returns the batch."""
+    batch = _batch_of(lwe_in, "lwe_in", p.n + 1)
+    _expect(bsk_dev, "bsk_dev", bsk_words(p))
+    _expect(ksk_dev, "ksk_dev", ksk_device_words(p))
+    _expect(lut, "lut", p.N)
+    return batch
+
+
 def pbs_batch(lwe_in, bsk_dev, ksk_dev, lut, params, out=None, stream=None):
     p = _params(params)
-    batch = lwe_in.numel() // (p.n + 1)
+    batch = _check_pbs_args(p, lwe_in, bsk_dev, ksk_dev, lut)
     if out is None:
         out = empty((batch, p.n + 1), lwe_in.device)
+    _expect(out, "lwe_out", batch * (p.n + 1))
     _check(lib().rosetta_pbs_batch(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
                                    _dev(ksk_dev, "ksk_dev"), _dev(lut, "lut"),
                                    _dev(out, "lwe_out"), batch, C.byref(p), _stream(stream)))
@@ -261,9 +297,13 @@ def pbs_workspace_bytes(params, batch: int) -> int:
 
 def pbs_batch_ws(lwe_in, bsk_dev, ksk_dev, lut, params, workspace, out=None, stream=None):
     p = _params(params)
-    batch = lwe_in.numel() // (p.n + 1)
+    batch = _check_pbs_args(p, lwe_in, bsk_dev, ksk_dev, lut)
     if out is None:
         out = empty((batch, p.n + 1), lwe_in.device)
+    _expect(out, "lwe_out", batch * (p.n + 1))
+    if _words(workspace) * 8 < pbs_workspace_bytes(p, batch):
+        raise ValueError(f"workspace holds {_words(workspace) * 8} bytes, the call needs "
+                         f"{pbs_workspace_bytes(p, batch)}")
     _check(lib().rosetta_pbs_batch_ws(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
                                       _dev(ksk_dev, "ksk_dev"), _dev(lut, "lut"),
                                       _dev(out, "lwe_out"), batch, C.byref(p),
@@ -275,9 +315,12 @@ def pbs_batch_ws(lwe_in, bsk_dev, ksk_dev, lut, params, workspace, out=None, str
 
 def blind_rotate(lwe_in, bsk_dev, lut, params, out=None, stream=None):
     p = _params(params)
-    batch = lwe_in.numel() // (p.n + 1)
+    batch = _batch_of(lwe_in, "lwe_in", p.n + 1)
+    _expect(bsk_dev, "bsk_dev", bsk_words(p))
+    _expect(lut, "lut", p.N)
     if out is None:
         out = empty((batch, 2 * p.N), lwe_in.device)
+    _expect(out, "glwe_out", batch * 2 * p.N)
     _check(lib().rosetta_blind_rotate(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
                                       _dev(lut, "lut"), _dev(out, "glwe_out"), batch, C.byref(p),
                                       _stream(stream)))
@@ -286,9 +329,12 @@ def blind_rotate(lwe_in, bsk_dev, lut, params, out=None, stream=None):
 
 def blind_rotate_extract(lwe_in, bsk_dev, lut, params, out=None, stream=None):
     p = _params(params)
-    batch = lwe_in.numel() // (p.n + 1)
+    batch = _batch_of(lwe_in, "lwe_in", p.n + 1)
+    _expect(bsk_dev, "bsk_dev", bsk_words(p))
+    _expect(lut, "lut", p.N)
     if out is None:
         out = empty((batch, p.N + 1), lwe_in.device)
+    _expect(out, "big_out", batch * (p.N + 1))
     _check(lib().rosetta_blind_rotate_extract(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
                                               _dev(lut, "lut"), _dev(out, "big_out"), batch,
                                               C.byref(p), _stream(stream)))
@@ -297,31 +343,37 @@ def blind_rotate_extract(lwe_in, bsk_dev, lut, params, out=None, stream=None):
 
 def keyswitch(big_in, ksk_dev, params, out=None, stream=None):
     p = _params(params)
-    batch = big_in.numel() // (p.N + 1)
+    batch = _batch_of(big_in, "big_in", p.N + 1)
+    _expect(ksk_dev, "ksk_dev", ksk_device_words(p))
     if out is None:
         out = empty((batch, p.n + 1), big_in.device)
+    _expect(out, "lwe_out", batch * (p.n + 1))
     _check(lib().rosetta_keyswitch(_dev(big_in, "big_in"), _dev(ksk_dev, "ksk_dev"),
                                    _dev(out, "lwe_out"), batch, C.byref(p), _stream(stream)))
     return out
 
 
 def ntt_forward(x, N: int, out=None, stream=None):
-    count = x.numel() // N
+    count = _batch_of(x, "in", N)
     out = empty(x.shape, x.device) if out is None else out
+    _expect(out, "out", count * N)
     _check(lib().rosetta_ntt_forward(_dev(x, "in"), _dev(out, "out"), count, N, _stream(stream)))
     return out
 
 
 def ntt_inverse(x, N: int, out=None, stream=None):
-    count = x.numel() // N
+    count = _batch_of(x, "in", N)
     out = empty(x.shape, x.device) if out is None else out
+    _expect(out, "out", count * N)
     _check(lib().rosetta_ntt_inverse(_dev(x, "in"), _dev(out, "out"), count, N, _stream(stream)))
     return out
 
 
 def poly_mul(a, b, N: int, out=None, stream=None):
-    count = a.numel() // N
+    count = _batch_of(a, "a", N)
+    _expect(b, "b", count * N)
     out = empty(a.shape, a.device) if out is None else out
+    _expect(out, "c", count * N)
     _check(lib().rosetta_poly_mul(_dev(a, "a"), _dev(b, "b"), _dev(out, "c"), count, N,
                                   _stream(stream)))
     return out
@@ -336,8 +388,12 @@ def field_op(op: int, a, b=None, c=None, out=None, stream=None):
     (op: FIELD_ADD, FIELD_SUB, FIELD_MUL, FIELD_MUL_ADD, FIELD_ADD_WEAK,
     FIELD_MUL_ADD_WEAK, FIELD_MUL_POW2 + e, FIELD_ROUND_TOP + s; the last
     returns int64 values as uint64)."""
-    count = a.numel()
+    count = _words(a)
+    for t, name in ((b, "b"), (c, "c")):
+        if t is not None:
+            _expect(t, name, count)
     out = empty(a.shape, a.device) if out is None else out
+    _expect(out, "out", count)
     _check(lib().rosetta_field_op(op, _dev(a, "a"), None if b is None else _dev(b, "b"),
                                   None if c is None else _dev(c, "c"), _dev(out, "out"), count,
                                   _stream(stream)))
@@ -348,6 +404,8 @@ def modmul_chain(seed: int, threads: int, iters: int, out=None, stream=None):
     """Throughput probe: 8 register-resident product chains per thread
     (see rosetta_modmul_chain); returns out[threads]."""
     out = empty(threads) if out is None else out
+    if _words(out) < threads:
+        raise ValueError(f"out holds {_words(out)} words, the call needs {threads}")
     _check(lib().rosetta_modmul_chain(seed, threads, iters, _dev(out, "out"), _stream(stream)))
     return out
 
@@ -363,10 +421,13 @@ def blind_rotate_glwe(lwe_in, bsk_dev, glwe_tp, params, extract=False, group=1, 
     """Blind rotation of GLWE test polynomials glwe_tp [batch*group][2N], each
     LWE selector of lwe_in [batch][n+1] serving `group` consecutive ones."""
     p = _params(params)
-    batch = lwe_in.numel() // (p.n + 1)
+    batch = _batch_of(lwe_in, "lwe_in", p.n + 1)
+    _expect(bsk_dev, "bsk_dev", bsk_words(p))
+    _expect(glwe_tp, "glwe_tp", batch * group * 2 * p.N)
+    shape = (batch * group, p.N + 1) if extract else (batch * group, 2 * p.N)
     if out is None:
-        shape = (batch * group, p.N + 1) if extract else (batch * group, 2 * p.N)
         out = empty(shape, lwe_in.device)
+    _expect(out, "out", shape[0] * shape[1])
     _check(lib().rosetta_blind_rotate_glwe(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
                                            _dev(glwe_tp, "glwe_tp"), _dev(out, "out"), batch,
                                            group, C.byref(p), 1 if extract else 0,
@@ -376,10 +437,11 @@ def blind_rotate_glwe(lwe_in, bsk_dev, glwe_tp, params, extract=False, group=1, 
 
 def lwe_add_consts(lwe_in, consts, dim: int, out=None, stream=None):
     """out[q][j] = lwe_in[q] + (0, .., 0, consts[j])."""
-    batch = lwe_in.numel() // (dim + 1)
+    batch = _batch_of(lwe_in, "lwe_in", dim + 1)
     c = np.ascontiguousarray(consts, dtype=np.uint64)
     if out is None:
         out = empty((batch, c.size, dim + 1), lwe_in.device)
+    _expect(out, "lwe_out", batch * c.size * (dim + 1))
     _check(lib().rosetta_lwe_add_consts(_dev(lwe_in, "lwe_in"), _np_ptr(c), _dev(out, "lwe_out"),
                                         batch, c.size, dim, _stream(stream)))
     return out
@@ -387,9 +449,10 @@ def lwe_add_consts(lwe_in, consts, dim: int, out=None, stream=None):
 
 def lwe_sum_groups(lwe_in, count: int, dim: int, c0: int = 0, out=None, stream=None):
     """out[q] = sum_j lwe_in[q][j] + (0, .., 0, c0)."""
-    batch = lwe_in.numel() // ((dim + 1) * count)
+    batch = _batch_of(lwe_in, "lwe_in", (dim + 1) * count)
     if out is None:
         out = empty((batch, dim + 1), lwe_in.device)
+    _expect(out, "lwe_out", batch * (dim + 1))
     _check(lib().rosetta_lwe_sum_groups(_dev(lwe_in, "lwe_in"), c0, _dev(out, "lwe_out"), batch,
                                         count, dim, _stream(stream)))
     return out
@@ -401,8 +464,10 @@ def autk_words(params, level: int) -> int:
 
 def autk_prepare(autk_std, params, level: int, out=None, stream=None):
     p = _params(params)
+    _expect(autk_std, "autk_std", autk_words(p, level))
     if out is None:
         out = empty(autk_words(p, level), autk_std.device)
+    _expect(out, "autk_dev", autk_words(p, level))
     _check(lib().rosetta_autk_prepare(_dev(autk_std, "autk_std"), _dev(out, "autk_dev"),
                                       C.byref(p), level, _stream(stream)))
     return out
@@ -410,9 +475,11 @@ def autk_prepare(autk_std, params, level: int, out=None, stream=None):
 
 def trace(glwe_in, autk_dev, params, level: int, base_log: int, out=None, stream=None):
     p = _params(params)
-    batch = glwe_in.numel() // (2 * p.N)
+    batch = _batch_of(glwe_in, "glwe_in", 2 * p.N)
+    _expect(autk_dev, "autk_dev", autk_words(p, level))
     if out is None:
         out = empty((batch, 2 * p.N), glwe_in.device)
+    _expect(out, "glwe_out", batch * 2 * p.N)
     _check(lib().rosetta_trace(_dev(glwe_in, "glwe_in"), _dev(autk_dev, "autk_dev"),
                                _dev(out, "glwe_out"), batch, C.byref(p), level, base_log,
                                _stream(stream)))
@@ -420,8 +487,9 @@ def trace(glwe_in, autk_dev, params, level: int, base_log: int, out=None, stream
 
 
 def plain_prepare(plain, N: int, out=None, stream=None):
-    count = plain.numel() // N
+    count = _batch_of(plain, "plain", N)
     out = empty(plain.shape, plain.device) if out is None else out
+    _expect(out, "plain_prep", count * N)
     _check(lib().rosetta_plain_prepare(_dev(plain, "plain"), _dev(out, "plain_prep"), count, N,
                                        _stream(stream)))
     return out
@@ -429,10 +497,13 @@ def plain_prepare(plain, N: int, out=None, stream=None):
 
 def glwe_mul_plain(glwe_in, pa_prep, pb, N: int, out=None, stream=None):
     """out[q][s] = pa_s * glwe_in[q] + (0, pb_s); pb may be None."""
-    batch = glwe_in.numel() // (2 * N)
-    npoly = pa_prep.numel() // N
+    batch = _batch_of(glwe_in, "glwe_in", 2 * N)
+    npoly = _batch_of(pa_prep, "pa_prep", N)
+    if pb is not None:
+        _expect(pb, "pb", npoly * N)
     if out is None:
         out = empty((batch, npoly, 2 * N), glwe_in.device)
+    _expect(out, "glwe_out", batch * npoly * 2 * N)
     _check(lib().rosetta_glwe_mul_plain(_dev(glwe_in, "glwe_in"), _dev(pa_prep, "pa_prep"),
                                         None if pb is None else _dev(pb, "pb"),
                                         _dev(out, "glwe_out"), batch, npoly, N, _stream(stream)))
@@ -450,9 +521,10 @@ def _exps(exps, count):
 
 def glwe_recombine(glwe_in, count: int, N: int, exps=None, out=None, stream=None):
     """out[q] = sum_s X^(exps[s]) glwe_in[q][s] (exps None: X^s)."""
-    batch = glwe_in.numel() // (2 * N * count)
+    batch = _batch_of(glwe_in, "glwe_in", 2 * N * count)
     if out is None:
         out = empty((batch, 2 * N), glwe_in.device)
+    _expect(out, "glwe_out", batch * 2 * N)
     e, ep = _exps(exps, count)
     _check(lib().rosetta_glwe_recombine(_dev(glwe_in, "glwe_in"), ep, _dev(out, "glwe_out"),
                                         batch, count, N, _stream(stream)))
@@ -461,19 +533,21 @@ def glwe_recombine(glwe_in, count: int, N: int, exps=None, out=None, stream=None
 
 def glwe_monomial_mul(glwe_in, exps, N: int, out=None, stream=None):
     """out[q][s] = X^(exps[s]) glwe_in[q]."""
-    batch = glwe_in.numel() // (2 * N)
+    batch = _batch_of(glwe_in, "glwe_in", 2 * N)
     e, ep = _exps(exps, len(exps))
     if out is None:
         out = empty((batch, e.size, 2 * N), glwe_in.device)
+    _expect(out, "glwe_out", batch * e.size * 2 * N)
     _check(lib().rosetta_glwe_monomial_mul(_dev(glwe_in, "glwe_in"), ep, _dev(out, "glwe_out"),
                                            batch, e.size, N, _stream(stream)))
     return out
 
 
 def sample_extract(glwe_in, N: int, out=None, stream=None):
-    batch = glwe_in.numel() // (2 * N)
+    batch = _batch_of(glwe_in, "glwe_in", 2 * N)
     if out is None:
         out = empty((batch, N + 1), glwe_in.device)
+    _expect(out, "big_out", batch * (N + 1))
     _check(lib().rosetta_sample_extract(_dev(glwe_in, "glwe_in"), _dev(out, "big_out"), batch, N,
                                         _stream(stream)))
     return out
@@ -652,7 +726,9 @@ def lookup_encode(params, lp: LookupParams, tau, a, b):
 
 def lookup_prepare(plain_dev, params, lp: LookupParams, out=None, stream=None):
     p = _params(params)
+    _expect(plain_dev, "plain", lib().rosetta_lookup_plain_words(C.byref(p), C.byref(lp)))
     out = empty(plain_dev.shape, plain_dev.device) if out is None else out
+    _expect(out, "plain_prep", _words(plain_dev))
     _check(lib().rosetta_lookup_prepare(_dev(plain_dev, "plain"), _dev(out, "plain_prep"),
                                         C.byref(p), C.byref(lp), _stream(stream)))
     return out
@@ -665,12 +741,22 @@ def lookup_workspace_bytes(params, lp: LookupParams, batch: int) -> int:
 def lookup_eval(x_rlwe, x_cmp, bsk_dev, ksk_dev, autk_dev, plain_prep, consts, params,
                 lp: LookupParams, workspace=None, out=None, stream=None):
     p = _params(params)
-    batch = x_cmp.numel() // (p.n + 1)
+    batch = _batch_of(x_cmp, "x_cmp", p.n + 1)
+    _expect(x_rlwe, "x_rlwe", batch * 2 * p.N)
+    _expect(bsk_dev, "bsk_dev", bsk_words(p))
+    _expect(ksk_dev, "ksk_dev", ksk_device_words(p))
+    _expect(autk_dev, "autk_dev", autk_words(p, lp.trace_level))
+    _expect(plain_prep, "plain_prep", lib().rosetta_lookup_plain_words(C.byref(p), C.byref(lp)))
     if out is None:
         out = empty((batch, 2 * p.N), x_cmp.device)
+    _expect(out, "out", batch * 2 * p.N)
     if workspace is None:
         workspace = empty(lookup_workspace_bytes(p, lp, batch) // 8, x_cmp.device)
+    if _words(workspace) * 8 < lookup_workspace_bytes(p, lp, batch):
+        raise ValueError(f"workspace holds {_words(workspace) * 8} bytes, the call needs "
+                         f"{lookup_workspace_bytes(p, lp, batch)}")
     c = np.ascontiguousarray(consts, np.uint64)
+    _expect(c, "consts", lp.nseg)
     _check(lib().rosetta_lookup_eval(_dev(x_rlwe, "x_rlwe"), _dev(x_cmp, "x_cmp"),
                                      _dev(bsk_dev, "bsk"), _dev(ksk_dev, "ksk"),
                                      _dev(autk_dev, "autk"), _dev(plain_prep, "plain_prep"),
