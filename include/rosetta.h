@@ -158,6 +158,29 @@ rosetta_status rosetta_pbs_batch_ws(const uint64_t *lwe_in, const uint64_t *bsk_
                                     const rosetta_params *params, void *workspace,
                                     size_t workspace_bytes, void *stream);
 
+/* Allocation-free rosetta_pbs_batch, for callers that cannot allocate device
+ * memory while they run: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments, layouts, validation and
+ * output bits as rosetta_pbs_batch (the same two kernels run); the scratch
+ * between them (the extracted ciphertexts, rosetta_pbs_workspace_bytes
+ * bytes) is a static device array of ROSETTA_NOALLOC_SCRATCH_BYTES that
+ * each GPU the library runs on holds until the process ends, and the
+ * twiddle tables are static device memory too.  Nothing is allocated: not
+ * on the first call on a device (which looks up that device's address of
+ * the array and uploads the twiddle table of N with hipMemcpy if no earlier
+ * call did), not later.  A batch whose scratch exceeds the array,
+ * batch * (N+1) * 8 > ROSETTA_NOALLOC_SCRATCH_BYTES (at most 4094
+ * ciphertexts at N = 2048, 2047 at N = 4096), is rejected with
+ * ROSETTA_ERR_SIZE before anything is enqueued.  All calls on one device
+ * share its array: calls on one stream run in order, but calls that overlap
+ * in time on one device (several streams or threads) race on it and give
+ * unspecified results.  The array needs no clearing between calls. */
+#define ROSETTA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+rosetta_status rosetta_pbs_batch_noalloc(const uint64_t *lwe_in, const uint64_t *bsk_dev,
+                                         const uint64_t *ksk_dev, const uint64_t *lut,
+                                         uint64_t *lwe_out, size_t batch,
+                                         const rosetta_params *params, void *stream);
+
 /* Steps a1-a6 alone: blind rotation, returning the GLWE accumulators
  * glwe_out [batch][2N] (device; must not overlap the inputs). */
 rosetta_status rosetta_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,

@@ -19,6 +19,8 @@
 
 using namespace rosetta;
 
+static __device__ __align__(256) uint64_t twiddle_store[256 + 512 + 1024 + 2048 + 4096];
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -95,13 +97,16 @@ bool any_overlap(const void *a, size_t na, const void *b, size_t nb) {
 
 // ---- per-device state ------------------------------------------------------
 
-struct DevTables {
-  uint64_t *zeta = nullptr;
-  uint64_t ninv = 0;
-};
+// Twiddle tables of every supported N live in one static device array (N
+// words each, at offset N - 256: 256 -> 0, 512 -> 256, .., 4096 -> 3840),
+// uploaded per device on first use of an N, so that no entry point ever
+// allocates memory for them.  Host code reaches the array only through the
+// address hipGetSymbolAddress returns on each device.
+constexpr size_t TWIDDLE_STORE_WORDS = 256 + 512 + 1024 + 2048 + 4096;
 
 struct DeviceState {
-  std::map<uint32_t, DevTables> tables;
+  uint64_t *twiddle_base = nullptr;  // this device's copy of twiddle_store
+  std::map<uint32_t, uint64_t> ninv;  // N -> N^-1, present once uploaded
   void *workspace = nullptr;
   size_t workspace_bytes = 0;
 };
@@ -117,13 +122,23 @@ uint32_t bitrev(uint32_t x, int bits) {
 }
 
 rosetta_status get_tables(uint32_t N, Tables &out) {
+  if (!is_pow2_in(N, 256, 4096))
+    return fail(ROSETTA_ERR_UNSUPPORTED, "no twiddle table for N = %u", N);
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   std::lock_guard<std::mutex> lock(g_mu);
   DeviceState &ds = g_dev[dev];
-  auto it = ds.tables.find(N);
-  if (it == ds.tables.end()) {
+  if (!ds.twiddle_base) {
+    e = hipGetSymbolAddress((void **)&ds.twiddle_base, HIP_SYMBOL(twiddle_store));
+    if (e != hipSuccess) {
+      ds.twiddle_base = nullptr;
+      return hip_fail(e, "hipGetSymbolAddress(twiddle_store)");
+    }
+  }
+  uint64_t *dst = ds.twiddle_base + (N - 256);
+  auto it = ds.ninv.find(N);
+  if (it == ds.ninv.end()) {
     const int logn = ilog2u(N);
     const u64 psi = gl_pow(7, (GL_P - 1) / (2 * (u64)N));
     std::vector<u64> z(N);
@@ -166,19 +181,13 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
         }
       }
     }
-    DevTables t;
-    e = hipMalloc(&t.zeta, z.size() * sizeof(u64));
-    if (e != hipSuccess) return hip_fail(e, "hipMalloc(twiddles)");
-    e = hipMemcpy(t.zeta, z.data(), z.size() * sizeof(u64), hipMemcpyHostToDevice);
-    if (e != hipSuccess) {
-      (void)hipFree(t.zeta);
-      return hip_fail(e, "hipMemcpy(twiddles)");
-    }
-    t.ninv = gl_inv(N);
-    it = ds.tables.emplace(N, t).first;
+    static_assert(256 + 512 + 1024 + 2048 + 4096 == TWIDDLE_STORE_WORDS, "table offsets");
+    e = hipMemcpy(dst, z.data(), z.size() * sizeof(u64), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(twiddles)");
+    it = ds.ninv.emplace(N, gl_inv(N)).first;
   }
-  out.zeta = it->second.zeta;
-  out.ninv = it->second.ninv;
+  out.zeta = dst;
+  out.ninv = it->second;
   return ROSETTA_OK;
 }
 
@@ -678,10 +687,11 @@ rosetta_status rosetta_shutdown(void) {
   for (auto &kv : g_dev) {
     (void)hipSetDevice(kv.first);
     (void)hipDeviceSynchronize();
-    for (auto &t : kv.second.tables) (void)hipFree(t.second.zeta);
+    // the twiddle tables stay: they live in static device memory
     if (kv.second.workspace) (void)hipFree(kv.second.workspace);
+    kv.second.workspace = nullptr;
+    kv.second.workspace_bytes = 0;
   }
-  g_dev.clear();
   (void)hipSetDevice(cur);
   return ok();
 }

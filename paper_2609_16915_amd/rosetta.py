@@ -66,6 +66,8 @@ SIGNATURES = {
     "rosetta_pbs_workspace_bytes": (C.c_size_t, [_pp, C.c_size_t]),
     "rosetta_pbs_batch_ws": (_ST, [_u64p, _u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp,
                                    C.c_void_p, C.c_size_t, C.c_void_p]),
+    "rosetta_pbs_batch_noalloc": (_ST, [_u64p, _u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp,
+                                        C.c_void_p]),
     "rosetta_blind_rotate": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp, C.c_void_p]),
     "rosetta_blind_rotate_extract": (_ST, [_u64p, _u64p, _u64p, _u64p, C.c_size_t, _pp,
                                            C.c_void_p]),
@@ -310,6 +312,22 @@ def pbs_batch_ws(lwe_in, bsk_dev, ksk_dev, lut, params, workspace, out=None, str
                                       _dev(workspace, "workspace"),
                                       workspace.numel() * workspace.element_size(),
                                       _stream(stream)))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def pbs_batch_noalloc(lwe_in, bsk_dev, ksk_dev, lut, params, out, stream=None):
+    """rosetta_pbs_batch_noalloc: the PBS with the library's static scratch
+    (the caller passes the output buffer; nothing is allocated)."""
+    p = _params(params)
+    batch = _check_pbs_args(p, lwe_in, bsk_dev, ksk_dev, lut)
+    _expect(out, "lwe_out", batch * (p.n + 1))
+    _check(lib().rosetta_pbs_batch_noalloc(_dev(lwe_in, "lwe_in"), _dev(bsk_dev, "bsk_dev"),
+                                           _dev(ksk_dev, "ksk_dev"), _dev(lut, "lut"),
+                                           _dev(out, "lwe_out"), batch, C.byref(p),
+                                           _stream(stream)))
     return out
 
 

@@ -38,9 +38,13 @@ def test_pbs_family(sizes):
         with pytest.raises(ValueError, match=name):
             R.pbs_batch(*bad, PRM)
         with pytest.raises(ValueError, match=name):
+            R.pbs_batch_noalloc(*bad, PRM, z(b * (n + 1)))
+        with pytest.raises(ValueError, match=name):
             R.pbs_batch_ws(*bad, PRM, z(b * (N + 1)))
     with pytest.raises(ValueError, match="lwe_out"):
         R.pbs_batch(*good, PRM, out=z(b * (n + 1) - 1))
+    with pytest.raises(ValueError, match="lwe_out"):
+        R.pbs_batch_noalloc(*good, PRM, z(b * (n + 1) + 1))
     with pytest.raises(ValueError, match="workspace"):
         R.pbs_batch_ws(*good, PRM, z(b * (N + 1) - 1))
     with pytest.raises(TypeError):
