@@ -86,7 +86,10 @@ typedef enum rosetta_status {
   ROSETTA_ERR_SIZE = 7         /* a caller-provided buffer is too small */
 } rosetta_status;
 
-/* Library version string. */
+/* Library version string, ending in "src:" and the first 16 hex digits of
+ * the SHA-256 of the sources the library was compiled from (every file of
+ * csrc/ and this header, each as its path then its bytes, in path order),
+ * so that a loaded library names the sources behind it. */
 const char *rosetta_version(void);
 
 /* Name of a status code. */
@@ -107,10 +110,14 @@ rosetta_status rosetta_check_params(const rosetta_params *params);
  * ceil((n+1)/32) * (N*l_ks/32) * 1024 words; otherwise the key words plus
  * n+1 column sums. */
 size_t rosetta_bsk_words(const rosetta_params *params);
+size_t rosetta_bsk_device_words(const rosetta_params *params); /* = rosetta_bsk_words */
 size_t rosetta_ksk_words(const rosetta_params *params);
 size_t rosetta_ksk_device_words(const rosetta_params *params);
 
 /* a0: bootstrapping-key preparation (once per key, not part of a PBS).
+ * The bootstrapping key is what blind rotation multiplies by (Sec. 2.2.2
+ * "TFHE Scheme", PBS item: the encrypted message drives the rotation, one
+ * GGSW encryption of each key bit s_i selecting X^(a~_i) or 1).
  * Transforms every GGSW row of `bsk_std_dev` (standard layout, device) into
  * the library's transform-domain layout in `bsk_dev` (device, same size,
  * must not overlap).  Rows are pre-scaled by N^-1 so that the inverse
@@ -118,7 +125,9 @@ size_t rosetta_ksk_device_words(const rosetta_params *params);
 rosetta_status rosetta_bsk_prepare(const uint64_t *bsk_std_dev, uint64_t *bsk_dev,
                                    const rosetta_params *params, void *stream);
 
-/* Key-switching-key preparation (once per key, not part of a PBS): writes
+/* Key-switching-key preparation (once per key, not part of a PBS; the key
+ * switch is the last step of the PBS, Sec. 2.2.2 "TFHE Scheme", PBS item,
+ * whose output is a fresh TFHE ciphertext under the input's key): writes
  * the prepared layout of the standard key `ksk_std_dev` into `ksk_dev`
  * (rosetta_ksk_device_words words, device, must not overlap):
  * the signed byte planes of every key word (each word w replaced by w or
@@ -128,7 +137,12 @@ rosetta_status rosetta_bsk_prepare(const uint64_t *bsk_std_dev, uint64_t *bsk_de
 rosetta_status rosetta_ksk_prepare(const uint64_t *ksk_std_dev, uint64_t *ksk_dev,
                                    const rosetta_params *params, void *stream);
 
-/* THE HOT PATH: programmable bootstrapping of `batch` LWE ciphertexts.
+/* THE HOT PATH: programmable bootstrapping of `batch` LWE ciphertexts
+ * (Sec. 2.2.2 "TFHE Scheme", PBS item, and Fig. rlwe_primitives(a): the
+ * table f in the coefficients of the test polynomial v, blind rotation by
+ * the encrypted message so that f(m) reaches the constant term, extraction
+ * of that term, Sec. 2.2.3 "LWE Extract", as a fresh ciphertext, then key
+ * switching back to the n-dimensional key).
  *   lwe_in   [batch][n+1]  device, canonical
  *   bsk_dev  prepared bootstrapping key (rosetta_bsk_prepare)
  *   ksk_dev  prepared key-switching key (rosetta_ksk_prepare)
@@ -181,13 +195,15 @@ rosetta_status rosetta_pbs_batch_noalloc(const uint64_t *lwe_in, const uint64_t 
                                          uint64_t *lwe_out, size_t batch,
                                          const rosetta_params *params, void *stream);
 
-/* Steps a1-a6 alone: blind rotation, returning the GLWE accumulators
+/* Steps a1-a6 alone: blind rotation (Sec. 2.2.2, PBS item: the RLWE
+ * encryption of the rotated test polynomial), returning the GLWE accumulators
  * glwe_out [batch][2N] (device; must not overlap the inputs). */
 rosetta_status rosetta_blind_rotate(const uint64_t *lwe_in, const uint64_t *bsk_dev,
                                     const uint64_t *lut, uint64_t *glwe_out, size_t batch,
                                     const rosetta_params *params, void *stream);
 
-/* Steps a1-a7: blind rotation and sample extraction, returning LWE
+/* Steps a1-a7: blind rotation and sample extraction (Sec. 2.2.3 "Scheme
+ * Conversion and Other Primitives", LWE Extract item), returning LWE
  * ciphertexts of dimension N under the GLWE key, big_out [batch][N+1]
  * (device; must not overlap the inputs). */
 rosetta_status rosetta_blind_rotate_extract(const uint64_t *lwe_in, const uint64_t *bsk_dev,
@@ -195,7 +211,8 @@ rosetta_status rosetta_blind_rotate_extract(const uint64_t *lwe_in, const uint64
                                             size_t batch, const rosetta_params *params,
                                             void *stream);
 
-/* Step a8: key switching of big_in [batch][N+1] to lwe_out [batch][n+1]
+/* Step a8: key switching (the PBS's return to the input key, Sec. 2.2.2,
+ * PBS item) of big_in [batch][N+1] to lwe_out [batch][n+1]
  * (device; must not overlap). */
 rosetta_status rosetta_keyswitch(const uint64_t *big_in, const uint64_t *ksk_dev,
                                  uint64_t *lwe_out, size_t batch, const rosetta_params *params,
@@ -517,7 +534,10 @@ rosetta_status rosetta_encode_fixed(const double *v, size_t count, int scale_log
 
 /* ---- test helpers: host memory, deterministic from the seed ------------ */
 
-/* Binary keys and the two switching keys in standard layout (host arrays of
+/* Key generation for the PBS (Sec. 2.2.2 "TFHE Scheme": LWE encryption of
+ * scalars, the GGSW bootstrapping key of blind rotation, and the
+ * key-switching key that returns its output to the LWE key).
+ * Binary keys and the two switching keys in standard layout (host arrays of
  * n, N, rosetta_bsk_words and rosetta_ksk_words words).  Randomness is
  * SplitMix64 used as a counter-based generator (Steele, Lea and Flood 2014):
  * word(key, i) = mix(key + (i+1) * 0x9E3779B97F4A7C15); sub-stream keys
@@ -531,7 +551,8 @@ rosetta_status rosetta_keygen(uint64_t seed, const rosetta_params *params, doubl
                               double sigma_glwe, uint64_t *lwe_key, uint64_t *glwe_key,
                               uint64_t *bsk_std, uint64_t *ksk_std);
 
-/* Encryption of msgs[count] (values in Z_2M) under a binary key of length
+/* TFHE-Enc of Sec. 2.2.2 "TFHE Scheme" (Encryption and Decryption item):
+ * encryption of msgs[count] (values in Z_2M) under a binary key of length
  * `dim` (host): masks from stream 7 word q*dim+c, noise from stream 8
  * Gaussian q, of sub-stream keys of `seed`. */
 rosetta_status rosetta_lwe_encrypt(uint64_t seed, const rosetta_params *params, double sigma,
@@ -544,12 +565,17 @@ rosetta_status rosetta_lwe_encrypt_plain(uint64_t seed, double sigma, const uint
                                          uint32_t dim, const uint64_t *plain, size_t count,
                                          uint64_t *lwe_out);
 
-/* Decryption of `count` ciphertexts of dimension `dim` to Z_2M (host). */
+/* TFHE-Dec of Sec. 2.2.2 "TFHE Scheme" (Encryption and Decryption item):
+ * decryption of `count` ciphertexts of dimension `dim` to Z_2M (host):
+ * m = floor((2M (b - <a, s>) + (p-1)/2) / p) mod 2M. */
 rosetta_status rosetta_lwe_decrypt(const rosetta_params *params, const uint64_t *key,
                                    uint32_t dim, const uint64_t *lwe, size_t count,
                                    uint32_t *msgs_out);
 
-/* Test polynomial [N] for a table of M entries in Z_2M (host). */
+/* Test polynomial v [N] for a table of M entries in Z_2M (host): the LUT
+ * entries laid out as coefficients (Sec. 2.2.2 "TFHE Scheme", PBS item, and
+ * Fig. rlwe_primitives(a)), with the padding-bit, half-box layout of the
+ * CONVENTIONS above. */
 rosetta_status rosetta_lut_build(const rosetta_params *params, const uint32_t *table,
                                  uint64_t *test_poly);
 

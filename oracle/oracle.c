@@ -629,7 +629,7 @@ static void or_br_loop(const or_params *P, const u64 *lwe, const u64 *bsk, const
       for (int j = 0; j < N; ++j)
         diff[(size_t)u * N + j] = or_sub(rot[(size_t)u * N + j], acc[(size_t)u * N + j]);
     }
-    const u64 *G = bsk + (size_t)i * ggsw_words;
+    const u64 *G = bsk ? bsk + (size_t)i * ggsw_words : NULL; /* NULL: fbsk only */
     if (kind == OR_SCHOOLBOOK) {
       or_external_product(P, G, diff, prod, OR_SCHOOLBOOK);
     } else {
@@ -703,15 +703,29 @@ void or_keyswitch(const or_params *P, const u64 *big, const u64 *ksk, u64 *out) 
  * switching.  Optional outputs: the GLWE accumulators [count][2N] and the
  * extracted ciphertexts [count][N+1].  Ciphertexts are independent; they are
  * spread over `nthreads` OpenMP threads (<= 0: the runtime default). */
+void or_pbs_prepared(const or_params *P, const u64 *lwe_in, const u64 *bsk, const u64 *fbsk,
+                     const u64 *ksk, const u64 *v, u64 *lwe_out, u64 *big_out, u64 *acc_out,
+                     size_t count, int kind, int nthreads);
+
 void or_pbs(const or_params *P, const u64 *lwe_in, const u64 *bsk, const u64 *ksk, const u64 *v,
             u64 *lwe_out, u64 *big_out, u64 *acc_out, size_t count, int kind, int nthreads) {
-  int n = (int)P->n, N = (int)P->N;
   int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
   u64 *fbsk = NULL;
   if (kind == OR_NTT) {
     fbsk = (u64 *)malloc(or_bsk_words(P) * sizeof(u64));
     or_bsk_transform(P, bsk, fbsk, nt);
   }
+  or_pbs_prepared(P, lwe_in, bsk, fbsk, ksk, v, lwe_out, big_out, acc_out, count, kind, nt);
+  free(fbsk);
+}
+
+/* or_pbs with the key's transform (or_bsk_transform) done by the caller:
+ * `fbsk` holds it for kind == OR_NTT (NULL: rows transformed when used). */
+void or_pbs_prepared(const or_params *P, const u64 *lwe_in, const u64 *bsk, const u64 *fbsk,
+                     const u64 *ksk, const u64 *v, u64 *lwe_out, u64 *big_out, u64 *acc_out,
+                     size_t count, int kind, int nthreads) {
+  int n = (int)P->n, N = (int)P->N;
+  int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
 #pragma omp parallel num_threads(nt)
   {
     u64 *acc = (u64 *)malloc((size_t)2 * N * sizeof(u64));
@@ -727,7 +741,6 @@ void or_pbs(const or_params *P, const u64 *lwe_in, const u64 *bsk, const u64 *ks
     free(acc);
     free(big);
   }
-  free(fbsk);
 }
 
 /* ------------------------------------------------------------------------- */

@@ -102,6 +102,8 @@ def _declare(L):
         "or_keyswitch": (None, [_pp, _u64p, _u64p, _u64p]),
         "or_pbs": (None, [_pp, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p, C.c_size_t,
                           C.c_int, C.c_int]),
+        "or_pbs_prepared": (None, [_pp, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p,
+                                   C.c_size_t, C.c_int, C.c_int]),
         "or_blind_rotate_glwe": (None, [_pp, _u64p, _u64p, _u64p, _u64p, _u64p, C.c_int]),
         "or_automorphism": (None, [_u64p, C.c_int, _u64p, C.c_int]),
         "or_glwe_keyswitch": (None, [C.c_int, C.c_int, C.c_int, _u64p, _u64p, _u64p, C.c_int]),
@@ -321,6 +323,26 @@ def pbs(params: Params, lwe_in, bsk, ksk, v, kind=NTT, nthreads=0,
     if want_acc:
         res.append(acc)
     return res[0] if len(res) == 1 else tuple(res)
+
+
+def bsk_transform(params: Params, bsk, nthreads=0) -> np.ndarray:
+    """Forward transform of every bootstrapping-key row (the tier-2 PBS's
+    once-per-key work)."""
+    bsk = _u64(bsk)
+    out = np.zeros_like(bsk)
+    lib().or_bsk_transform(C.byref(params), _ptr(bsk), _ptr(out), nthreads)
+    return out
+
+
+def pbs_prepared(params: Params, lwe_in, fbsk, ksk, v, nthreads=0) -> np.ndarray:
+    """Tier-2 PBS of a batch with the key transform already done
+    (bsk_transform): returns lwe_out."""
+    lwe_in = _u64(lwe_in).reshape(-1, params.n + 1)
+    fbsk, ksk, v = _u64(fbsk), _u64(ksk), _u64(v)
+    out = np.zeros((lwe_in.shape[0], params.n + 1), dtype=np.uint64)
+    lib().or_pbs_prepared(C.byref(params), _ptr(lwe_in), None, _ptr(fbsk), _ptr(ksk), _ptr(v),
+                          _ptr(out), None, None, lwe_in.shape[0], NTT, nthreads)
+    return out
 
 
 # --------------------------------------------------------------------------

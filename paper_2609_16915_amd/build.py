@@ -43,8 +43,26 @@ FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",
 TRANSFORM_FLAGS = ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]
 
 
-def _flags(src: str):
-    return FLAGS + (TRANSFORM_FLAGS if src == "kernels.hip" else [])
+def source_digest() -> str:
+    """First 16 hex digits of the SHA-256 over every source the library is
+    built from (csrc/ and include/rosetta.h: each file's name, then its
+    bytes, in name order).  The build bakes it into rosetta_version(), so a
+    loaded library names the sources it was compiled from."""
+    import hashlib
+    files = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
+                   if f.endswith((".hip", ".cpp", ".hpp", ".h")))
+    files.append(os.path.join(INCLUDE, "rosetta.h"))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.relpath(f, ROOT).encode() + b"\0")
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _flags(src: str, digest: str):
+    return (FLAGS + [f'-DROSETTA_SOURCE_DIGEST="{digest}"'] +
+            (TRANSFORM_FLAGS if src == "kernels.hip" else []))
 
 
 def _filter(stderr: str) -> str:
@@ -57,7 +75,8 @@ def build(verbose: bool = False) -> str:
     import tempfile
     with tempfile.TemporaryDirectory(prefix="rosetta_build_") as tmpdir:
         objs = [os.path.join(tmpdir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
-        cmds = [[hipcc(), *_flags(s), "-c", os.path.join(CSRC, s), "-o", o]
+        digest = source_digest()
+        cmds = [[hipcc(), *_flags(s, digest), "-c", os.path.join(CSRC, s), "-o", o]
                 for s, o in zip(SOURCES, objs)]
         if verbose:
             for c in cmds:

@@ -225,7 +225,12 @@ void rosetta::set_last_error(const char *msg) { g_last_error = msg; }
 
 extern "C" {
 
-const char *rosetta_version(void) { return "rosetta-pbs 0.1.0 (gfx950)"; }
+#ifndef ROSETTA_SOURCE_DIGEST
+#define ROSETTA_SOURCE_DIGEST "unknown"
+#endif
+const char *rosetta_version(void) {
+  return "rosetta-pbs 0.2.0 (gfx950) src:" ROSETTA_SOURCE_DIGEST;
+}
 
 const char *rosetta_status_string(int st) {
   switch (st) {
@@ -251,6 +256,8 @@ rosetta_status rosetta_check_params(const rosetta_params *params) {
 size_t rosetta_bsk_words(const rosetta_params *p) {
   return p ? (size_t)p->n * 2 * p->pbs_level * 2 * p->N : 0;
 }
+
+size_t rosetta_bsk_device_words(const rosetta_params *p) { return rosetta_bsk_words(p); }
 
 size_t rosetta_ksk_words(const rosetta_params *p) {
   return p ? (size_t)p->N * p->ks_level * (p->n + 1) : 0;

@@ -57,6 +57,7 @@ SIGNATURES = {
     "rosetta_last_error": (C.c_char_p, []),
     "rosetta_check_params": (_ST, [_pp]),
     "rosetta_bsk_words": (C.c_size_t, [_pp]),
+    "rosetta_bsk_device_words": (C.c_size_t, [_pp]),
     "rosetta_ksk_words": (C.c_size_t, [_pp]),
     "rosetta_ksk_device_words": (C.c_size_t, [_pp]),
     "rosetta_bsk_prepare": (_ST, [_u64p, _u64p, _pp, C.c_void_p]),
@@ -236,6 +237,11 @@ def to_host(t) -> np.ndarray:
 
 def bsk_words(params) -> int:
     return lib().rosetta_bsk_words(C.byref(_params(params)))
+
+
+def version() -> str:
+    """rosetta_version(): the version and the digest of the sources built."""
+    return lib().rosetta_version().decode()
 
 
 def ksk_words(params) -> int:

@@ -42,6 +42,22 @@ def test_status_strings(L):
     assert L.rosetta_version().decode().startswith("rosetta-pbs")
 
 
+def test_version_names_the_built_sources(L):
+    """rosetta_version() carries the digest of the sources the library was
+    compiled from; it must equal the digest of the sources in the tree (a
+    stale library, built before a source change, fails here)."""
+    from paper_2609_16915_amd import build as B
+    v = L.rosetta_version().decode()
+    assert v.endswith("src:" + B.source_digest()), (v, B.source_digest())
+
+
+def test_bsk_device_words_is_the_standard_size(L):
+    for kw in (dict(), dict(n=1024, N=2048, pbs_level=3), dict(n=7, N=4096, pbs_level=4)):
+        p = P(**kw)
+        assert L.rosetta_bsk_device_words(C.byref(p)) == L.rosetta_bsk_words(C.byref(p)) == \
+            p.n * 2 * p.pbs_level * 2 * p.N
+
+
 def P(**kw):
     base = dict(n=64, k=1, N=256, pbs_level=2, pbs_base_log=8, ks_level=3, ks_base_log=4,
                 msg_bits=3)
