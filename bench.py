@@ -266,6 +266,148 @@ def lookup_protocol(R, W, w, p, keys, bsk, ksk, stream, steps, batch):
                               "max_abs_err": float(err.max())}}
 
 
+# Precision of the encrypted lookup (Algorithm 1) against the paper's
+# primitive tables: (function, range, boundary spacing, bits the paper
+# reports for its segmented LUT).
+PRECISION_CASES = [("silu", -20.0, 20.0, "uniform", 16.8), ("gelu", -20.0, 20.0, "uniform", 15.5),
+                   ("inv", 0.01, 10.0, "log", 12.7), ("inv", 0.01, 100.0, "log", 12.5),
+                   ("inv_sqrt", 0.01, 10.0, "log", 16.7), ("inv_sqrt", 0.01, 100.0, "log", 12.7)]
+
+
+def _exact(fn, x):
+    import math
+    if fn == "silu":
+        return x / (1.0 + np.exp(-x))
+    if fn == "gelu":
+        return 0.5 * x * (1.0 + np.array([math.erf(v / math.sqrt(2.0)) for v in x]))
+    if fn == "inv":
+        return 1.0 / x
+    if fn == "inv_sqrt":
+        return 1.0 / np.sqrt(x)
+    raise ValueError(fn)
+
+
+def _bits(err) -> float:
+    return float(-np.log2(np.sqrt(np.mean(np.square(err)))))
+
+
+def _lwe_phase(cts, key):
+    """b - <a, s> mod p, exact (Python integers)."""
+    P = 0xFFFFFFFF00000001
+    n = key.shape[0]
+    sel = np.nonzero(key)[0]
+    return np.array([(int(c[n]) - sum(int(v) for v in c[sel])) % P for c in cts], dtype=object)
+
+
+def _modswitched_phase(cts, key, N):
+    """b~ - sum a~_i s_i mod 2N with a~ = nearest integer to 2N a / p: the
+    rotation a blind rotation by these ciphertexts applies."""
+    P = 0xFFFFFFFF00000001
+    n = key.shape[0]
+    sel = np.nonzero(key)[0]
+    ms = lambda a: ((2 * N * int(a) + (P - 1) // 2) // P) % (2 * N)
+    return np.array([(ms(c[n]) - sum(ms(v) for v in c[sel])) % (2 * N) for c in cts])
+
+
+def lookup_precision(R, w, p, keys, bsk, ksk, stream, count: int):
+    """Encrypted lookup precision, -log2 RMSE over `count` inputs drawn
+    uniformly from each range of the paper's primitive tables, 4 segments,
+    at the headline ring and keys.  The error is split into its sources:
+    the segmented LUT itself (cleartext, exact indices), the interval the
+    blind rotation of Step 3 actually selected (from the decrypted segment
+    index S and the modulus-switched selector I, both read from the
+    workspace), and what remains (value noise of the traces and products).
+    The selector's error is split too: the key switch's noise on I (its
+    decrypted phase against the exact t) and the modulus switch's drift
+    (the modulus-switched phase against the decrypted one)."""
+    import torch
+    P = 0xFFFFFFFF00000001
+    N, n, nseg, margin = w.N, w.n, 4, 192
+    nbr = N - 2 * margin
+    sx = 40
+    sp = 63 - int(math.log2(N)) - sx
+    autk = R.autk_prepare(R.to_device(R.autk_keygen(w.key_seed + 1, p, TRACE_LEVEL,
+                                                    TRACE_BASE_LOG, w.sigma_glwe,
+                                                    keys["glwe_key"])), p, TRACE_LEVEL)
+    rows = []
+    for k, (fn, lo, hi, spacing, paper) in enumerate(PRECISION_CASES):
+        tau = R.seglut_boundaries(lo, hi, nseg, spacing)
+        a, b = R.seglut_build(fn, tau, nbr)
+        grid = np.linspace(lo, hi, 20001)
+        fmax = float(np.max(np.abs(_exact(fn, grid))))
+        reach = max(max(abs(lo - t), abs(hi - t)) for t in tau[1:-1])
+        sc = int(math.floor(math.log2(2.0 ** 62 / reach)))
+        sv = int(math.floor(62.5 - math.log2(fmax))) - sx
+        lp = R.LookupParams(nseg=nseg, nbr=nbr, margin=margin, x_scale_log=sx,
+                            coef_scale_log=sp, val_scale_log=sv, cmp_scale_log=sc,
+                            trace_level=TRACE_LEVEL, trace_base_log=TRACE_BASE_LOG)
+        plain, consts = R.lookup_encode(p, lp, tau, a, b)
+        prep = R.lookup_prepare(R.to_device(plain), p, lp)
+        xs = np.random.default_rng(w.data_seed + 10 + k).uniform(lo, hi, count)
+        m = np.zeros((count, N), np.uint64)
+        m[:, 0] = R.encode_fixed(xs, sx)
+        x_rlwe = R.to_device(R.glwe_encrypt(w.enc_seed + 10 + k, p, w.sigma_glwe,
+                                            keys["glwe_key"], m))
+        x_cmp = R.to_device(R.lwe_encrypt_plain(w.enc_seed + 20 + k, p, w.sigma_lwe,
+                                                keys["lwe_key"], R.encode_fixed(xs, sc)))
+        ws = R.empty(R.lookup_workspace_bytes(p, lp, count) // 8)
+        out = R.lookup_eval(x_rlwe, x_cmp, bsk, ksk, autk, prep, consts, p, lp, workspace=ws)
+        torch.cuda.synchronize()
+        ph = R.glwe_phase(p, keys["glwe_key"], R.to_host(out))[:, 0].astype(object)
+        y = np.array([(v if v <= P // 2 else v - P) / 2.0 ** (sx + sv) for v in ph])
+        wsh = R.to_host(ws)
+        oS = R.lookup_workspace_offset(p, lp, count, R.LOOKUP_PART_S)
+        oI = R.lookup_workspace_offset(p, lp, count, R.LOOKUP_PART_I)
+        S_ct = wsh[oS:oS + count * (n + 1)].reshape(count, n + 1)
+        I_ct = wsh[oI:oI + count * (n + 1)].reshape(count, n + 1)
+        key = keys["lwe_key"]
+        S_dec = np.array([int(round(float(v) * 2 * nseg / P)) % (2 * nseg)
+                          for v in _lwe_phase(S_ct, key)])
+        I_ph = np.array([float(v) * 2 * N / P for v in _lwe_phase(I_ct, key)])
+        rot = _modswitched_phase(I_ct, key, N)
+        # exact segment, interval and selector value
+        S_true = np.array([int(np.sum(x >= tau[1:-1])) for x in xs])
+        width = tau[S_true + 1] - tau[S_true]
+        t_true = nbr * (xs - tau[S_true]) / width + margin - 0.5
+        i_true = np.clip(np.floor(nbr * (xs - tau[S_true]) / width), 0, nbr - 1).astype(int)
+        centred = lambda d, M: (d + M / 2) % M - M / 2
+        ok = S_dec == S_true
+        ks_noise = centred(I_ph - t_true, 2 * N)[ok]
+        drift = centred(rot - I_ph, 2 * N)[ok]
+        S_used = np.clip(S_dec, 0, nseg - 1)
+        # the rotation moves coefficient rot of r_S to the constant term;
+        # beyond N the negacyclic wrap negates coefficient rot - N, and
+        # coefficient j holds interval clamp(j - margin)
+        i_sel = np.clip(rot % N - margin, 0, nbr - 1).astype(int)
+        sign = np.where(rot >= N, -1.0, 1.0)
+        y_sel = sign * (a[S_used, i_sel] * xs + b[S_used, i_sel])
+        y_lut = a[S_true, i_true] * xs + b[S_true, i_true]
+        f = _exact(fn, xs)
+        sim = R.seglut_precision(fn, tau, a, b, xs,
+                                 np.rint(np.random.default_rng(7).normal(
+                                     0, float(np.sqrt(np.mean(np.square(ks_noise + drift)))),
+                                     count)).astype(np.int32))
+        rows.append({"function": fn, "range": [lo, hi], "spacing": spacing, "inputs": count,
+                     "scales": {"x": sx, "coef": sp, "val": sv, "cmp": sc},
+                     "bits_vs_exact": round(_bits(y - f), 2),
+                     "bits_vs_cleartext_lut": round(_bits(y - y_lut), 2),
+                     "paper_bits": paper,
+                     "sources_bits": {"cleartext_lut_vs_exact": round(_bits(y_lut - f), 2),
+                                      "selection_vs_cleartext_lut": round(_bits(y_sel - y_lut), 2),
+                                      "value_noise": round(_bits(y - y_sel), 2)},
+                     "segment_misses": int(np.sum(~ok)),
+                     "selector_steps_rms": {"key_switch_noise": round(float(np.sqrt(np.mean(
+                                                ks_noise ** 2))), 2),
+                                            "modulus_switch_drift": round(float(np.sqrt(np.mean(
+                                                drift ** 2))), 2)},
+                     "interval_error_rms": round(float(np.sqrt(np.mean(
+                         (i_sel - i_true)[ok].astype(float) ** 2))), 2),
+                     "simulated_bits_at_measured_selector_rms": round(sim, 2)})
+        log(f"[precision] {fn} [{lo}, {hi}]: {rows[-1]['bits_vs_exact']} bits "
+            f"(paper {paper})")
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -282,6 +424,9 @@ def main():
                     help="timed steps of the full lookup pipeline (0 = skip)")
     ap.add_argument("--protocol-batch", type=int, default=0,
                     help="inputs of the lookup pipeline (default: the workload's batch)")
+    ap.add_argument("--precision", type=int, default=0,
+                    help="instead of the benchmark: encrypted lookup precision in bits over "
+                         "this many uniform inputs per primitive of the paper's tables")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB, outside the timed "
                          "region, as the reference kernel for memory-traffic counters")
@@ -314,6 +459,11 @@ def main():
 
     bsk = R.bsk_prepare(R.to_device(keys["bsk"]), p)
     ksk = R.ksk_prepare(R.to_device(keys["ksk"]), p)
+    if args.precision:
+        rows = lookup_precision(R, w, p, keys, bsk, ksk, stream, args.precision)
+        print(json.dumps({"lookup_precision": rows, "workload": name, "library": R.version()}),
+              flush=True)
+        return
     d_in, d_v = R.to_device(cts), R.to_device(v)
     d_out = R.empty((w.batch, w.n + 1))
     ws = R.empty(R.pbs_workspace_bytes(p, w.batch) // 8)

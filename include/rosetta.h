@@ -462,6 +462,19 @@ rosetta_status rosetta_lookup_prepare(const uint64_t *plain_dev, uint64_t *plain
 size_t rosetta_lookup_workspace_bytes(const rosetta_params *params,
                                       const rosetta_lookup_params *lp, size_t batch);
 
+/* Where rosetta_lookup_eval leaves its intermediates in the workspace, so
+ * that a caller holding the keys can inspect them after the call: the word
+ * offset of part `part` for `batch` inputs, or (size_t)-1 for an unknown
+ * part.  Parts: ROSETTA_LOOKUP_PART_CMP, the comparison results
+ * [batch][nseg-1][n+1] (LWE); ROSETTA_LOOKUP_PART_S, the segment index S
+ * [batch][n+1] (LWE, S at scale 2 floor(p / 4 nseg)); ROSETTA_LOOKUP_PART_I,
+ * the interval selector I [batch][n+1] (LWE, one rotation step p / 2N per
+ * unit). */
+enum { ROSETTA_LOOKUP_PART_CMP = 2, ROSETTA_LOOKUP_PART_S = 3, ROSETTA_LOOKUP_PART_I = 6 };
+size_t rosetta_lookup_workspace_offset(const rosetta_params *params,
+                                       const rosetta_lookup_params *lp, size_t batch,
+                                       uint32_t part);
+
 /* Steps 1-3 for a batch: x_rlwe [batch][2N], x_cmp [batch][n+1], prepared
  * keys (bootstrapping, key switching, automorphism), the prepared plaintext
  * block and the host constants; out [batch][2N] (device, not overlapping the

@@ -107,7 +107,7 @@ struct Scratch {
 
 // Workspace layout of rosetta_lookup_eval (words), in call order.
 size_t lookup_ws_words(const rosetta_params *p, const rosetta_lookup_params *lp, size_t batch,
-                       uint64_t **parts, void *base) {
+                       uint64_t **parts, void *base, size_t *offsets = nullptr) {
   const size_t N = p->N, w = p->n + 1, ns = lp->nseg, nc = ns - 1;
   Scratch sc(base);
   const size_t sizes[] = {
@@ -124,6 +124,7 @@ size_t lookup_ws_words(const rosetta_params *p, const rosetta_lookup_params *lp,
       batch * 2 * N,         // 10 R spread over the windows
   };
   for (int i = 0; i < 11; ++i) {
+    if (offsets) offsets[i] = sc.off;
     uint64_t *q = sc.take(sizes[i]);
     if (parts) parts[i] = q;
   }
@@ -219,6 +220,17 @@ size_t rosetta_lookup_workspace_bytes(const rosetta_params *p, const rosetta_loo
                                       size_t batch) {
   if (!p || !lp || lp->nseg < 2) return 0;
   return lookup_ws_words(p, lp, batch, nullptr, nullptr) * 8;
+}
+
+size_t rosetta_lookup_workspace_offset(const rosetta_params *p, const rosetta_lookup_params *lp,
+                                       size_t batch, uint32_t part) {
+  if (!p || !lp || lp->nseg < 2) return (size_t)-1;
+  if (part != ROSETTA_LOOKUP_PART_CMP && part != ROSETTA_LOOKUP_PART_S &&
+      part != ROSETTA_LOOKUP_PART_I)
+    return (size_t)-1;
+  size_t offsets[11];
+  lookup_ws_words(p, lp, batch, nullptr, nullptr, offsets);
+  return offsets[part];
 }
 
 rosetta_status rosetta_lookup_eval(const uint64_t *x_rlwe, const uint64_t *x_cmp,

@@ -137,6 +137,7 @@ SIGNATURES.update({
     "rosetta_lookup_encode": (_ST, [_pp, _lpp, _u64p, _u64p, _u64p, _u64p, _u64p]),
     "rosetta_lookup_prepare": (_ST, [_u64p, _u64p, _pp, _lpp, C.c_void_p]),
     "rosetta_lookup_workspace_bytes": (C.c_size_t, [_pp, _lpp, C.c_size_t]),
+    "rosetta_lookup_workspace_offset": (C.c_size_t, [_pp, _lpp, C.c_size_t, C.c_uint32]),
     "rosetta_lookup_eval": (_ST, [_u64p, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p, _u64p,
                                   C.c_size_t, _pp, _lpp, _u64p, C.c_size_t, C.c_void_p]),
 })
@@ -760,6 +761,19 @@ def lookup_prepare(plain_dev, params, lp: LookupParams, out=None, stream=None):
 
 def lookup_workspace_bytes(params, lp: LookupParams, batch: int) -> int:
     return lib().rosetta_lookup_workspace_bytes(C.byref(_params(params)), C.byref(lp), batch)
+
+
+LOOKUP_PART_CMP, LOOKUP_PART_S, LOOKUP_PART_I = 2, 3, 6
+
+
+def lookup_workspace_offset(params, lp: LookupParams, batch: int, part: int) -> int:
+    """Word offset of an intermediate of rosetta_lookup_eval in its workspace
+    (LOOKUP_PART_CMP, LOOKUP_PART_S or LOOKUP_PART_I)."""
+    off = lib().rosetta_lookup_workspace_offset(C.byref(_params(params)), C.byref(lp), batch,
+                                                part)
+    if off == (1 << 64) - 1:
+        raise ValueError(f"unknown lookup workspace part {part}")
+    return off
 
 
 def lookup_eval(x_rlwe, x_cmp, bsk_dev, ksk_dev, autk_dev, plain_prep, consts, params,

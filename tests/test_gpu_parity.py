@@ -229,15 +229,59 @@ def test_keyswitch_rows_independent_of_batch_tiling(O, torch_dev):
 
 FULL = ["gpt2_gelu", "tinyllama_silu", "llama3_8b_silu", "llama3_8b_softmax_exp",
         "llama3_8b_softmax_recip"]
-# decryption of the key-switched output recovers T[m] except for the
-# noise-induced misses these parameter sets have (the two largest
-# parameter sets drift by a visible fraction of a box)
-MIN_DECRYPT_RATE = {"gpt2_gelu": 0.999, "tinyllama_silu": 0.999, "llama3_8b_silu": 0.85,
-                    "llama3_8b_softmax_exp": 0.40, "llama3_8b_softmax_recip": 0.40}
+# Decryption of the key-switched output recovers T[m] except for the misses
+# the noise of these parameter sets implies (binary keys, uniform modulus-
+# switch rounding: the drift is about sqrt(n/24) rotation steps against half
+# a box of N/2M, and the key switch adds about 2^-9 p): about 1e-30 and 2e-5
+# misses for the two n = 742 sets, about 5 % at n = 1024, N = 2048, 6-bit
+# messages and about 49 % at N = 4096, 7-bit messages.  The extracted
+# ciphertexts (before the key switch, noise about 2^-16 p) miss only by the
+# drift: about 1.4 % at n = 1024.
+MIN_DECRYPT_RATE = {"gpt2_gelu": 0.9999, "tinyllama_silu": 0.999, "llama3_8b_silu": 0.94,
+                    "llama3_8b_softmax_exp": 0.50, "llama3_8b_softmax_recip": 0.40}
+MIN_EXTRACTED_RATE = {"gpt2_gelu": 0.9999, "tinyllama_silu": 0.999, "llama3_8b_silu": 0.98,
+                      "llama3_8b_softmax_exp": 0.98, "llama3_8b_softmax_recip": 0.90}
+
+
+def resident_workgroups(N: int) -> int:
+    """Blind-rotation workgroups the chip holds at once (256 CUs x 3
+    workgroups up to N = 2048, one at N = 4096): a batch runs in rounds of
+    this many ciphertexts."""
+    return 256 * (3 if N <= 2048 else 1)
+
+
+def dense_picks(batch: int, N: int, seed: int):
+    """At least 64 ciphertexts (the whole batch when it is smaller): both
+    ends of the first, the second and the last residency round (the last
+    one partial unless the batch is a multiple of the round), 48 evenly
+    spaced across the batch, and one at random in each of up to 16 rounds
+    drawn at random."""
+    R = resident_workgroups(N)
+    rounds = (batch + R - 1) // R
+    last = (rounds - 1) * R
+    picks = {0, 1, min(R - 1, batch - 1), min(R, batch - 1), min(2 * R - 1, batch - 1),
+             last, min(last + 1, batch - 1), batch - 2 if batch > 1 else 0, batch - 1}
+    picks |= {int(x) for x in np.linspace(0, batch - 1, 48)}
+    rng = np.random.default_rng(seed)
+    for r in rng.choice(rounds, size=min(16, rounds), replace=False):
+        lo, hi = r * R, min(batch, (r + 1) * R)
+        picks.add(int(rng.integers(lo, hi)))
+    extra = iter(rng.permutation(batch))
+    while len(picks) < min(64, batch):
+        picks.add(int(next(extra)))
+    return sorted(picks)
 
 
 @pytest.mark.parametrize("name", FULL)
-def test_full_workload_sampled_parity(O, torch_dev, name):
+def test_full_workload_dense_parity(O, torch_dev, name):
+    """The whole batch in the benchmark's launch configuration (blind
+    rotation + extraction into one buffer, then the key switch, the two
+    kernels rosetta_pbs_batch runs), compared with the oracle on at least 64
+    ciphertexts spread over every residency round the batch runs in (first,
+    second, last and partial last included), both the extracted and the
+    key-switched ciphertexts of that one launch; then the single entry point
+    on the same inputs: bit-identical to the pair (determinism across
+    launches); then decryption rates over the whole batch."""
     torch = torch_dev
     w, op, ks, bsk, ksk = keyset(O, name)
     msgs = w.messages()
@@ -246,22 +290,31 @@ def test_full_workload_sampled_parity(O, torch_dev, name):
     table = w.table()
     v = O.test_poly(op, table)
     d_in, d_v = R.to_device(cts), R.to_device(v)
-    say(f"[{name}] GPU PBS of {w.batch}")
-    out = R.pbs_batch(d_in, bsk, ksk, d_v, w.params())
+    say(f"[{name}] GPU: blind rotation + extraction, key switch of {w.batch}")
+    big_dev = R.blind_rotate_extract(d_in, bsk, d_v, w.params())
+    out_dev = R.keyswitch(big_dev, ksk, w.params())
     torch.cuda.synchronize()
-    out = R.to_host(out)
-    rng = np.random.default_rng(w.data_seed)
-    picks = sorted({0, w.batch - 1, *rng.choice(w.batch, size=min(6, w.batch), replace=False)})
-    say(f"[{name}] oracle on {len(picks)} sampled ciphertexts")
+    big, out = R.to_host(big_dev), R.to_host(out_dev)
+    del big_dev
+    picks = dense_picks(w.batch, w.N, w.data_seed)
+    assert len(picks) >= min(64, w.batch)
+    say(f"[{name}] oracle on {len(picks)} ciphertexts over "
+        f"{-(-w.batch // resident_workgroups(w.N))} residency rounds")
     ref_out, ref_big = O.pbs(op, cts[picks], ks.bsk, ks.ksk, v, O.NTT, 0, want_big=True)
-    assert np.array_equal(out[picks], ref_out)
-    big = R.to_host(R.blind_rotate_extract(R.to_device(cts[picks]), bsk, d_v, w.params()))
-    assert np.array_equal(big, ref_big)
+    for i, q in enumerate(picks):
+        assert np.array_equal(big[q], ref_big[i]), f"extracted ciphertext {q}"
+        assert np.array_equal(out[q], ref_out[i]), f"key-switched ciphertext {q}"
+    say(f"[{name}] GPU: rosetta_pbs_batch on the same inputs")
+    again = R.to_host(R.pbs_batch(d_in, bsk, ksk, d_v, w.params()))
+    assert np.array_equal(again, out), "a second launch gave other bits"
     # properties over the whole batch
-    assert np.all(out < np.uint64(P))
+    assert np.all(out < np.uint64(P)) and np.all(big < np.uint64(P))
     rate = np.mean(O.lwe_decrypt(op, ks.lwe_key, out) == table[msgs])
-    say(f"[{name}] decrypt(PBS(Enc m)) = T[m] on {rate:.4%} of {w.batch}")
+    rate_big = np.mean(O.lwe_decrypt(op, ks.glwe_key, big) == table[msgs])
+    say(f"[{name}] decrypt = T[m]: key-switched {rate:.4%}, extracted {rate_big:.4%} "
+        f"of {w.batch}")
     assert rate >= MIN_DECRYPT_RATE[name]
+    assert rate_big >= MIN_EXTRACTED_RATE[name]
 
 
 def test_determinism(O, torch_dev):

@@ -114,7 +114,7 @@ def test_pipeline_small_ring_bit_exact(O, torch_dev):
 def test_pipeline_headline_ring(O, torch_dev):
     """n = 1024, N = 2048, l = 3 x 8 (the headline keys), SiLU on [-20, 20]
     with 4 uniform segments of 1664 intervals and margins of 192: 256 inputs
-    on the GPU; two sampled inputs bit-exact against the oracle pipeline;
+    on the GPU; 16 sampled inputs bit-exact against the oracle pipeline;
     every output decrypts to f~(x) within the selection and boundary errors
     of these parameters: median below 2e-3; inputs that Step 1 places in a
     neighbouring segment (within its resolution of a boundary) get that
@@ -130,8 +130,14 @@ def test_pipeline_headline_ring(O, torch_dev):
     say("[protocol] headline ring, 256 inputs")
     got = R.to_host(R.lookup_eval(R.to_device(x_rlwe), R.to_device(x_cmp), bsk, ksk, autk_dev,
                                   prep, consts, w.params(), lp))
-    rows = [0, 255]
-    say("[protocol] oracle pipeline on 2 sampled inputs")
+    # 16 inputs: both ends, every segment, and inputs on both sides of the
+    # three inner boundaries (-10, 0, 10), where Step 1 decides
+    near = [int(np.argmin(np.abs(xs - t))) for t in (-10.0, 0.0, 10.0)]
+    far = [int(np.argmin(np.abs(xs - c))) for c in (-15.0, -5.0, 5.0, 15.0)]
+    rows = sorted({0, 255, *near, *far, *range(16, 256, 37)})[:16]
+    while len(rows) < 16:
+        rows = sorted(set(rows) | {len(rows) * 11 + 3})
+    say(f"[protocol] oracle pipeline on {len(rows)} sampled inputs")
     ref = OL.evaluate(op, ks, autk, lp.trace_level, lp.trace_base_log, parts, lp.nseg,
                       x_rlwe[rows], x_cmp[rows])
     for i, q in enumerate(rows):
