@@ -7,6 +7,19 @@ rosetta_lookup_params, written out here independently:
 
   Step 1  y_j = [[x]]_cmp - round(tau_j 2^sc); c_j = PBS(y_j, v = mu) + mu,
           mu = floor(p / 4 nseg); S = sum_j c_j.
+          With a refinement of k bits (refine = k > 0) the comparison
+          chains four PBS instead (the paper's HomComp chains several, Sec.
+          3.2 Step 1), so that its resolution is 2^k times finer:
+            y'  = y_j + h,  h = floor(p / 2^(k+1))      (half a digit D = p/2^k)
+            z   = 2^k y'                                 (fine phase phi)
+            s1' = PBS(z, floor(p/4)),  s1 = PBS(z, floor(p / 2^(k+2)))
+            s2  = PBS(z - s1', f),  f(phi) = -phi / 2^k on [-p/4, p/4)
+            c_j = PBS(y_j - s1 + s2, mu) + mu
+          y' - s1 + s2 is about D round(y'/D), a whole number of digits,
+          and it is at least D exactly when y_j >= 0, so the last sign
+          bootstrap decides half a digit away from zero; only y_j within the
+          fine PBS's resolution (the drift of z's modulus switch, divided by
+          2^k) can land on either side.
   Step 2  t = p(X) [[x]] + q(X) (segment s over the window of rotations
           rounding to s N/nseg, the wrapped part negated); I = KS(SE(
           BlindRot(t, S))).
@@ -29,7 +42,25 @@ def enc(v: float, k: int) -> int:
     return round(float(v) * 2.0 ** k) % P
 
 
-def encode(N, nseg, nbr, margin, sx, sp, sv, sc, tau, a, b):
+def refine_polys(N, k):
+    """Test polynomials of the refined comparison: the constants floor(p/4)
+    and floor(p / 2^(k+2)) (signs at the fine and the coarse scale) and
+    f with coefficient j = -round(w_j p / (2^(k+1) N)), w_j = min(j, N - j)
+    (rounded half up): a rotation r < N/2 selects f_r, the value at phase
+    r p / 2N, and a rotation r >= 3N/2 selects -f_(r-N), the value at phase
+    (r - 2N) p / 2N, so that on phases in [-p/4, p/4) the bootstrap returns
+    -phase / 2^k."""
+    q4 = np.full(N, P // 4, np.uint64)
+    c1 = np.full(N, P // 2 ** (k + 2), np.uint64)
+    f = np.zeros(N, np.uint64)
+    for j in range(N):
+        w = min(j, N - j)
+        g = (2 * w * P + 2 ** (k + 1) * N) // (2 ** (k + 2) * N)   # round half up
+        f[j] = (P - g) % P
+    return q4, c1, f
+
+
+def encode(N, nseg, nbr, margin, sx, sp, sv, sc, tau, a, b, refine=0):
     """Plaintext polynomials and constants of the lookup (host side)."""
     box = N // nseg
     h = box // 2
@@ -60,18 +91,61 @@ def encode(N, nseg, nbr, margin, sx, sp, sv, sc, tau, a, b):
     sign_lut = np.full(N, mu, np.uint64)
     consts = np.array([enc(-tau[j], sc) for j in range(1, nseg)] + [(nseg - 1) * mu % P],
                       dtype=np.uint64)
-    return dict(p_hat=p_hat, q_hat=q_hat, a_hat=a_hat, b_hat=b_hat, window=window,
-                sign_lut=sign_lut, consts=consts)
+    out = dict(p_hat=p_hat, q_hat=q_hat, a_hat=a_hat, b_hat=b_hat, window=window,
+               sign_lut=sign_lut, consts=consts, refine=refine)
+    if refine:
+        out["q4"], out["c1"], out["f"] = refine_polys(N, refine)
+    return out
 
 
 def block(parts) -> np.ndarray:
-    """The library's plaintext block order: p, q, a_s, b_s, W, sign LUT."""
+    """The library's plaintext block order: p, q, a_s, b_s, W, sign LUT, then
+    with a refined comparison its three test polynomials."""
+    extra = [parts["q4"], parts["c1"], parts["f"]] if parts.get("refine") else []
     return np.concatenate([parts["p_hat"], parts["q_hat"], parts["a_hat"].reshape(-1),
-                           parts["b_hat"].reshape(-1), parts["window"], parts["sign_lut"]])
+                           parts["b_hat"].reshape(-1), parts["window"], parts["sign_lut"],
+                           *extra])
 
 
 def lwe_add(a, b):
     return ((a.astype(object) + b.astype(object)) % P).astype(np.uint64)
+
+
+def lwe_sub(a, b):
+    return ((a.astype(object) - b.astype(object)) % P).astype(np.uint64)
+
+
+def lwe_scale(a, m: int):
+    return ((a.astype(object) * m) % P).astype(np.uint64)
+
+
+def compare(prm, ks, parts, ys, kind=O.NTT, nthreads=0, want_steps=False):
+    """HomComp of Step 1 on the comparison inputs ys [count][n+1] (phase
+    (x - tau) 2^sc): c = 0 or 2 mu, mu = the sign test polynomial's value."""
+    n = prm.n
+    k = parts.get("refine", 0)
+    mu_poly = parts["sign_lut"]
+    mu = int(mu_poly[0])
+
+    def pbs(cts, v):
+        return O.pbs(prm, cts, ks.bsk, ks.ksk, v, kind, nthreads)
+
+    steps = {}
+    if k == 0:
+        y2 = ys
+    else:
+        h = P // 2 ** (k + 1)
+        yp = ys.copy()
+        yp[:, n] = (yp[:, n].astype(object) + h) % P
+        z = lwe_scale(yp, 2 ** k)
+        s1p = pbs(z, parts["q4"])
+        s1 = pbs(z, parts["c1"])
+        s2 = pbs(lwe_sub(z, s1p), parts["f"])
+        y2 = lwe_add(lwe_sub(ys, s1), s2)
+        steps = dict(z=z, s1p=s1p, s1=s1, s2=s2, y2=y2)
+    c = pbs(y2, mu_poly)
+    c[:, n] = (c[:, n].astype(object) + mu) % P
+    return (c, steps) if want_steps else c
 
 
 def evaluate(prm, ks, autk, trace_level, trace_base_log, parts, nseg, x_rlwe, x_cmp,
@@ -85,7 +159,10 @@ def evaluate(prm, ks, autk, trace_level, trace_base_log, parts, nseg, x_rlwe, x_
         for j in range(nseg - 1):
             ys[q, j] = x_cmp[q]
             ys[q, j, n] = (int(x_cmp[q, n]) + int(consts[j])) % P
-    cmp = O.pbs(prm, ys.reshape(-1, n + 1), ks.bsk, ks.ksk, parts["sign_lut"], kind, nthreads)
+    cmp = compare(prm, ks, parts, ys.reshape(-1, n + 1), kind, nthreads)
+    # c_j = PBS + mu, summed: S = sum_j PBS_j + (nseg - 1) mu
+    mu = int(parts["sign_lut"][0])
+    cmp[:, n] = (cmp[:, n].astype(object) - mu) % P
     cmp = cmp.reshape(batch, nseg - 1, n + 1)
     S = np.zeros((batch, n + 1), np.uint64)
     for q in range(batch):
