@@ -208,18 +208,26 @@ def lookup_select(R, W, w, p, keys, d_in, bsk, stream, steps):
                                "per_launch_modmul": tr_mm, "launch_ms": round(tr_ms, 3)}}
 
 
-def lookup_protocol(R, W, w, p, keys, bsk, ksk, stream, steps, batch):
+def lookup_protocol(R, W, stream, steps, batch):
     """The lookup pipeline of Algorithm 1 (Steps 1-3) for SiLU on [-20, 20]
-    with 4 uniform segments over the batch: inputs x ~ N(0, 1) (the FFN
-    activations) encrypted as [[x]]_RLWE and [[x]]_cmp with the library's
-    host helpers; timed on the device; a sample of outputs is decrypted and
-    compared with the cleartext segmented LUT."""
+    with 4 uniform segments, at the lookup key set (n = 1024, N = 2048,
+    14-bit gadget digits, 8 x 2-bit key switch), a 5-bit refined
+    comparison and margins of 32: inputs x ~ N(0, 1) (the FFN activations)
+    encrypted as [[x]]_RLWE and [[x]]_cmp with the library's host helpers;
+    timed on the device; a sample of outputs is decrypted and compared with
+    the cleartext segmented LUT."""
     import torch
-    sx, sv, sc, margin, nseg = 40, 18, 57, 192, 4
+    w = W.get("llama3_8b_lookup")
+    p = R.Params.from_dict(w.params())
+    keys = R.keygen(w.key_seed, p, w.sigma_lwe, w.sigma_glwe)
+    bsk = R.bsk_prepare(R.to_device(keys["bsk"]), p)
+    ksk = R.ksk_prepare(R.to_device(keys["ksk"]), p)
+    sx, sv, sc, margin, nseg, refine = 40, 18, 57, 32, 4, 5
     sp = 63 - int(math.log2(w.N)) - sx
     lp = R.LookupParams(nseg=nseg, nbr=w.N - 2 * margin, margin=margin, x_scale_log=sx,
                         coef_scale_log=sp, val_scale_log=sv, cmp_scale_log=sc,
-                        trace_level=TRACE_LEVEL, trace_base_log=TRACE_BASE_LOG)
+                        trace_level=TRACE_LEVEL, trace_base_log=TRACE_BASE_LOG,
+                        cmp_refine_log=refine)
     tau = R.seglut_boundaries(-20.0, 20.0, nseg, "uniform")
     a, b = R.seglut_build("silu", tau, lp.nbr)
     plain, consts = R.lookup_encode(p, lp, tau, a, b)
@@ -255,11 +263,12 @@ def lookup_protocol(R, W, w, p, keys, bsk, ksk, stream, steps, batch):
     P = 0xFFFFFFFF00000001
     got = np.array([(v if v <= P // 2 else v - P) / 2.0 ** (sx + sv) for v in ph], dtype=float)
     err = np.abs(got - R.seglut_eval(tau, a, b, xs[sample]))
-    return {"function": "silu", "domain": [-20.0, 20.0], "nseg": nseg, "nbr": lp.nbr,
+    return {"function": "silu", "domain": [-20.0, 20.0], "keys": w.name, "nseg": nseg,
+            "nbr": lp.nbr, "margin": margin, "cmp_refine_log": refine,
             "batch": batch, "lookups_per_s": round(batch / wall, 2),
             "ms_per_step": round(wall * 1e3, 3),
             "events_ms_per_step": round(e0.elapsed_time(e1) / steps, 3),
-            "per_lookup": {"pbs": nseg - 1, "blind_rotations_encrypted_tp": nseg + 2,
+            "per_lookup": {"pbs": 4 * (nseg - 1), "blind_rotations_encrypted_tp": nseg + 2,
                            "traces": nseg + 1, "plaintext_products": nseg + 2},
             "decrypt_check": {"sample": int(sample.size), "median_abs_err": float(np.median(err)),
                               "p99_abs_err": float(np.quantile(err, 0.99)),
@@ -309,7 +318,7 @@ def _modswitched_phase(cts, key, N):
     return np.array([(ms(c[n]) - sum(ms(v) for v in c[sel])) % (2 * N) for c in cts])
 
 
-def lookup_precision(R, w, p, keys, bsk, ksk, stream, count: int):
+def lookup_precision(R, w, p, keys, bsk, ksk, stream, count: int, variants):
     """Encrypted lookup precision, -log2 RMSE over `count` inputs drawn
     uniformly from each range of the paper's primitive tables, 4 segments,
     at the headline ring and keys.  The error is split into its sources:
@@ -319,18 +328,21 @@ def lookup_precision(R, w, p, keys, bsk, ksk, stream, count: int):
     workspace), and what remains (value noise of the traces and products).
     The selector's error is split too: the key switch's noise on I (its
     decrypted phase against the exact t) and the modulus switch's drift
-    (the modulus-switched phase against the decrypted one)."""
+    (the modulus-switched phase against the decrypted one).  `variants`
+    lists (comparison refinement bits, margin) pairs to run."""
     import torch
     P = 0xFFFFFFFF00000001
-    N, n, nseg, margin = w.N, w.n, 4, 192
-    nbr = N - 2 * margin
+    N, n, nseg = w.N, w.n, 4
     sx = 40
     sp = 63 - int(math.log2(N)) - sx
     autk = R.autk_prepare(R.to_device(R.autk_keygen(w.key_seed + 1, p, TRACE_LEVEL,
                                                     TRACE_BASE_LOG, w.sigma_glwe,
                                                     keys["glwe_key"])), p, TRACE_LEVEL)
     rows = []
-    for k, (fn, lo, hi, spacing, paper) in enumerate(PRECISION_CASES):
+    cases = [(refine, margin, k, case) for refine, margin in variants
+             for k, case in enumerate(PRECISION_CASES)]
+    for refine, margin, k, (fn, lo, hi, spacing, paper) in cases:
+        nbr = N - 2 * margin
         tau = R.seglut_boundaries(lo, hi, nseg, spacing)
         a, b = R.seglut_build(fn, tau, nbr)
         grid = np.linspace(lo, hi, 20001)
@@ -340,7 +352,8 @@ def lookup_precision(R, w, p, keys, bsk, ksk, stream, count: int):
         sv = int(math.floor(62.5 - math.log2(fmax))) - sx
         lp = R.LookupParams(nseg=nseg, nbr=nbr, margin=margin, x_scale_log=sx,
                             coef_scale_log=sp, val_scale_log=sv, cmp_scale_log=sc,
-                            trace_level=TRACE_LEVEL, trace_base_log=TRACE_BASE_LOG)
+                            trace_level=TRACE_LEVEL, trace_base_log=TRACE_BASE_LOG,
+                            cmp_refine_log=refine)
         plain, consts = R.lookup_encode(p, lp, tau, a, b)
         prep = R.lookup_prepare(R.to_device(plain), p, lp)
         xs = np.random.default_rng(w.data_seed + 10 + k).uniform(lo, hi, count)
@@ -388,6 +401,7 @@ def lookup_precision(R, w, p, keys, bsk, ksk, stream, count: int):
                                      0, float(np.sqrt(np.mean(np.square(ks_noise + drift)))),
                                      count)).astype(np.int32))
         rows.append({"function": fn, "range": [lo, hi], "spacing": spacing, "inputs": count,
+                     "cmp_refine_log": refine, "margin": margin, "nbr": nbr,
                      "scales": {"x": sx, "coef": sp, "val": sv, "cmp": sc},
                      "bits_vs_exact": round(_bits(y - f), 2),
                      "bits_vs_cleartext_lut": round(_bits(y - y_lut), 2),
@@ -403,8 +417,8 @@ def lookup_precision(R, w, p, keys, bsk, ksk, stream, count: int):
                      "interval_error_rms": round(float(np.sqrt(np.mean(
                          (i_sel - i_true)[ok].astype(float) ** 2))), 2),
                      "simulated_bits_at_measured_selector_rms": round(sim, 2)})
-        log(f"[precision] {fn} [{lo}, {hi}]: {rows[-1]['bits_vs_exact']} bits "
-            f"(paper {paper})")
+        log(f"[precision] refine {refine} margin {margin}: {fn} [{lo}, {hi}]: "
+            f"{rows[-1]['bits_vs_exact']} bits (paper {paper})")
     return rows
 
 
@@ -422,11 +436,14 @@ def main():
                     help="timed steps of the lookup select (0 = skip)")
     ap.add_argument("--protocol-steps", type=int, default=1,
                     help="timed steps of the full lookup pipeline (0 = skip)")
-    ap.add_argument("--protocol-batch", type=int, default=0,
-                    help="inputs of the lookup pipeline (default: the workload's batch)")
+    ap.add_argument("--protocol-batch", type=int, default=4096,
+                    help="inputs of the lookup pipeline")
     ap.add_argument("--precision", type=int, default=0,
                     help="instead of the benchmark: encrypted lookup precision in bits over "
-                         "this many uniform inputs per primitive of the paper's tables")
+                         "this many uniform inputs per primitive of the paper's tables "
+                         "(keys: --workload, default llama3_8b_lookup)")
+    ap.add_argument("--precision-variants", default="5:32",
+                    help="comma-separated refine:margin pairs of the precision run")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB, outside the timed "
                          "region, as the reference kernel for memory-traffic counters")
@@ -441,7 +458,7 @@ def main():
     from paper_2609_16915_amd import rosetta as R
     from paper_2609_16915_amd import workloads as W
 
-    name = args.workload or W.HEADLINE
+    name = args.workload or ("llama3_8b_lookup" if args.precision else W.HEADLINE)
     w = W.get(name)
     if args.batch:
         import dataclasses
@@ -460,7 +477,9 @@ def main():
     bsk = R.bsk_prepare(R.to_device(keys["bsk"]), p)
     ksk = R.ksk_prepare(R.to_device(keys["ksk"]), p)
     if args.precision:
-        rows = lookup_precision(R, w, p, keys, bsk, ksk, stream, args.precision)
+        variants = [tuple(int(v) for v in pair.split(":"))
+                    for pair in args.precision_variants.split(",")]
+        rows = lookup_precision(R, w, p, keys, bsk, ksk, stream, args.precision, variants)
         print(json.dumps({"lookup_precision": rows, "workload": name, "library": R.version()}),
               flush=True)
         return
@@ -572,9 +591,8 @@ def main():
                                                 args.lookup_steps)
     if args.protocol_steps > 0:
         log("[bench] lookup pipeline (Algorithm 1, Steps 1-3)")
-        result["lookup_protocol"] = lookup_protocol(R, W, w, p, keys, bsk, ksk, stream,
-                                                    args.protocol_steps,
-                                                    args.protocol_batch or w.batch)
+        result["lookup_protocol"] = lookup_protocol(R, W, stream, args.protocol_steps,
+                                                    args.protocol_batch)
     if args.cpu_seconds > 0:
         log("[bench] CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(w, keys, cts, v, args.cpu_seconds)

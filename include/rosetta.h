@@ -320,6 +320,17 @@ rosetta_status rosetta_lwe_add_consts(const uint64_t *lwe_in, const uint64_t *co
                                       uint64_t *lwe_out, size_t batch, uint32_t count,
                                       uint32_t dim, void *stream);
 
+/* Linear combination of LWE arrays, word by word (an LWE ciphertext is
+ * linear in its phase, so this is the ciphertext of the same combination of
+ * phases; the refined comparison of Step 1 scales and subtracts with it):
+ * out[i] = alpha a[i] + beta b[i] + gamma c[i] mod p for i < words.  b and c
+ * may be NULL (their term is then left out); alpha, beta, gamma below p
+ * (else ROSETTA_ERR_PARAMS); out may be exactly a, b or c but must not
+ * partially overlap them (device). */
+rosetta_status rosetta_lwe_combine(const uint64_t *a, uint64_t alpha, const uint64_t *b,
+                                   uint64_t beta, const uint64_t *c, uint64_t gamma,
+                                   uint64_t *out, size_t words, void *stream);
+
 /* Group sums (the segment index S = sum_j [x >= tau_j] of Step 1):
  * lwe_out[q] = sum_{j < count} lwe_in[q][j] + (0, .., 0, c0), lwe_in
  * [batch][count][dim+1], lwe_out [batch][dim+1] (device, not overlapping). */
@@ -396,11 +407,22 @@ rosetta_status rosetta_sample_extract(const uint64_t *glwe_in, uint64_t *big_out
  *
  * ENCODINGS (the paper names the steps but not their encodings):
  *  - Step 1, HomComp(x, tau_j) for j = 1..nseg-1: a PBS of
- *    [[x]]_cmp - round(tau_j 2^sc) with the constant test polynomial
+ *    y_j = [[x]]_cmp - round(tau_j 2^sc) with the constant test polynomial
  *    mu = floor(p / 4 nseg) (a sign bootstrap), plus mu: 2 mu if x >= tau_j,
  *    else 0 (up to noise; inputs within the bootstrap's resolution of tau_j
  *    may fall on either side).  S = sum_j of them: the segment index at scale
  *    2 mu ~ p / 2 nseg, i.e. a rotation by S N / nseg.
+ *    With cmp_refine_log = k > 0 each comparison chains four PBS (the paper's
+ *    HomComp chains several for precision), which divides the resolution
+ *    by 2^k: with h = floor(p / 2^(k+1)),
+ *      z   = 2^k (y_j + (0, h)),
+ *      s1' = PBS(z, floor(p/4)),  s1 = PBS(z, floor(p / 2^(k+2))),
+ *      s2  = PBS(z - s1', f),  f_i = -round(min(i, N-i) p / (2^(k+1) N))
+ *            (half up; the bootstrap then returns -phase / 2^k on phases
+ *            in [-p/4, p/4), where z - s1' lies),
+ *      c_j = PBS(y_j - s1 + s2, mu) + mu;
+ *    y_j - s1 + s2 is a whole number of digits p / 2^k less half a digit,
+ *    positive exactly when x >= tau_j (up to the fine resolution).
  *  - Step 2, construct: t = p(X) [[x]]_RLWE + q(X), where coefficient j of
  *    p and q holds segment s = floor((j + h) / box)'s slope
  *    nbr / (tau_{s+1} - tau_s) at scale 2^sp and offset
@@ -420,13 +442,15 @@ rosetta_status rosetta_sample_extract(const uint64_t *glwe_in, uint64_t *big_out
  *    product with W(X) = sum_{k=-h}^{box-h-1} X^k.  Select by S:
  *    Trace(BlindRot(R W, S)).
  *  - Requirements: nseg a power of two in [2, 16]; nbr + 2 margin <= N;
- *    sx + sp = 63 - log2 N; sx + sv <= 62; |x - tau_j| 2^sc < p / 4.  Coefficients are
+ *    sx + sp = 63 - log2 N; sx + sv <= 62; cmp_refine_log <= 6;
+ *    |x - tau_j| 2^sc < p / 4.  Coefficients are
  *    round(v 2^k) (half to even, as doubles) reduced exactly mod p, so
  *    offsets larger than the scale allows (q_s) wrap harmlessly: only
  *    p_s x + q_s, in [0, nbr) for the selected segment, must fit.
  *
  * The plaintext block [(4 + 2 nseg) N] words: p, q, a_0..a_{nseg-1},
- * b_0..b_{nseg-1}, W, the sign test polynomial; constants [nseg]:
+ * b_0..b_{nseg-1}, W, the sign test polynomial, then with a refined
+ * comparison floor(p/4), floor(p / 2^(k+2)) and f (3 N more); constants [nseg]:
  * -round(tau_j 2^sc) mod p for j = 1..nseg-1, then (nseg-1) mu. */
 typedef struct rosetta_lookup_params {
   uint32_t nseg;           /* N_seg, a power of two in [2, 16] */
@@ -438,9 +462,12 @@ typedef struct rosetta_lookup_params {
   uint32_t cmp_scale_log;  /* sc: scale of [[x]]_cmp */
   uint32_t trace_level;    /* automorphism key levels */
   uint32_t trace_base_log; /* automorphism key base log */
+  uint32_t cmp_refine_log; /* k: bits of refinement of the comparison (0: one sign
+                              bootstrap per boundary; 1..6: four, see Step 1) */
 } rosetta_lookup_params;
 
-/* Words of the plaintext block: (4 + 2 nseg) N. */
+/* Words of the plaintext block: (4 + 2 nseg) N, plus 3 N with a refined
+ * comparison. */
 size_t rosetta_lookup_plain_words(const rosetta_params *params,
                                   const rosetta_lookup_params *lp);
 
@@ -478,7 +505,8 @@ size_t rosetta_lookup_workspace_offset(const rosetta_params *params,
 /* Steps 1-3 for a batch: x_rlwe [batch][2N], x_cmp [batch][n+1], prepared
  * keys (bootstrapping, key switching, automorphism), the prepared plaintext
  * block and the host constants; out [batch][2N] (device, not overlapping the
- * workspace).  Per input: nseg-1 PBS (Step 1), one blind rotation of an
+ * workspace).  Per input: nseg-1 PBS (Step 1; 4 (nseg-1) with a refined
+ * comparison), one blind rotation of an
  * encrypted test polynomial + extraction + key switch (Step 2), nseg + 1
  * blind rotations of encrypted test polynomials and traces (Step 3), and
  * nseg + 2 plaintext products. */

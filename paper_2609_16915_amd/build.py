@@ -15,8 +15,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "librosetta.so")
-SOURCES = ["kernels.hip", "keyswitch.hip", "abi.cpp", "noalloc.hip", "host_helpers.cpp",
-           "seglut.cpp", "lookup.cpp"]
+SOURCES = ["kernels.hip", "keyswitch.hip", "lwe_ops.hip", "abi.cpp", "noalloc.hip",
+           "host_helpers.cpp", "seglut.cpp", "lookup.cpp"]
 ARCH = os.environ.get("ROSETTA_OFFLOAD_ARCH", "gfx950")
 
 

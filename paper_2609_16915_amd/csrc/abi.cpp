@@ -523,6 +523,21 @@ rosetta_status rosetta_lwe_add_consts(const uint64_t *lwe_in, const uint64_t *co
   return e == hipSuccess ? ok() : hip_fail(e, "lwe_add_consts launch");
 }
 
+rosetta_status rosetta_lwe_combine(const uint64_t *a, uint64_t alpha, const uint64_t *b,
+                                   uint64_t beta, const uint64_t *c, uint64_t gamma,
+                                   uint64_t *out, size_t words, void *stream) {
+  if (alpha >= GL_P || beta >= GL_P || gamma >= GL_P)
+    return fail(ROSETTA_ERR_PARAMS, "coefficients must be below p");
+  if (words == 0) return ok();
+  if (!a || !out) return fail(ROSETTA_ERR_NULL, "NULL pointer argument");
+  const size_t bytes = words * 8;
+  if (partial_overlap(a, bytes, out, bytes) || (b && partial_overlap(b, bytes, out, bytes)) ||
+      (c && partial_overlap(c, bytes, out, bytes)))
+    return fail(ROSETTA_ERR_ALIAS, "out partially overlaps an input");
+  hipError_t e = launch_lwe_combine(a, alpha, b, beta, c, gamma, out, words, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "lwe_combine launch");
+}
+
 rosetta_status rosetta_lwe_sum_groups(const uint64_t *lwe_in, uint64_t c0, uint64_t *lwe_out,
                                       size_t batch, uint32_t count, uint32_t dim,
                                       void *stream) {

@@ -71,6 +71,9 @@ struct Consts {
 };
 hipError_t launch_lwe_add_consts(const uint64_t *in, uint64_t *out, size_t batch, int count,
                                 int dim, const Consts &cs, hipStream_t st);
+hipError_t launch_lwe_combine(const uint64_t *a, uint64_t alpha, const uint64_t *b, uint64_t beta,
+                              const uint64_t *c, uint64_t gamma, uint64_t *out, size_t words,
+                              hipStream_t st);
 hipError_t launch_lwe_sum_groups(const uint64_t *in, uint64_t *out, size_t batch, int count,
                                  int dim, uint64_t c0, hipStream_t st);
 // op as in rosetta_field_op (validated by the caller)

@@ -60,6 +60,7 @@ rosetta_status check_lookup(const rosetta_params *p, const rosetta_lookup_params
   if (lp->trace_level < 1 || lp->trace_level > 4 || lp->trace_base_log < 1 ||
       lp->trace_base_log > 30 || lp->trace_level * lp->trace_base_log > 62)
     return err(ROSETTA_ERR_UNSUPPORTED, "trace level/base_log out of range");
+  if (lp->cmp_refine_log > 6) return err(ROSETTA_ERR_PARAMS, "cmp_refine_log must be <= 6");
   return ROSETTA_OK;
 }
 
@@ -84,14 +85,18 @@ bool enc(double v, int k, u64 *out) {
 
 // Words of each part of the plaintext block.
 struct Block {
-  size_t N, nseg;
+  size_t N, nseg, refine;
   size_t p_hat() const { return 0; }
   size_t q_hat() const { return N; }
   size_t a_hat(size_t s) const { return (2 + s) * N; }
   size_t b_hat(size_t s) const { return (2 + nseg + s) * N; }
   size_t window() const { return (2 + 2 * nseg) * N; }
   size_t sign_lut() const { return (3 + 2 * nseg) * N; }
-  size_t words() const { return (4 + 2 * nseg) * N; }
+  // the refined comparison's test polynomials (present when refine > 0)
+  size_t quarter() const { return (4 + 2 * nseg) * N; }
+  size_t coarse_sign() const { return (5 + 2 * nseg) * N; }
+  size_t fine_part() const { return (6 + 2 * nseg) * N; }
+  size_t words() const { return (4 + 2 * nseg + (refine ? 3 : 0)) * N; }
 };
 
 struct Scratch {
@@ -106,9 +111,12 @@ struct Scratch {
 };
 
 // Workspace layout of rosetta_lookup_eval (words), in call order.
+constexpr int LOOKUP_WS_PARTS = 17;
+
 size_t lookup_ws_words(const rosetta_params *p, const rosetta_lookup_params *lp, size_t batch,
                        uint64_t **parts, void *base, size_t *offsets = nullptr) {
   const size_t N = p->N, w = p->n + 1, ns = lp->nseg, nc = ns - 1;
+  const size_t rf = lp->cmp_refine_log ? 1 : 0;  // refined comparison parts
   Scratch sc(base);
   const size_t sizes[] = {
       batch * nc * w,        // 0 comparison inputs
@@ -122,8 +130,14 @@ size_t lookup_ws_words(const rosetta_params *p, const rosetta_lookup_params *lp,
       batch * ns * 2 * N,    // 8 selected r_s
       batch * 2 * N,         // 9 R
       batch * 2 * N,         // 10 R spread over the windows
+      rf * batch * nc * w,   // 11 z = 2^k (y + h)
+      rf * batch * nc * w,   // 12 s1' (sign of z at the fine scale)
+      rf * batch * nc * w,   // 13 s1 (sign of z at the coarse scale)
+      rf * batch * nc * w,   // 14 z - s1'
+      rf * batch * nc * w,   // 15 s2 (-phase / 2^k)
+      rf * batch * nc * w,   // 16 y - s1 + s2
   };
-  for (int i = 0; i < 11; ++i) {
+  for (int i = 0; i < LOOKUP_WS_PARTS; ++i) {
     if (offsets) offsets[i] = sc.off;
     uint64_t *q = sc.take(sizes[i]);
     if (parts) parts[i] = q;
@@ -137,7 +151,7 @@ extern "C" {
 
 size_t rosetta_lookup_plain_words(const rosetta_params *p, const rosetta_lookup_params *lp) {
   if (!p || !lp) return 0;
-  return Block{p->N, lp->nseg}.words();
+  return Block{p->N, lp->nseg, lp->cmp_refine_log}.words();
 }
 
 rosetta_status rosetta_lookup_encode(const rosetta_params *p, const rosetta_lookup_params *lp,
@@ -151,7 +165,7 @@ rosetta_status rosetta_lookup_encode(const rosetta_params *p, const rosetta_look
   const int sv = (int)lp->val_scale_log;
   for (int s = 0; s < ns; ++s)
     if (!(tau[s] < tau[s + 1])) return err(ROSETTA_ERR_PARAMS, "boundaries must increase");
-  const Block B{(size_t)N, (size_t)ns};
+  const Block B{(size_t)N, (size_t)ns, lp->cmp_refine_log};
   const int box = N / ns, h = box / 2;
   // Step 2: slope and offset repeated over each segment's rotation window
   for (int j = 0; j < N; ++j) {
@@ -188,6 +202,19 @@ rosetta_status rosetta_lookup_encode(const rosetta_params *p, const rosetta_look
     consts[j - 1] = t;
   }
   consts[ns - 1] = gl_mul(mu, (u64)(ns - 1));
+  // the refined comparison: floor(p/4), floor(p / 2^(k+2)) and
+  // f_i = -round(min(i, N-i) p / (2^(k+1) N)) (half up)
+  if (const int k = (int)lp->cmp_refine_log) {
+    const u64 q4 = GL_P / 4, c1 = GL_P >> (k + 2);
+    const unsigned __int128 den = (unsigned __int128)N << (k + 2);
+    for (int j = 0; j < N; ++j) {
+      const u64 w = (u64)(j < N - j ? j : N - j);
+      const u64 g = (u64)(((unsigned __int128)2 * w * GL_P + (den >> 1)) / den);
+      plain[B.quarter() + j] = q4;
+      plain[B.coarse_sign() + j] = c1;
+      plain[B.fine_part() + j] = g ? GL_P - g : 0;
+    }
+  }
   return ROSETTA_OK;
 }
 
@@ -197,7 +224,7 @@ rosetta_status rosetta_lookup_prepare(const uint64_t *plain_dev, uint64_t *plain
   rosetta_status st = check_lookup(p, lp);
   if (st) return st;
   if (!plain_dev || !plain_prep_dev) return err(ROSETTA_ERR_NULL, "NULL pointer argument");
-  const Block B{p->N, lp->nseg};
+  const Block B{p->N, lp->nseg, lp->cmp_refine_log};
   const size_t bytes = B.words() * 8;
   {
     const char *x = (const char *)plain_dev, *y = (const char *)plain_prep_dev;
@@ -228,7 +255,7 @@ size_t rosetta_lookup_workspace_offset(const rosetta_params *p, const rosetta_lo
   if (part != ROSETTA_LOOKUP_PART_CMP && part != ROSETTA_LOOKUP_PART_S &&
       part != ROSETTA_LOOKUP_PART_I)
     return (size_t)-1;
-  size_t offsets[11];
+  size_t offsets[LOOKUP_WS_PARTS];
   lookup_ws_words(p, lp, batch, nullptr, nullptr, offsets);
   return offsets[part];
 }
@@ -253,16 +280,44 @@ rosetta_status rosetta_lookup_eval(const uint64_t *x_rlwe, const uint64_t *x_cmp
     if (o < w + need && w < o + ob) return err(ROSETTA_ERR_ALIAS, "out overlaps the workspace");
   }
   const uint32_t N = p->N, n = p->n, ns = lp->nseg, nc = ns - 1;
-  const Block B{N, ns};
-  uint64_t *ws[11];
+  const Block B{N, ns, lp->cmp_refine_log};
+  uint64_t *ws[LOOKUP_WS_PARTS];
   lookup_ws_words(p, lp, batch, ws, workspace);
   void *s = stream;
   const uint32_t tl = lp->trace_level, tb = lp->trace_base_log;
 
   // Step 1: segment index S = sum_j HomComp(x, tau_j)
+  const size_t cmp_cts = batch * nc, cmp_words = cmp_cts * (n + 1);
+  const size_t pbs_ws = cmp_cts * (N + 1) * 8;
   if ((st = rosetta_lwe_add_consts(x_cmp, consts, ws[0], batch, nc, n, s))) return st;
-  if ((st = rosetta_pbs_batch_ws(ws[0], bsk_dev, ksk_dev, plain_prep_dev + B.sign_lut(), ws[2],
-                                 batch * nc, p, ws[1], batch * nc * (N + 1) * 8, s)))
+  const uint64_t *cmp_in = ws[0];
+  if (const int k = (int)lp->cmp_refine_log) {
+    // z = 2^k (y + h); s1', s1 its signs at the fine and the coarse scale;
+    // s2 = -(z - s1') / 2^k; the sign bootstrap then takes y - s1 + s2
+    uint64_t shifted[MAX_MONOMIALS / 4];
+    const u64 h = GL_P >> (k + 1);
+    for (uint32_t j = 0; j < nc; ++j) shifted[j] = gl_add(consts[j], h);
+    if ((st = rosetta_lwe_add_consts(x_cmp, shifted, ws[11], batch, nc, n, s))) return st;
+    if ((st = rosetta_lwe_combine(ws[11], (u64)1 << k, nullptr, 0, nullptr, 0, ws[11], cmp_words,
+                                  s)))
+      return st;
+    if ((st = rosetta_pbs_batch_ws(ws[11], bsk_dev, ksk_dev, plain_prep_dev + B.quarter(), ws[12],
+                                   cmp_cts, p, ws[1], pbs_ws, s)))
+      return st;
+    if ((st = rosetta_pbs_batch_ws(ws[11], bsk_dev, ksk_dev, plain_prep_dev + B.coarse_sign(),
+                                   ws[13], cmp_cts, p, ws[1], pbs_ws, s)))
+      return st;
+    if ((st = rosetta_lwe_combine(ws[11], 1, ws[12], GL_P - 1, nullptr, 0, ws[14], cmp_words, s)))
+      return st;
+    if ((st = rosetta_pbs_batch_ws(ws[14], bsk_dev, ksk_dev, plain_prep_dev + B.fine_part(),
+                                   ws[15], cmp_cts, p, ws[1], pbs_ws, s)))
+      return st;
+    if ((st = rosetta_lwe_combine(ws[0], 1, ws[13], GL_P - 1, ws[15], 1, ws[16], cmp_words, s)))
+      return st;
+    cmp_in = ws[16];
+  }
+  if ((st = rosetta_pbs_batch_ws(cmp_in, bsk_dev, ksk_dev, plain_prep_dev + B.sign_lut(), ws[2],
+                                 cmp_cts, p, ws[1], pbs_ws, s)))
     return st;
   if ((st = rosetta_lwe_sum_groups(ws[2], consts[nc], ws[3], batch, nc, n, s))) return st;
   // Step 2: t = p [[x]] + q; I = PBS(t, S)

@@ -93,6 +93,8 @@ SIGNATURES = {
                                      C.c_void_p]),
     "rosetta_lwe_sum_groups": (_ST, [_u64p, C.c_uint64, _u64p, C.c_size_t, C.c_uint32,
                                      C.c_uint32, C.c_void_p]),
+    "rosetta_lwe_combine": (_ST, [_u64p, C.c_uint64, _u64p, C.c_uint64, _u64p, C.c_uint64, _u64p,
+                                  C.c_size_t, C.c_void_p]),
     "rosetta_autk_words": (C.c_size_t, [_pp, C.c_uint32]),
     "rosetta_autk_prepare": (_ST, [_u64p, _u64p, _pp, C.c_uint32, C.c_void_p]),
     "rosetta_trace": (_ST, [_u64p, _u64p, _u64p, C.c_size_t, _pp, C.c_uint32, C.c_uint32,
@@ -128,7 +130,7 @@ class LookupParams(C.Structure):
 
     _fields_ = [(name, C.c_uint32) for name in
                 ("nseg", "nbr", "margin", "x_scale_log", "coef_scale_log", "val_scale_log",
-                 "cmp_scale_log", "trace_level", "trace_base_log")]
+                 "cmp_scale_log", "trace_level", "trace_base_log", "cmp_refine_log")]
 
 
 _lpp = C.POINTER(LookupParams)
@@ -480,6 +482,21 @@ def lwe_sum_groups(lwe_in, count: int, dim: int, c0: int = 0, out=None, stream=N
     _expect(out, "lwe_out", batch * (dim + 1))
     _check(lib().rosetta_lwe_sum_groups(_dev(lwe_in, "lwe_in"), c0, _dev(out, "lwe_out"), batch,
                                         count, dim, _stream(stream)))
+    return out
+
+
+def lwe_combine(a, alpha: int, b=None, beta: int = 0, c=None, gamma: int = 0, out=None,
+                stream=None):
+    """out = alpha a + beta b + gamma c mod p, word by word (b, c optional)."""
+    words = _words(a)
+    for t, name in ((b, "b"), (c, "c")):
+        if t is not None:
+            _expect(t, name, words)
+    out = empty(a.shape, a.device) if out is None else out
+    _expect(out, "out", words)
+    _check(lib().rosetta_lwe_combine(_dev(a, "a"), alpha, None if b is None else _dev(b, "b"),
+                                     beta, None if c is None else _dev(c, "c"), gamma,
+                                     _dev(out, "out"), words, _stream(stream)))
     return out
 
 

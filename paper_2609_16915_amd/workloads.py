@@ -23,6 +23,8 @@ the Goldilocks prime):
                         [-16,0] of scores minus the row max, batch 65536 =
                         32 heads x 2048 context; plus a 32-element reciprocal
                         batch over the row sums.
+  llama3_8b_lookup      keys of the lookup protocol (Algorithm 1): n=1024,
+                        N=2048, l=3 beta=14, KS 8x2, batch 14336.
 
 LUT semantics (Sec. 3.1, single uniform LUT): the input range is cut into M
 equal intervals; index m = clamp(floor((x - lo) / dx), 0, M-1) and the entry
@@ -179,6 +181,16 @@ WORKLOADS: dict[str, Workload] = {
                                         msg_bits=7, batch=32, sigma_lwe=_S17, sigma_glwe=_S51,
                                         key_seed=5, enc_seed=106, data_seed=206,
                                         function="recip", lo=0.0, dx=0.5),
+    # the lookup protocol of Algorithm 1 at the LLaMA-3-8B FFN width: the
+    # headline ring and LWE dimension with 14-bit gadget digits (the blind
+    # rotation's noise on a selected value drops from about 2^48 to 2^37
+    # absolute at the same cost) and an 8 x 2-bit key switch (smaller
+    # noise on the selectors S and I)
+    "llama3_8b_lookup": Workload("llama3_8b_lookup", n=1024, N=2048, pbs_level=3,
+                                 pbs_base_log=14, ks_level=8, ks_base_log=2, msg_bits=6,
+                                 batch=14336, sigma_lwe=_S17, sigma_glwe=_S51, key_seed=7,
+                                 enc_seed=107, data_seed=207, function="silu", lo=-8.0,
+                                 dx=0.25, act_sigma=1.0),
 }
 
 # The headline workload (LLaMA-3-8B FFN SiLU, N = 2048, batch 14336).

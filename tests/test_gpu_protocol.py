@@ -24,11 +24,11 @@ def torch_dev():
     return require_gpu()
 
 
-def lparams(N, sx, sv, sc, margin, nseg=4):
+def lparams(N, sx, sv, sc, margin, nseg=4, refine=0):
     sp = 63 - int(math.log2(N)) - sx
     return R.LookupParams(nseg=nseg, nbr=N - 2 * margin, margin=margin, x_scale_log=sx,
                           coef_scale_log=sp, val_scale_log=sv, cmp_scale_log=sc,
-                          trace_level=4, trace_base_log=12)
+                          trace_level=4, trace_base_log=12, cmp_refine_log=refine)
 
 
 def centred(v):
@@ -41,7 +41,7 @@ def setup(O, op, ks, lp, fn, lo, hi, spacing, sigma, seed):
     tau = G.boundaries(lo, hi, lp.nseg, spacing)
     A, B = G.build(G.FUNCTIONS[fn], tau, lp.nbr)
     parts = OL.encode(N, lp.nseg, lp.nbr, lp.margin, lp.x_scale_log, lp.coef_scale_log,
-                      lp.val_scale_log, lp.cmp_scale_log, tau, A, B)
+                      lp.val_scale_log, lp.cmp_scale_log, tau, A, B, refine=lp.cmp_refine_log)
     autk = O.autk_keygen(seed, N, lp.trace_level, lp.trace_base_log, sigma, ks.glwe_key)
     plain, consts = R.lookup_encode(op.as_dict() | {"k": 1}, lp, tau, A, B)
     assert np.array_equal(plain, OL.block(parts)) and np.array_equal(consts, parts["consts"])
@@ -83,6 +83,61 @@ def test_lwe_maps_and_grouped_selection(O, torch_dev):
                                         group=4))
     ref = O.blind_rotate_glwe_batch(op, np.repeat(lwe, 4, axis=0), ks.bsk, tp, O.NTT)
     assert np.array_equal(got, ref)
+
+
+def test_lwe_combine_exact(torch_dev):
+    """alpha a + beta b + gamma c mod p word by word, against Python
+    integers: edge words, random coefficients, terms left out, in place."""
+    rng = np.random.default_rng(4)
+    words = 3001
+    a, b, c = (rng.integers(0, P, words, dtype=np.uint64) for _ in range(3))
+    a[:4] = [0, 1, P - 1, P // 2]
+    b[:4] = [P - 1, P - 1, P - 1, 1]
+    for alpha, beta, gamma in ((1, P - 1, 1), (1 << 5, 0, 0), (P - 1, 2 ** 63, 12345),
+                               (int(rng.integers(0, P, dtype=np.uint64)), 7, P - 2)):
+        got = R.to_host(R.lwe_combine(R.to_device(a), alpha, R.to_device(b), beta,
+                                      R.to_device(c), gamma))
+        want = [(alpha * int(x) + beta * int(y) + gamma * int(z)) % P for x, y, z in zip(a, b, c)]
+        assert [int(v) for v in got] == want
+    d = R.to_device(a)
+    R.lwe_combine(d, 1 << 6, out=d)                     # in place, b and c left out
+    assert [int(v) for v in R.to_host(d)] == [(int(x) << 6) % P for x in a]
+
+
+def test_pipeline_small_ring_refined_bit_exact(O, torch_dev):
+    """The refined comparison (2 bits, four PBS per boundary) inside the
+    whole pipeline at the small ring, inputs on both sides of every
+    boundary at 1.2 coarse steps and in the segments: GPU output = oracle
+    output bit for bit (the segment index S too), within 2e-3 of f~(x)
+    (0.05 for the inputs next to a boundary, which a miss of the comparison
+    sends to the neighbouring segment's edge line)."""
+    op = O.Params.make(**{k: v for k, v in SMALL.items() if k != "k"})
+    sigma = 2.0 ** -40
+    ks = O.KeySet(op, 5, sigma, sigma)
+    lp = lparams(256, sx=44, sv=16, sc=58, margin=64, refine=2)
+    tau, A, B, parts, autk, prep, autk_dev, consts = setup(O, op, ks, lp, "inv", 1.0, 16.0, "log",
+                                                           sigma, 6)
+    bsk = R.bsk_prepare(R.to_device(ks.bsk), SMALL)
+    ksk = R.ksk_prepare(R.to_device(ks.ksk), SMALL)
+    xs = np.concatenate([np.random.default_rng(2).uniform(1.0, 16.0, 7),
+                         [t + d for t in tau[1:-1] for d in (-0.15, 0.15)]])
+    x_rlwe, x_cmp = inputs(O, ks, lp, xs, sigma, 50, 256)
+    say(f"[protocol] small ring, refined comparison, {len(xs)} inputs")
+    ws = R.empty(R.lookup_workspace_bytes(SMALL, lp, len(xs)) // 8)
+    got = R.to_host(R.lookup_eval(R.to_device(x_rlwe), R.to_device(x_cmp), bsk, ksk, autk_dev,
+                                  prep, consts, SMALL, lp, workspace=ws))
+    ref, st = OL.evaluate(op, ks, autk, lp.trace_level, lp.trace_base_log, parts, lp.nseg,
+                          x_rlwe, x_cmp, want_steps=True)
+    assert np.array_equal(got, ref)
+    wsh = R.to_host(ws)
+    oS = R.lookup_workspace_offset(SMALL, lp, len(xs), R.LOOKUP_PART_S)
+    assert np.array_equal(wsh[oS:oS + len(xs) * (op.n + 1)].reshape(len(xs), -1), st["S"])
+    scale = 2.0 ** (lp.x_scale_log + lp.val_scale_log)
+    want = G.evaluate(xs, tau, A, B)
+    for q in range(len(xs)):
+        v = centred(O.glwe_phase(ks.glwe_key, got[q])[0]) / scale
+        near = np.min(np.abs(xs[q] - tau[1:-1])) < 0.2
+        assert abs(v - want[q]) < (0.05 if near else 2e-3), (xs[q], v, want[q])
 
 
 def test_pipeline_small_ring_bit_exact(O, torch_dev):
@@ -148,3 +203,36 @@ def test_pipeline_headline_ring(O, torch_dev):
     err = np.abs(np.array(ph) - want)
     say(f"[protocol] decrypt error median {np.median(err):.2e} max {err.max():.2e}")
     assert np.median(err) < 2e-3 and err.max() < 0.2
+
+
+def test_pipeline_lookup_keys_refined(O, torch_dev):
+    """The lookup keys (n = 1024, N = 2048, l = 3 x 14, key switch 8 x 2),
+    SiLU on [-20, 20], 4 segments of 1984 intervals with margins of 32 and a
+    5-bit refined comparison: 128 inputs on the GPU (24 of them within 0.05
+    of a boundary, 1.6 coarse steps), 16 sampled inputs bit-exact against the
+    oracle pipeline; every output within 0.02 of f~(x) and the median within
+    1e-3."""
+    w, op, ks, bsk, ksk = keyset(O, "llama3_8b_lookup")
+    sigma = w.sigma_glwe
+    lp = lparams(2048, sx=40, sv=18, sc=57, margin=32, refine=5)
+    tau, A, B, parts, autk, prep, autk_dev, consts = setup(O, op, ks, lp, "silu", -20.0, 20.0,
+                                                           "uniform", sigma, 8)
+    rng = np.random.default_rng(8)
+    xs = np.concatenate([rng.uniform(-20.0, 20.0, 104),
+                         [t + d for t in tau[1:-1] for d in np.linspace(-0.05, 0.05, 8)]])
+    x_rlwe, x_cmp = inputs(O, ks, lp, xs, sigma, 70, 2048)
+    say("[protocol] lookup keys, refined comparison, 128 inputs")
+    got = R.to_host(R.lookup_eval(R.to_device(x_rlwe), R.to_device(x_cmp), bsk, ksk, autk_dev,
+                                  prep, consts, w.params(), lp))
+    rows = sorted({0, 127, *range(104, 128, 3), *range(5, 104, 13)})[:16]
+    say(f"[protocol] oracle pipeline on {len(rows)} sampled inputs")
+    ref = OL.evaluate(op, ks, autk, lp.trace_level, lp.trace_base_log, parts, lp.nseg,
+                      x_rlwe[rows], x_cmp[rows])
+    for i, q in enumerate(rows):
+        assert np.array_equal(got[q], ref[i]), q
+    scale = 2.0 ** (lp.x_scale_log + lp.val_scale_log)
+    want = G.evaluate(xs, tau, A, B)
+    err = np.abs(np.array([centred(O.glwe_phase(ks.glwe_key, got[q])[0]) / scale
+                           for q in range(len(xs))]) - want)
+    say(f"[protocol] decrypt error median {np.median(err):.2e} max {err.max():.2e}")
+    assert np.median(err) < 1e-3 and err.max() < 0.02

@@ -19,27 +19,30 @@ SMALL = dict(n=64, k=1, N=256, pbs_level=3, pbs_base_log=8, ks_level=4, ks_base_
 SIG = 2.0 ** -40
 
 
-def lookup_params(N, nseg=4, margin=16, sc=58, tl=4, tb=12, sx=44, sv=16):
+def lookup_params(N, nseg=4, margin=16, sc=58, tl=4, tb=12, sx=44, sv=16, refine=0):
     """sx + sp = 63 - log2 N (one unit of t per rotation step); values at
     2^(sx+sv)."""
     sp = 63 - int(math.log2(N)) - sx
     return R.LookupParams(nseg=nseg, nbr=N - 2 * margin, margin=margin, x_scale_log=sx,
                           coef_scale_log=sp, val_scale_log=sv, cmp_scale_log=sc,
-                          trace_level=tl, trace_base_log=tb)
+                          trace_level=tl, trace_base_log=tb, cmp_refine_log=refine)
 
 
-@pytest.mark.parametrize("N,fn,lo,hi,spacing", [
-    (256, "inv", 1.0, 16.0, "log"), (2048, "silu", -20.0, 20.0, "uniform"),
-    (2048, "inv", 0.01, 10.0, "log"), (512, "gelu", -8.0, 8.0, "uniform")])
-def test_encoder_matches_oracle(N, fn, lo, hi, spacing):
-    lp = lookup_params(N, sc=56 if N == 2048 else 58, sx=40 if N == 2048 else 44,
-                       sv=18 if N == 2048 else 16)
+@pytest.mark.parametrize("N,fn,lo,hi,spacing,refine", [
+    (256, "inv", 1.0, 16.0, "log", 0), (2048, "silu", -20.0, 20.0, "uniform", 0),
+    (2048, "inv", 0.01, 10.0, "log", 0), (512, "gelu", -8.0, 8.0, "uniform", 0),
+    (256, "inv", 1.0, 16.0, "log", 2), (2048, "silu", -20.0, 20.0, "uniform", 5),
+    (4096, "inv_sqrt", 0.01, 100.0, "log", 6), (1024, "gelu", -8.0, 8.0, "uniform", 1)])
+def test_encoder_matches_oracle(N, fn, lo, hi, spacing, refine):
+    lp = lookup_params(N, sc=56 if N >= 2048 else 58, sx=40 if N >= 2048 else 44,
+                       sv=18 if N >= 2048 else 16, refine=refine)
     prm = dict(SMALL, N=N)
     tau = R.seglut_boundaries(lo, hi, lp.nseg, spacing)
     a, b = R.seglut_build(fn, tau, lp.nbr)
     plain, consts = R.lookup_encode(prm, lp, tau, a, b)
     parts = OL.encode(N, lp.nseg, lp.nbr, lp.margin, lp.x_scale_log, lp.coef_scale_log,
-                      lp.val_scale_log, lp.cmp_scale_log, tau, a, b)
+                      lp.val_scale_log, lp.cmp_scale_log, tau, a, b, refine=refine)
+    assert plain.size == (4 + 2 * lp.nseg + (3 if refine else 0)) * N
     assert np.array_equal(plain, OL.block(parts))
     assert np.array_equal(consts, parts["consts"])
 
@@ -50,7 +53,7 @@ def test_encoder_validation():
     tau = R.seglut_boundaries(1.0, 16.0, 4, "log")
     a, b = R.seglut_build("inv", tau, lp.nbr)
     for field, bad in (("nseg", 3), ("nbr", 250), ("x_scale_log", 41), ("trace_level", 5),
-                       ("val_scale_log", 19)):
+                       ("val_scale_log", 19), ("cmp_refine_log", 7)):
         lp2 = lookup_params(256)
         setattr(lp2, field, bad)
         with pytest.raises(R.RosettaError):
