@@ -121,8 +121,10 @@ k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta, u64
 // Waves per SIMD the blind-rotation kernel is compiled for.  Up to N = 2048
 // three workgroups fit a CU's LDS, so the kernel targets 3 waves per SIMD
 // (<= 168 registers; the few spills touch only the accumulator, read twice
-// per step).  At N = 4096 one 512-thread workgroup fills the LDS and runs
-// 2 waves per SIMD, so it keeps 256 registers.
+// per step).  At N = 4096 a workgroup is 256 threads of 16 elements (66 KiB
+// of LDS): two workgroups share a CU, one wave of each per SIMD, with 256
+// registers each, so that one workgroup's barrier waits overlap the other's
+// work.
 #ifndef BR_WAVES_PER_EU
 #define BR_WAVES_PER_EU 3
 #endif
@@ -186,6 +188,12 @@ size_t br_lds_bytes(int n) {
 // tp_glwe = g > 1 pairs each LWE selector with g consecutive test-polynomial
 // ciphertexts (workgroup b uses selector b / g), so that one encrypted
 // index selects in several ciphertexts at once.
+#ifndef BR_KEY_CHUNK
+#define BR_KEY_CHUNK 2
+#endif
+#ifndef BR_CHUNK_FENCE
+#define BR_CHUNK_FENCE() __builtin_amdgcn_sched_barrier(0)
+#endif
 template <class S, int L, typename RT, bool PF>
 __global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(br_waves_per_eu<S>())))
 k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
@@ -260,8 +268,19 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
 #pragma unroll 1
       for (int t = L - 1; t >= 0; --t) {
         const int row = (u * L + t) * 2 * N * 8;  // byte offset of GGSW_i[u][t][0]
-        u64 g0[E], g1[E];
-        if constexpr (PF) {
+        u64 g0[E <= 8 ? E : 1], g1[E <= 8 ? E : 1];
+        // 16 elements: the first chunk of the two key rows is requested
+        // before the digit transform, so that the transform hides its
+        // latency (the later chunks overlap the chunk before them)
+        u64 h0[BR_KEY_CHUNK], h1[BR_KEY_CHUNK];
+        if constexpr (E > 8) {
+#pragma unroll
+          for (int k = 0; k < BR_KEY_CHUNK; ++k) {
+            h0[k] = G.load(tid * 8, row + k * T * 8);
+            h1[k] = G.load(tid * 8, row + (N + k * T) * 8);
+          }
+        }
+        if constexpr (PF && E <= 8) {
 #pragma unroll
           for (int k = 0; k < E; ++k) {
             g0[k] = G.load(tid * 8, row + k * T * 8);
@@ -292,18 +311,50 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
           ntt_forward<S>(x, lds, tid, tw);
         }
         // a5: multiply-accumulate with the two rows of GGSW_i[u][t]
-        if constexpr (!PF) {
+        // (running sums weak until the inverse transform takes them)
+        if constexpr (E <= 8) {
+          if constexpr (!PF) {
+#pragma unroll
+            for (int k = 0; k < E; ++k) {
+              g0[k] = G.load(tid * 8, row + k * T * 8);
+              g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
+            }
+          }
 #pragma unroll
           for (int k = 0; k < E; ++k) {
-            g0[k] = G.load(tid * 8, row + k * T * 8);
-            g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
+            Y0[k] = gl_mul_add_weak(x[k], g0[k], Y0[k]);
+            Y1[k] = gl_mul_add_weak(x[k], g1[k], Y1[k]);
           }
-        }
-        // (running sums weak until the inverse transform takes them)
+        } else {
+          // 16 elements: the key rows a chunk at a time (BR_KEY_CHUNK
+          // elements, 4 registers each), the next chunk requested before
+          // the products of the current one, so that 2 chunks rather than
+          // 64 registers hold them (chunks of 2: 1409 ms per 8192
+          // ciphertexts at N = 4096, 4: 1433, 8: 1500, unpipelined 4: 1445)
 #pragma unroll
-        for (int k = 0; k < E; ++k) {
-          Y0[k] = gl_mul_add_weak(x[k], g0[k], Y0[k]);
-          Y1[k] = gl_mul_add_weak(x[k], g1[k], Y1[k]);
+          for (int k0 = 0; k0 < E; k0 += BR_KEY_CHUNK) {
+            u64 n0[BR_KEY_CHUNK], n1[BR_KEY_CHUNK];
+            if (k0 + BR_KEY_CHUNK < E) {
+#pragma unroll
+              for (int k = 0; k < BR_KEY_CHUNK; ++k) {
+                n0[k] = G.load(tid * 8, row + (k0 + BR_KEY_CHUNK + k) * T * 8);
+                n1[k] = G.load(tid * 8, row + (N + (k0 + BR_KEY_CHUNK + k) * T) * 8);
+              }
+            }
+#pragma unroll
+            for (int k = 0; k < BR_KEY_CHUNK; ++k) {
+              Y0[k0 + k] = gl_mul_add_weak(x[k0 + k], h0[k], Y0[k0 + k]);
+              Y1[k0 + k] = gl_mul_add_weak(x[k0 + k], h1[k], Y1[k0 + k]);
+            }
+            if (k0 + BR_KEY_CHUNK < E) {
+#pragma unroll
+              for (int k = 0; k < BR_KEY_CHUNK; ++k) {
+                h0[k] = n0[k];
+                h1[k] = n1[k];
+              }
+            }
+            BR_CHUNK_FENCE();
+          }
         }
       }
     }
@@ -377,9 +428,12 @@ __device__ __forceinline__ u64 automorphism_coef(const u64 *a, int j, u32 dinv) 
 #ifndef TRACE_WAVES_PER_EU
 #define TRACE_WAVES_PER_EU 3
 #endif
+// At N = 4096 (16 elements per thread, 64-bit digits) the trace kernel
+// takes the whole register file of a SIMD (one wave): its live state is
+// about 300 registers, and the allocator fails on it at two waves.
 template <class S>
 constexpr int trace_waves_per_eu() {
-  return S::LOGN >= 12 ? 2 : TRACE_WAVES_PER_EU;
+  return S::LOGN >= 12 ? 1 : TRACE_WAVES_PER_EU;
 }
 
 template <class S, int L>
@@ -457,10 +511,24 @@ k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restric
         ntt_forward<S>(x, lds, tid, tw);
       }
       gconst_u64 *g = G + (size_t)(t * 2) * N;
+      if constexpr (E <= 8) {
 #pragma unroll
-      for (int k = 0; k < E; ++k) {
-        Y0[k] = gl_mul_add_weak(x[k], g[k * T], Y0[k]);
-        Y1[k] = gl_mul_add_weak(x[k], g[N + k * T], Y1[k]);
+        for (int k = 0; k < E; ++k) {
+          Y0[k] = gl_mul_add_weak(x[k], g[k * T], Y0[k]);
+          Y1[k] = gl_mul_add_weak(x[k], g[N + k * T], Y1[k]);
+        }
+      } else {
+        // 16 elements: the key rows a quarter at a time, as in the blind
+        // rotation
+#pragma unroll
+        for (int k0 = 0; k0 < E; k0 += BR_KEY_CHUNK) {
+#pragma unroll
+          for (int k = k0; k < k0 + BR_KEY_CHUNK; ++k) {
+            Y0[k] = gl_mul_add_weak(x[k], g[k * T], Y0[k]);
+            Y1[k] = gl_mul_add_weak(x[k], g[N + k * T], Y1[k]);
+          }
+          BR_CHUNK_FENCE();
+        }
       }
     }
 #pragma unroll
@@ -653,13 +721,13 @@ hipError_t launch_bsk_prepare(const uint64_t *bsk_std, uint64_t *bsk_dev,
   return hipGetLastError();
 }
 
-// Key rows loaded before each digit transform (PF): at N = 4096 the kernel
-// runs two waves per SIMD with registers to spare, and the early loads hide
-// their latency behind the transform (about 2 % there); at N <= 2048 the
-// extra 32 registers per thread cost more in spills than they save.
+// Key rows loaded before each digit transform (PF): with 8 elements per
+// thread at N <= 2048 the extra 32 registers per thread cost more in spills
+// than the early loads save, and with 16 per thread (N = 4096) the 64 they
+// would take are not there.
 template <class S>
 constexpr bool br_prefetch() {
-  return S::LOGN >= 12;
+  return false;
 }
 
 template <class S, int L>

@@ -245,9 +245,9 @@ MIN_EXTRACTED_RATE = {"gpt2_gelu": 0.9999, "tinyllama_silu": 0.999, "llama3_8b_s
 
 def resident_workgroups(N: int) -> int:
     """Blind-rotation workgroups the chip holds at once (256 CUs x 3
-    workgroups up to N = 2048, one at N = 4096): a batch runs in rounds of
+    workgroups up to N = 2048, 2 at N = 4096): a batch runs in rounds of
     this many ciphertexts."""
-    return 256 * (3 if N <= 2048 else 1)
+    return 256 * (3 if N <= 2048 else 2)
 
 
 def dense_picks(batch: int, N: int, seed: int):
