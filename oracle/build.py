@@ -11,14 +11,20 @@ SRC = os.path.join(HERE, "oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
 
-def build(verbose: bool = False) -> str:
-    """Compile oracle.c; always recompiles.  Returns the library path."""
-    tmp = LIB + ".tmp"
+def compile_to(src: str, out: str, verbose: bool = False) -> str:
+    """Compile one oracle source file into the shared library `out`."""
     cmd = ["gcc", "-O2", "-std=gnu11", "-fopenmp", "-fPIC", "-shared",
-           "-Wall", "-Wextra", "-o", tmp, SRC, "-lm"]
+           "-Wall", "-Wextra", "-o", out, src, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Compile oracle.c; always recompiles.  Returns the library path."""
+    tmp = LIB + ".tmp"
+    compile_to(SRC, tmp, verbose)
     os.replace(tmp, LIB)
     return LIB
 

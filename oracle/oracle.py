@@ -18,7 +18,9 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liboracle.so")
+# ROSETTA_ORACLE_LIB names another build of oracle.c (the mutation tests load
+# copies with one planted mistake each through it)
+LIB_PATH = os.environ.get("ROSETTA_ORACLE_LIB") or os.path.join(HERE, "liboracle.so")
 
 P = 0xFFFFFFFF00000001
 SCHOOLBOOK = 0

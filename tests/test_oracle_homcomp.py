@@ -39,10 +39,12 @@ def test_refine_poly_is_minus_phase_over_2k(O, N, k):
         assert abs(centred(const) - want) <= 1, (r, centred(const), float(want))
 
 
-def _grid_compare(O, refine, n, N, sc_steps):
+def _grid_compare(O, refine, n, N, sc_steps, want_steps=False):
     """Comparison of x against tau = 0 for inputs x whose comparison phase is
     y = s * p / 2N, s on a grid of `sc_steps` (coarse rotation steps):
-    returns the decrypted bits (c / 2 mu)."""
+    returns the decrypted bits (c / 2 mu), with want_steps also the inputs'
+    phases, the refined comparison's intermediate ciphertexts and the LWE
+    key."""
     prm = O.Params.make(n=n, N=N, pbs_level=3, pbs_base_log=8, ks_level=4, ks_base_log=5,
                         msg_bits=2)
     ks = O.KeySet(prm, 31 + n, 0.0, 0.0)
@@ -52,7 +54,7 @@ def _grid_compare(O, refine, n, N, sc_steps):
         parts["q4"], parts["c1"], parts["f"] = OL.refine_polys(N, refine)
     ys = np.array([round(s * P / (2 * N)) % P for s in sc_steps], dtype=np.uint64)
     cts = O.lwe_encrypt_plain(77, 0.0, ks.lwe_key, ys)
-    c = OL.compare(prm, ks, parts, cts)
+    c, steps = OL.compare(prm, ks, parts, cts, want_steps=True)
     mu = P // (4 * nseg)
     ph = O.lwe_phase(ks.lwe_key, c)
     bits = []
@@ -60,6 +62,8 @@ def _grid_compare(O, refine, n, N, sc_steps):
         v = centred(v)
         assert abs(v) < mu // 2 or abs(v - 2 * mu) < mu // 2, "not 0 or 2 mu"
         bits.append(1 if abs(v - 2 * mu) < mu // 2 else 0)
+    if want_steps:
+        return np.array(bits), ys, steps, ks.lwe_key
     return np.array(bits)
 
 
@@ -86,6 +90,37 @@ def test_refined_comparison_exact_outside_its_band(O):
     # drift, well inside the worst case), the refined one none at 0.1 steps
     assert np.sum(single != want) > 0
     assert np.sum(ref != want) < np.sum(single != want)
+
+
+def test_refined_comparison_lands_half_a_digit_from_zero(O):
+    """The value the last sign bootstrap of the refined comparison decides
+    on, y2 = y - s1 + s2, decrypts to D round(y'/D) - h (y' = y + h, digit
+    D = p/2^k, h = D/2), i.e. half a digit on the side of zero that y is on,
+    within the fine bootstrap's resolution: the drift of z's modulus switch,
+    (n+1)/2 coarse steps, divided by 2^k (8.5/8 of 2^55 here), plus the key
+    switch rounding of two outputs.  Inputs within 2 coarse steps of a digit
+    boundary of y' (where the drift may round either way) are left out.
+    Noise-free keys, n = 16, N = 256, k = 3."""
+    n, N, k = 16, 256, 3
+    rng = np.random.default_rng(8)
+    steps = np.concatenate([np.round(np.arange(-30.0, 30.0, 0.7), 3),
+                            rng.uniform(-(N - N / 2 ** k - 2), N - N / 2 ** k - 2, 60)])
+    _, ys, st, key = _grid_compare(O, k, n, N, steps, want_steps=True)
+    D = Fraction(P, 2 ** k)
+    h = P // 2 ** (k + 1)
+    coarse = Fraction(P, 2 * N)
+    tol = Fraction(n + 1, 2) * coarse / 2 ** k + 2 ** 53
+    y2 = O.lwe_phase(key, st["y2"])
+    checked = 0
+    for y, v in zip(ys, y2):
+        yp = centred(y) + h
+        m = round(Fraction(yp) / D)
+        if abs(Fraction(yp) - (m - Fraction(1, 2)) * D) < 2 * coarse or \
+                abs(Fraction(yp) - (m + Fraction(1, 2)) * D) < 2 * coarse:
+            continue
+        assert abs(centred(v) - (m * D - h)) <= tol, (centred(y) / coarse, centred(v) / D)
+        checked += 1
+    assert checked > 100
 
 
 def test_refined_pipeline_decrypts_to_the_segmented_lut(O):

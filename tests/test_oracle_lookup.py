@@ -332,6 +332,50 @@ def test_paper_lookup_example_end_to_end(O):
     assert abs(out[0] - pr["result"]) <= 5e-4 and all(abs(v) < 1e-6 for v in out[1:])
 
 
+@pytest.mark.parametrize("spacing,lo,hi", [("uniform", -20.0, 20.0), ("log", 0.01, 10.0)])
+def test_encoding_selects_the_segmented_lut_interval(spacing, lo, hi):
+    """The plaintext polynomials of Steps 2-3 in the clear (no encryption):
+    for each segment s and each rotation r of its window (the rotations that
+    round to s N/nseg, those below zero for s = 0 read through X^N = -1),
+    the constant term of X^(-r) (p x + q) is (x - tau_s) nbr / width_s -
+    1/2 + margin, which rounds to the interval index of the segmented LUT
+    (oracle/seglut.py, the cleartext lookup of Sec. 3.1) plus the margin, at
+    several positions inside every probed interval; coefficient i + margin
+    of (a_s, b_s) holds that interval's line, and W keeps the window."""
+    from oracle import lookup as OL
+    N, nseg, margin, sx, sv, sc = 256, 4, 8, 40, 16, 50
+    sp = 63 - int(math.log2(N)) - sx
+    nbr = N - 2 * margin
+    tau = G.boundaries(lo, hi, nseg, spacing)
+    A, B = G.build(G.FUNCTIONS["silu" if spacing == "uniform" else "inv"], tau, nbr)
+    parts = OL.encode(N, nseg, nbr, margin, sx, sp, sv, sc, tau, A, B)
+    box, h = N // nseg, N // nseg // 2
+
+    def const_after(poly, r):                   # constant term of X^(-r) poly
+        return int(poly[r]) if r >= 0 else (P - int(poly[N + r])) % P
+
+    for s in range(nseg):
+        width = tau[s + 1] - tau[s]
+        rots = [s * box + d for d in range(-h, box - h)]
+        for r in rots[::7] + [rots[0], rots[-1]]:
+            pr, qr = const_after(parts["p_hat"], r), const_after(parts["q_hat"], r)
+            for i in (0, 1, nbr // 3, nbr - 2, nbr - 1):
+                for frac in (0.1, 0.45, 0.55, 0.9):
+                    x = tau[s] + (i + frac) * width / nbr
+                    v = centred(pr * OL.enc(x, sx) + qr) / 2.0 ** (sx + sp)
+                    assert abs(v - ((x - tau[s]) * nbr / width - 0.5 + margin)) < 1e-3, (s, r)
+                    I = int(G.interval_index(np.array([x]), tau, np.array([s]), nbr)[0])
+                    assert round(v) == I + margin, (s, r, i, frac, v)
+        for i in (0, nbr // 2, nbr - 1):
+            assert centred(parts["a_hat"][s, i + margin]) == centred(OL.enc(A[s][i], sv))
+            assert centred(parts["b_hat"][s, i + margin]) == centred(OL.enc(B[s][i], sx + sv))
+    # W = sum over the window of rotations of segment 0: X^d for 0 <= d < box - h,
+    # and X^d = -X^(N+d) for -h <= d < 0
+    w = [centred(c) for c in parts["window"]]
+    assert w[:box - h] == [1] * (box - h) and w[N - h:] == [-1] * h
+    assert all(c == 0 for c in w[box - h:N - h])
+
+
 # ---------------------------------------------------------- multi-value batching ---
 
 def test_multi_value_batching_trivial_exact(O):
