@@ -4,8 +4,8 @@ Each mutant is a copy of one oracle source with one plausible slip (a
 dropped term, a wrong sign, index, root or scale, a transposed operand):
 oracle/oracle.c compiled the way oracle/build.py compiles it and loaded
 through ROSETTA_ORACLE_LIB, or a Python oracle module (oracle/lookup.py,
-oracle/mini.py) executed in place of the real one, each in a fresh pytest
-process.  The pins of that part of the oracle (closed forms, the paper's
+oracle/mini.py, oracle/seglut.py) executed in place of the real one, each in
+a fresh pytest process.  The pins of that part of the oracle (closed forms, the paper's
 worked examples, phase identities and noise bounds, decryption of every
 message, agreement of the independent codings) must fail on every mutant: a
 mutant that passes them names a convention that no pin fixes.  The
@@ -216,7 +216,36 @@ PY_MUTANTS = {
             "v.append(delta * int(table[j // box]) % P)"),
     },
 }
-PY_PINS = {"lookup": LOOKUP_PINS, "mini": MINI_PINS}
+PY_MUTANTS["seglut"] = {
+    "log_spacing_linear": (
+        "logarithmic boundaries spaced linearly",
+        "t = lo * (hi / lo) ** (j / nseg)", "t = lo + (hi - lo) * j / nseg"),
+    "chebyshev_nodes_at_ends": (
+        "lines through the interval's end points instead of its Chebyshev nodes",
+        "x1, x2 = c - r * math.cos(math.pi / 4), c + r * math.cos(math.pi / 4)",
+        "x1, x2 = c - r, c + r"),
+    "intercept_at_x2": (
+        "intercept taken at the wrong node",
+        "return slope, y1 - slope * x1", "return slope, y1 - slope * x2"),
+    "segment_includes_first": (
+        "segment index counting tau_0 too",
+        "for j in range(1, len(taus) - 1):", "for j in range(0, len(taus) - 1):"),
+    "segment_strict": (
+        "x = tau_j counted in the lower segment",
+        "S += (x >= taus[j]).astype(np.int64)", "S += (x > taus[j]).astype(np.int64)"),
+    "interval_round": (
+        "interval index rounded instead of floored",
+        "I = np.floor((x - lo) / (hi - lo) * nbr).astype(np.int64)",
+        "I = np.round((x - lo) / (hi - lo) * nbr).astype(np.int64)"),
+    "protocol_q_sign": (
+        "Step 2 offset +tau_s N_br / width",
+        "q = -taus[:-1] * nbr / width", "q = taus[:-1] * nbr / width"),
+    "protocol_q_upper": (
+        "Step 2 offset from the segment's upper boundary",
+        "q = -taus[:-1] * nbr / width", "q = -taus[1:] * nbr / width"),
+}
+SEGLUT_PINS = ["tests/test_oracle_seglut.py"]
+PY_PINS = {"lookup": LOOKUP_PINS, "mini": MINI_PINS, "seglut": SEGLUT_PINS}
 
 # Runs the pins with one module of the oracle package replaced by the source
 # file given: argv = repository root, module name, source file, pin files.
@@ -312,7 +341,7 @@ def outcomes():
             return {name: f.result() for name, f in futs.items()}
 
 
-@pytest.mark.parametrize("which", ["c", "lookup", "mini"])
+@pytest.mark.parametrize("which", ["c", "lookup", "mini", "seglut"])
 def test_unmodified_oracle_passes_through_the_same_harness(outcomes, which):
     rc, failed, errored = outcomes[which + ".control"]
     assert rc == 0 and failed is None and not errored
