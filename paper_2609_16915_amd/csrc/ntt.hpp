@@ -125,11 +125,15 @@ struct Ntt {
   // before each write as well)
   static constexpr int NCROSS = (T > 64 && LOGN >= 12 && LE == 3) ? 2 : 1;
   // With 16 elements per thread the exchanges within a wave share the one
-  // cross-wave buffer (SHARED): after a cross exchange each wave reads only
-  // its own block (the reading layout keeps the wave's block), so writing
-  // that block again needs no barrier, and every cross exchange starts
-  // with one.  That keeps the LDS of a workgroup at 2N words plus the
-  // rotation amounts, so that two workgroups fit a CU.
+  // cross-wave buffer (SHARED): after a cross exchange into a layout that
+  // keeps each wave's block, each wave reads only its own block, so
+  // writing that block again needs no barrier; after one into a layout that
+  // spreads a wave over the buffer (pass 0: the second inverse transform of
+  // a step starts right after the first one's last exchange), and after the
+  // rotation and automorphism reads, the next local exchange starts with a
+  // barrier (LdsBufs::spread); every cross exchange starts with one.  That
+  // keeps the LDS of a workgroup at 2N words plus the rotation amounts, so
+  // that two workgroups fit a CU.
   static constexpr bool SHARED = LE == 4;
   // words after the twiddle area: the cross-wave buffers, then (unless
   // SHARED) one N-word buffer in which every wave exchanges within its own
@@ -755,13 +759,20 @@ __device__ __forceinline__ void wave_sync() {
 // cross(): a buffer for an exchange between waves, free of the previous
 // contents every wave may still read (alternation with one buffer in
 // between, or a barrier).  local(): the buffer of exchanges inside each
-// wave's own block; no other wave touches that block of it.
+// wave's own block; no other wave touches that block of it.  When the two
+// are one buffer (SHARED), `spread` records that some wave may still be
+// reading outside its own block (any use of cross() except an exchange
+// whose reading layout keeps each wave's block): the next local() then
+// starts with a barrier.  In the unrolled transforms the flag is known at
+// compile time; across the non-unrolled loops it is uniform.
 template <class S>
 struct LdsBufs {
   u64 *base;
   int par;
-  __device__ __forceinline__ explicit LdsBufs(u64 *b) : base(b), par(0) {}
+  bool spread;
+  __device__ __forceinline__ explicit LdsBufs(u64 *b) : base(b), par(0), spread(false) {}
   __device__ __forceinline__ u64 *cross() {
+    spread = true;
     if constexpr (S::NCROSS == 1) {
       __syncthreads();
       return base;
@@ -772,6 +783,12 @@ struct LdsBufs {
     }
   }
   __device__ __forceinline__ u64 *local() {
+    if constexpr (S::SHARED) {
+      if (spread) {
+        __syncthreads();
+        spread = false;
+      }
+    }
     return S::SHARED ? base : base + S::NCROSS * S::N;
   }
 };
@@ -798,6 +815,9 @@ __device__ __forceinline__ void ntt_exchange(u64 (&x)[S::E], LdsBufs<S> &lds, in
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < S::E; ++k) x[k] = buf[rb ^ S::swz(k << S::lo(QR))];
+    // each wave read its own block only: a local exchange may follow
+    // without a barrier
+    if constexpr (S::wave_block(QR)) lds.spread = false;
   }
 }
 
