@@ -145,11 +145,10 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
     for (uint32_t m = 0; m < N; ++m) z[m] = gl_pow(psi, bitrev(m, logn));
     // The pass structure of the kernels' transform (E = 2^le elements per
     // thread, pass 0 spanning f stages, every later pass le: ntt_le and
-    // ntt_first).  Passes after the first that span le = 3 or 4 stages run in
-    // twisted radix-8 or radix-16 form: their table region [2^s0, 2^(s0+le))
-    // (the twiddles of stages s0..s0+le-1, read by no other pass) becomes
-    // the powers q^1..q^(2^le - 1) of q = zeta[2^(le-1) (2^s0 + b)],
-    // 2^le - 1 words per block b.  The last pass (threads own E consecutive
+    // ntt_first).  Passes after the first that span le = 3 stages run in
+    // twisted radix-8 form: their table region [2^s0, 2^(s0+3)) (the
+    // twiddles of stages s0..s0+2, read by no other pass) becomes the powers
+    // q^1..q^7 of q = zeta[4 (2^s0 + b)], 7 words per block b.  The last pass (threads own E consecutive
     // indices), when it is not twisted: each of its stages s stores block
     // t nc + c (nc = E / 2^(logn - s) blocks per thread, T = N / E threads)
     // at 2^s + c T + t.
@@ -159,7 +158,7 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
       for (int s = 0; s < logn; s += begin.size() == 1 ? f : le) begin.push_back(s);
       const std::vector<u64> z0 = z;
       const int s_last = begin.back();
-      const bool last_twisted = begin.size() > 1 && (le == 3 || le == 4) && logn - s_last == le;
+      const bool last_twisted = begin.size() > 1 && le == 3 && logn - s_last == le;
       if (!last_twisted) {
         const uint32_t T = N >> le;
         for (int s = s_last; s < logn; ++s) {
@@ -170,7 +169,7 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
       }
       for (size_t q = 1; q < begin.size(); ++q) {
         const int s0 = begin[q];
-        if ((le != 3 && le != 4) || std::min(logn, s0 + le) - s0 != le) continue;
+        if (le != 3 || std::min(logn, s0 + le) - s0 != le) continue;
         const uint32_t nb = 1u << s0, np = (1u << le) - 1;
         for (uint32_t b = 0; b < nb; ++b) {
           const u64 qq = z0[(1u << (le - 1)) * (nb + b)];

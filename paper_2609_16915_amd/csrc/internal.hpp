@@ -19,7 +19,7 @@ constexpr uint32_t MAX_LWE_N = 2048;
 // elements per thread, pass 0 spanning ntt_first(logn) stages and every
 // later pass ntt_le(logn) (Ntt in ntt.hpp).  The twiddle table (abi.cpp)
 // is laid out for exactly this shape.
-constexpr int ntt_le(int logn) { return logn == 8 ? 2 : (logn == 12 ? 4 : 3); }
+constexpr int ntt_le(int logn) { return logn == 8 ? 2 : 3; }
 constexpr int ntt_first(int logn) { return logn == 11 ? 2 : ntt_le(logn); }
 
 // Per-device, per-N transform tables (device pointers) and N^-1.

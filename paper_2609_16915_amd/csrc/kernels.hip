@@ -121,16 +121,21 @@ k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta, u64
 // Waves per SIMD the blind-rotation kernel is compiled for.  Up to N = 2048
 // three workgroups fit a CU's LDS, so the kernel targets 3 waves per SIMD
 // (<= 168 registers; the few spills touch only the accumulator, read twice
-// per step).  At N = 4096 a workgroup is 256 threads of 16 elements (66 KiB
-// of LDS): two workgroups share a CU, one wave of each per SIMD, with 256
-// registers each, so that one workgroup's barrier waits overlap the other's
-// work.
+// per step; 4 waves at 128 registers, with the LDS of the N = 4096 layout
+// below, spilled 107 and ran 1010 instead of 902 ms per headline launch).
+// At N = 4096 a workgroup is 512 threads of 8 elements whose exchanges
+// share one LDS buffer (66 KiB): two workgroups share a CU, two waves of
+// each per SIMD, with 128 registers each.  The spills (about 100 registers
+// of the accumulator and the running sums) cost less than the waits that
+// two waves per SIMD leave exposed: 1297 ms per 8192 ciphertexts, against
+// 1426 ms for 16 elements per thread in 256-thread workgroups at 2 waves
+// (radix-16 passes, 5 % fewer instructions).
 #ifndef BR_WAVES_PER_EU
 #define BR_WAVES_PER_EU 3
 #endif
 template <class S>
 constexpr int br_waves_per_eu() {
-  return S::LOGN >= 12 ? 2 : BR_WAVES_PER_EU;
+  return S::LOGN >= 12 ? 4 : BR_WAVES_PER_EU;
 }
 
 // Rows of one GGSW read through a raw buffer descriptor: a wave-uniform
@@ -200,6 +205,9 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
                const u64 *__restrict__ lut, u64 *__restrict__ out, int n, int beta, int mode,
                int tp_glwe, const u64 *__restrict__ zeta) {
   constexpr int N = S::N, E = S::E, T = S::T;
+  static_assert(E <= 8, "at most 8 elements per thread");
+  // key rows a chunk at a time at the 128-register budget of N = 4096
+  constexpr bool CHUNKED = S::LOGN >= 12;
   u64 *tw = lds_dyn;
   LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   uint16_t *rot = (uint16_t *)(lds_dyn + S::TW_WORDS + S::XCHG_WORDS);
@@ -268,19 +276,19 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
 #pragma unroll 1
       for (int t = L - 1; t >= 0; --t) {
         const int row = (u * L + t) * 2 * N * 8;  // byte offset of GGSW_i[u][t][0]
-        u64 g0[E <= 8 ? E : 1], g1[E <= 8 ? E : 1];
-        // 16 elements: the first chunk of the two key rows is requested
-        // before the digit transform, so that the transform hides its
-        // latency (the later chunks overlap the chunk before them)
+        u64 g0[CHUNKED ? 1 : E], g1[CHUNKED ? 1 : E];
+        // chunked: the first chunk of the two key rows is requested before
+        // the digit transform, so that the transform hides its latency (the
+        // later chunks overlap the chunk before them)
         u64 h0[BR_KEY_CHUNK], h1[BR_KEY_CHUNK];
-        if constexpr (E > 8) {
+        if constexpr (CHUNKED) {
 #pragma unroll
           for (int k = 0; k < BR_KEY_CHUNK; ++k) {
             h0[k] = G.load(tid * 8, row + k * T * 8);
             h1[k] = G.load(tid * 8, row + (N + k * T) * 8);
           }
         }
-        if constexpr (PF && E <= 8) {
+        if constexpr (PF && !CHUNKED) {
 #pragma unroll
           for (int k = 0; k < E; ++k) {
             g0[k] = G.load(tid * 8, row + k * T * 8);
@@ -312,7 +320,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
         }
         // a5: multiply-accumulate with the two rows of GGSW_i[u][t]
         // (running sums weak until the inverse transform takes them)
-        if constexpr (E <= 8) {
+        if constexpr (!CHUNKED) {
           if constexpr (!PF) {
 #pragma unroll
             for (int k = 0; k < E; ++k) {
@@ -326,11 +334,13 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
             Y1[k] = gl_mul_add_weak(x[k], g1[k], Y1[k]);
           }
         } else {
-          // 16 elements: the key rows a chunk at a time (BR_KEY_CHUNK
-          // elements, 4 registers each), the next chunk requested before
-          // the products of the current one, so that 2 chunks rather than
-          // 64 registers hold them (chunks of 2: 1409 ms per 8192
-          // ciphertexts at N = 4096, 4: 1433, 8: 1500, unpipelined 4: 1445)
+          // the key rows a chunk at a time (BR_KEY_CHUNK elements, 4
+          // registers each), the next chunk requested before the products
+          // of the current one, so that 2 chunks rather than 32 registers
+          // hold them (N = 4096, per 8192 ciphertexts: chunks of 2 with a
+          // scheduling fence between chunks 1297 ms, without it 1327,
+          // chunks of 4: 1489, all rows after the transform: 1321; at
+          // N = 2048, 3 waves, chunks of 2 ran 908 against 902 ms)
 #pragma unroll
           for (int k0 = 0; k0 < E; k0 += BR_KEY_CHUNK) {
             u64 n0[BR_KEY_CHUNK], n1[BR_KEY_CHUNK];
@@ -428,12 +438,11 @@ __device__ __forceinline__ u64 automorphism_coef(const u64 *a, int j, u32 dinv) 
 #ifndef TRACE_WAVES_PER_EU
 #define TRACE_WAVES_PER_EU 3
 #endif
-// At N = 4096 (16 elements per thread, 64-bit digits) the trace kernel
-// takes the whole register file of a SIMD (one wave): its live state is
-// about 300 registers, and the allocator fails on it at two waves.
+// At N = 4096 a workgroup is 512 threads (8 waves): two waves per SIMD,
+// one workgroup per CU (its 64-bit digits keep about 190 registers live).
 template <class S>
 constexpr int trace_waves_per_eu() {
-  return S::LOGN >= 12 ? 1 : TRACE_WAVES_PER_EU;
+  return S::LOGN >= 12 ? 2 : TRACE_WAVES_PER_EU;
 }
 
 template <class S, int L>
@@ -511,24 +520,10 @@ k_trace(const u64 *__restrict__ in, const u64 *__restrict__ autk, u64 *__restric
         ntt_forward<S>(x, lds, tid, tw);
       }
       gconst_u64 *g = G + (size_t)(t * 2) * N;
-      if constexpr (E <= 8) {
 #pragma unroll
-        for (int k = 0; k < E; ++k) {
-          Y0[k] = gl_mul_add_weak(x[k], g[k * T], Y0[k]);
-          Y1[k] = gl_mul_add_weak(x[k], g[N + k * T], Y1[k]);
-        }
-      } else {
-        // 16 elements: the key rows a quarter at a time, as in the blind
-        // rotation
-#pragma unroll
-        for (int k0 = 0; k0 < E; k0 += BR_KEY_CHUNK) {
-#pragma unroll
-          for (int k = k0; k < k0 + BR_KEY_CHUNK; ++k) {
-            Y0[k] = gl_mul_add_weak(x[k], g[k * T], Y0[k]);
-            Y1[k] = gl_mul_add_weak(x[k], g[N + k * T], Y1[k]);
-          }
-          BR_CHUNK_FENCE();
-        }
+      for (int k = 0; k < E; ++k) {
+        Y0[k] = gl_mul_add_weak(x[k], g[k * T], Y0[k]);
+        Y1[k] = gl_mul_add_weak(x[k], g[N + k * T], Y1[k]);
       }
     }
 #pragma unroll

@@ -20,8 +20,9 @@
 //   j = (tid mod 2^lo) + (k << lo) + ((tid >> lo) << (lo + LE)).
 // Pass 0 is the natural layout j = tid + T*k (lo_0 = LOGN - LE).
 // Butterflies inside a pass are register-only; between passes the workgroup
-// transposes through LDS (one write, one barrier, one read), alternating
-// between two buffers so that one barrier per transpose suffices.
+// transposes through LDS: between waves a barrier, the writes, a barrier and
+// the reads; within each wave (both layouts keep the wave's block) a
+// wave-level fence between writes and reads (ntt_exchange).
 //
 // LDS word addresses of the transposes go through a linear XOR swizzle
 // (bit b < 5 of the address is flipped by the parity of j & SWZ_MASK[b],
@@ -44,10 +45,6 @@ namespace rosetta {
 typedef const u64 __attribute__((address_space(1))) gconst_u64;
 
 constexpr unsigned SWZ_MASK[5] = {0x7b0, 0x574, 0x538, 0xa60, 0x3e0};
-// the same search for the layouts of 16 elements per thread at N = 4096
-// (pass lo = 8, 4, 0), which the masks above leave one bank short in one
-// of them
-constexpr unsigned SWZ_MASK16[5] = {0xcea, 0xc2c, 0x218, 0xa70, 0xdc0};
 
 __host__ __device__ constexpr int swz_masks(int j, const unsigned *m) {
   int a = j;
@@ -88,17 +85,8 @@ struct Ntt {
   __host__ __device__ static constexpr bool twisted(int q) {
     return q >= 1 && LE == 3 && stage_end(q) - stage_begin(q) == 3;
   }
-  // The same for passes of four stages with 16 elements per thread: the
-  // region [2^s0, 2^(s0+4)) holds q^1..q^15 of q = zeta[8 (2^s0 + b)] at
-  // 2^s0 + 15 b (15 words per block fill it exactly; the odd stride keeps
-  // the blocks of a half wave on distinct banks).
-  __host__ __device__ static constexpr bool twisted16(int q) {
-    return q >= 1 && LE == 4 && stage_end(q) - stage_begin(q) == 4;
-  }
   // word address of index j in an exchange buffer
-  __host__ __device__ static constexpr int swz(int j) {
-    return swz_masks(j, LE == 4 ? SWZ_MASK16 : SWZ_MASK);
-  }
+  __host__ __device__ static constexpr int swz(int j) { return swz_masks(j, SWZ_MASK); }
   // A twisted pass whose first stage is s0 <= 2 has q = zeta[4 (2^s0 + b)]
   // among the 64th roots of unity, which are powers of two; when, in
   // addition, lo >= 6, the block b = tid >> lo is the wave's index, so the
@@ -120,25 +108,21 @@ struct Ntt {
   __host__ __device__ static constexpr bool local_exchange(int qa, int qb) {
     return wave_block(qa) && wave_block(qb);
   }
-  // exchange buffers that move data between waves: two (used alternately,
-  // one barrier per exchange) when the LDS allows it, else one (a barrier
-  // before each write as well)
-  static constexpr int NCROSS = (T > 64 && LOGN >= 12 && LE == 3) ? 2 : 1;
-  // With 16 elements per thread the exchanges within a wave share the one
-  // cross-wave buffer (SHARED): after a cross exchange into a layout that
-  // keeps each wave's block, each wave reads only its own block, so
-  // writing that block again needs no barrier; after one into a layout that
-  // spreads a wave over the buffer (pass 0: the second inverse transform of
-  // a step starts right after the first one's last exchange), and after the
-  // rotation and automorphism reads, the next local exchange starts with a
-  // barrier (LdsBufs::spread); every cross exchange starts with one.  That
-  // keeps the LDS of a workgroup at 2N words plus the rotation amounts, so
-  // that two workgroups fit a CU.
-  static constexpr bool SHARED = LE == 4;
-  // words after the twiddle area: the cross-wave buffers, then (unless
+  // At N = 4096 the exchanges within a wave share the one cross-wave buffer
+  // (SHARED): after a cross exchange into a layout that keeps each wave's
+  // block, each wave reads only its own block, so writing that block again
+  // needs no barrier; after one into a layout that spreads a wave over the
+  // buffer (pass 0: the second inverse transform of a step starts right
+  // after the first one's last exchange), and after the rotation and
+  // automorphism reads, the next local exchange starts with a barrier
+  // (LdsBufs::spread); every cross exchange starts with one.  That keeps the
+  // LDS of a workgroup at 2N words plus the rotation amounts, so that two
+  // 512-thread workgroups fit a CU.
+  static constexpr bool SHARED = LOGN >= 12;
+  // words after the twiddle area: the cross-wave buffer, then (unless
   // SHARED) one N-word buffer in which every wave exchanges within its own
   // block
-  static constexpr int XCHG_WORDS = (NCROSS + (SHARED ? 0 : 1)) * N;
+  static constexpr int XCHG_WORDS = (SHARED ? 1 : 2) * N;
 };
 
 // Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
@@ -563,113 +547,6 @@ __device__ __forceinline__ void ntt_inv_pass_shift_twist(u64 (&x)[S::E]) {
   });
 }
 
-// Twisted radix-16 form of a four-stage pass (16 elements per thread).  The
-// stage s0 + t twiddle of the thread's sub-block c (c < 2^t) is
-// zeta[2^t (2^s0 + b)] zeta[c] (the two indices have disjoint bits, so
-// their bit reversals add), and zeta[2^t m] = q^(2^(3-t)) for q =
-// zeta[8 m], m = 2^s0 + b.  The merged stages therefore evaluate the
-// block polynomial sum x_k Z^k at q times 16th roots of unity: the twist
-// y_k = q^k x_k (15 products, powers from the table region of the pass),
-// then the fixed 16-point network whose stage-t twiddle is zeta[c], a
-// power of two (mul_small_root).  The inverse (Gentleman-Sande) stages use
-// zeta[2^(s+1) - 1 - B] = zeta[2^t (2^s0 + b_r)] zeta[2^t - 1 - c] with the
-// reflected block b_r = 2^s0 - 1 - b; the q_r = zeta[8 (2^s0 + b_r)] parts
-// are the same within every butterfly pair, so they come out of the network
-// as the untwist x_k = q_r^k z_k at the end.
-//
-// Weak forward form (W): as in the radix-8 pass, only x[0] may arrive
-// non-canonical, and a sum must leave canonical when a later butterfly takes
-// it, directly or through first operands, as the second operand of a
-// twiddle-1 butterfly (r16_keep_canonical).
-__host__ __device__ constexpr bool r16_keep_canonical(int t, int k) {
-  if (t >= 3) return false;
-  const int bit = 1 << (2 - t);  // split bit of stage t + 1
-  if (k & bit) return (k >> (3 - t)) == 0;  // second operand there, twiddle zeta[0] = 1
-  return r16_keep_canonical(t + 1, k);
-}
-
-// x_k <- q^k x_k for k = 1..15, the powers read from the LDS table a few
-// at a time (R16_TWIST_CHUNK), so that they do not all hold registers at
-// once next to the sixteen elements.
-#ifndef R16_TWIST_CHUNK
-#define R16_TWIST_CHUNK 5
-#endif
-#ifndef TWIST_LOAD_FENCE
-#define TWIST_LOAD_FENCE()
-#endif
-__device__ __forceinline__ void r16_twist(u64 (&x)[16], const u64 *qp) {
-  TWIST_LOAD_FENCE();
-  static_for<0, (15 + R16_TWIST_CHUNK - 1) / R16_TWIST_CHUNK>([&](auto cc) {
-    constexpr int k0 = 1 + decltype(cc)::value * R16_TWIST_CHUNK;
-    constexpr int k1 = k0 + R16_TWIST_CHUNK < 16 ? k0 + R16_TWIST_CHUNK : 16;
-    static_for<k0, k1>([&](auto kc) {
-      constexpr int k = decltype(kc)::value;
-      x[k] = gl_mul(x[k], qp[k - 1]);
-    });
-    if constexpr (k1 < 16) __builtin_amdgcn_sched_barrier(0);
-  });
-}
-
-template <class S, int Q, bool W = false>
-__device__ __forceinline__ void ntt_fwd_pass_twisted16(u64 (&x)[S::E], int tid, const u64 *tw) {
-  static_assert(S::E == 16, "sixteen elements per thread");
-  constexpr int lo = S::lo(Q), s0 = S::stage_begin(Q);
-  const int b = tid >> lo;  // block at stage s0
-  const u64 *qp = tw + (1 << s0) + 15 * b;  // q^1 .. q^15
-  r16_twist(x, qp);
-  static_for<0, 4>([&](auto tc) {
-    constexpr int t = decltype(tc)::value;
-    constexpr int span = 8 >> t;
-    static_for<0, 16>([&](auto kc) {
-      constexpr int k = decltype(kc)::value;
-      if constexpr (!(k & span)) {
-        constexpr int k2 = k | span, c = k >> (4 - t);
-        const u64 u = x[k];
-        if constexpr (c == 0) {
-          const u64 v = x[k2];
-          x[k] = (!W || r16_keep_canonical(t, k)) ? gl_add(u, v) : fwd_sum<W>(u, v);
-          x[k2] = gl_sub(u, v);
-        } else if constexpr (small_root_negative<c>()) {  // w = -|w|
-          const u64 v = mul_small_root<c>(x[k2]);
-          x[k] = gl_sub(u, v);
-          x[k2] = (!W || r16_keep_canonical(t, k2)) ? gl_add(u, v) : fwd_sum<W>(u, v);
-        } else {
-          const u64 v = mul_small_root<c>(x[k2]);
-          x[k] = (!W || r16_keep_canonical(t, k)) ? gl_add(u, v) : fwd_sum<W>(u, v);
-          x[k2] = gl_sub(u, v);
-        }
-      }
-    });
-  });
-}
-
-template <class S, int Q>
-__device__ __forceinline__ void ntt_inv_pass_twisted16(u64 (&x)[S::E], int tid, const u64 *tw) {
-  static_assert(S::E == 16, "sixteen elements per thread");
-  constexpr int lo = S::lo(Q), s0 = S::stage_begin(Q);
-  const int br = (1 << s0) - 1 - (tid >> lo);  // reflected block
-  const u64 *qp = tw + (1 << s0) + 15 * br;    // powers of q_r
-  static_for<0, 4>([&](auto rc) {
-    constexpr int t = 3 - decltype(rc)::value;
-    constexpr int span = 8 >> t;
-    static_for<0, 16>([&](auto kc) {
-      constexpr int k = decltype(kc)::value;
-      if constexpr (!(k & span)) {
-        constexpr int k2 = k | span, m = (1 << t) - 1 - (k >> (4 - t));
-        const u64 u = x[k], v = x[k2];
-        x[k] = gl_add(u, v);
-        if constexpr (m == 0)
-          x[k2] = gl_sub(v, u);
-        else if constexpr (small_root_negative<m>())  // (v - u)(-|w|) = (u - v)|w|
-          x[k2] = mul_small_root<m>(gl_sub(u, v));
-        else
-          x[k2] = mul_small_root<m>(gl_sub(v, u));
-      }
-    });
-  });
-  r16_twist(x, qp);
-}
-
 // Dispatch of a shift-twisted pass to the copy of the wave's block b
 // (wave-uniform, so the branches are scalar).
 template <class S, int Q, bool W, int B = 0>
@@ -768,19 +645,12 @@ __device__ __forceinline__ void wave_sync() {
 template <class S>
 struct LdsBufs {
   u64 *base;
-  int par;
   bool spread;
-  __device__ __forceinline__ explicit LdsBufs(u64 *b) : base(b), par(0), spread(false) {}
+  __device__ __forceinline__ explicit LdsBufs(u64 *b) : base(b), spread(false) {}
   __device__ __forceinline__ u64 *cross() {
     spread = true;
-    if constexpr (S::NCROSS == 1) {
-      __syncthreads();
-      return base;
-    } else {
-      u64 *p = base + par * S::N;
-      par ^= 1;
-      return p;
-    }
+    __syncthreads();
+    return base;
   }
   __device__ __forceinline__ u64 *local() {
     if constexpr (S::SHARED) {
@@ -789,7 +659,7 @@ struct LdsBufs {
         spread = false;
       }
     }
-    return S::SHARED ? base : base + S::NCROSS * S::N;
+    return S::SHARED ? base : base + S::N;
   }
 };
 
@@ -830,8 +700,6 @@ __device__ __forceinline__ void ntt_fwd_from(u64 (&x)[S::E], LdsBufs<S> &lds, in
     ntt_fwd_shift_twist_block<S, Q, W>(x, __builtin_amdgcn_readfirstlane(tid >> S::lo(Q)));
   else if constexpr (S::twisted(Q))
     ntt_fwd_pass_twisted<S, Q, W>(x, tid, tw);
-  else if constexpr (S::twisted16(Q))
-    ntt_fwd_pass_twisted16<S, Q, W>(x, tid, tw);
   else
     ntt_fwd_pass<S, Q, W>(x, tid, tw);
   if constexpr (Q + 1 < S::PASSES) {
@@ -849,8 +717,6 @@ __device__ __forceinline__ void ntt_inv_from(u64 (&x)[S::E], LdsBufs<S> &lds, in
     ntt_inv_shift_twist_block<S, Q>(x, __builtin_amdgcn_readfirstlane(tid >> S::lo(Q)));
   else if constexpr (S::twisted(Q))
     ntt_inv_pass_twisted<S, Q>(x, tid, tw);
-  else if constexpr (S::twisted16(Q))
-    ntt_inv_pass_twisted16<S, Q>(x, tid, tw);
   else
     ntt_inv_pass<S, Q>(x, tid, tw);
   if constexpr (Q > 0) {
