@@ -194,7 +194,7 @@ size_t br_lds_bytes(int n) {
 // ciphertexts (workgroup b uses selector b / g), so that one encrypted
 // index selects in several ciphertexts at once.
 #ifndef BR_KEY_CHUNK
-#define BR_KEY_CHUNK 2
+#define BR_KEY_CHUNK 1
 #endif
 #ifndef BR_CHUNK_FENCE
 #define BR_CHUNK_FENCE() __builtin_amdgcn_sched_barrier(0)
@@ -337,10 +337,12 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
           // the key rows a chunk at a time (BR_KEY_CHUNK elements, 4
           // registers each), the next chunk requested before the products
           // of the current one, so that 2 chunks rather than 32 registers
-          // hold them (N = 4096, per 8192 ciphertexts: chunks of 2 with a
-          // scheduling fence between chunks 1297 ms, without it 1327,
-          // chunks of 4: 1489, all rows after the transform: 1321; at
-          // N = 2048, 3 waves, chunks of 2 ran 908 against 902 ms)
+          // hold them (N = 4096, ms per 8192 ciphertexts on one box: chunks
+          // of 1 1322 and 1329 against 1346 and 1349 for chunks of 2; on
+          // another, chunks of 2 with a scheduling fence between chunks
+          // 1297, without it 1327, chunks of 4 1489, all rows after the
+          // transform 1321; at N = 2048, 3 waves, chunks of 2 ran 908
+          // against 902 ms unchunked)
 #pragma unroll
           for (int k0 = 0; k0 < E; k0 += BR_KEY_CHUNK) {
             u64 n0[BR_KEY_CHUNK], n1[BR_KEY_CHUNK];
