@@ -341,7 +341,7 @@ CORNERS = {
     # the largest LWE dimension
     "n2048_N2048": dict(n=2048, N=2048, pbs_level=3, pbs_base_log=8, ks_level=2, ks_base_log=8,
                         msg_bits=3),
-    # the largest ring, general first stage, 2 waves per SIMD
+    # the largest ring, general first stage, 4 waves per SIMD
     "l4_b15_N4096": dict(n=24, N=4096, pbs_level=4, pbs_base_log=15, ks_level=3, ks_base_log=6,
                          msg_bits=3),
     # small-digit first stages (integer stages 0-1) at the rings no workload uses
