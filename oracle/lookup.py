@@ -8,13 +8,20 @@ rosetta_lookup_params, written out here independently:
   Step 1  y_j = [[x]]_cmp - round(tau_j 2^sc); c_j = PBS(y_j, v = mu) + mu,
           mu = floor(p / 4 nseg); S = sum_j c_j.
           With a refinement of k bits (refine = k > 0) the comparison
-          chains four PBS instead (the paper's HomComp chains several, Sec.
-          3.2 Step 1), so that its resolution is 2^k times finer:
+          chains three blind rotations instead (the paper's HomComp chains
+          several PBS, Sec. 3.2 Step 1), so that its resolution is 2^k times
+          finer:
             y'  = y_j + h,  h = floor(p / 2^(k+1))      (half a digit D = p/2^k)
             z   = 2^k y'                                 (fine phase phi)
-            s1' = PBS(z, floor(p/4)),  s1 = PBS(z, floor(p / 2^(k+2)))
+            e   = SE(BlindRot(z, c1)),  c1 = floor(p / 2^(k+2))
+            s1  = KS(e),  s1' = KS(2^k e)                (signs of z at the coarse
+                                                          and, within 2^k, the
+                                                          fine scale p/4)
             s2  = PBS(z - s1', f),  f(phi) = -phi / 2^k on [-p/4, p/4)
             c_j = PBS(y_j - s1 + s2, mu) + mu
+          One blind rotation gives both signs: the extracted ciphertext is
+          scaled before the key switch, so that its small blind-rotation
+          noise, not the key switch's, is what 2^k multiplies.
           y' - s1 + s2 is about D round(y'/D), a whole number of digits,
           and it is at least D exactly when y_j >= 0, so the last sign
           bootstrap decides half a digit away from zero; only y_j within the
@@ -43,21 +50,20 @@ def enc(v: float, k: int) -> int:
 
 
 def refine_polys(N, k):
-    """Test polynomials of the refined comparison: the constants floor(p/4)
-    and floor(p / 2^(k+2)) (signs at the fine and the coarse scale) and
-    f with coefficient j = -round(w_j p / (2^(k+1) N)), w_j = min(j, N - j)
+    """Test polynomials of the refined comparison: the constant
+    floor(p / 2^(k+2)) (the sign at the coarse scale; 2^k times it, the fine
+    one) and f with coefficient j = -round(w_j p / (2^(k+1) N)), w_j = min(j, N - j)
     (rounded half up): a rotation r < N/2 selects f_r, the value at phase
     r p / 2N, and a rotation r >= 3N/2 selects -f_(r-N), the value at phase
     (r - 2N) p / 2N, so that on phases in [-p/4, p/4) the bootstrap returns
     -phase / 2^k."""
-    q4 = np.full(N, P // 4, np.uint64)
     c1 = np.full(N, P // 2 ** (k + 2), np.uint64)
     f = np.zeros(N, np.uint64)
     for j in range(N):
         w = min(j, N - j)
         g = (2 * w * P + 2 ** (k + 1) * N) // (2 ** (k + 2) * N)   # round half up
         f[j] = (P - g) % P
-    return q4, c1, f
+    return c1, f
 
 
 def encode(N, nseg, nbr, margin, sx, sp, sv, sc, tau, a, b, refine=0):
@@ -94,14 +100,14 @@ def encode(N, nseg, nbr, margin, sx, sp, sv, sc, tau, a, b, refine=0):
     out = dict(p_hat=p_hat, q_hat=q_hat, a_hat=a_hat, b_hat=b_hat, window=window,
                sign_lut=sign_lut, consts=consts, refine=refine)
     if refine:
-        out["q4"], out["c1"], out["f"] = refine_polys(N, refine)
+        out["c1"], out["f"] = refine_polys(N, refine)
     return out
 
 
 def block(parts) -> np.ndarray:
     """The library's plaintext block order: p, q, a_s, b_s, W, sign LUT, then
-    with a refined comparison its three test polynomials."""
-    extra = [parts["q4"], parts["c1"], parts["f"]] if parts.get("refine") else []
+    with a refined comparison its two test polynomials."""
+    extra = [parts["c1"], parts["f"]] if parts.get("refine") else []
     return np.concatenate([parts["p_hat"], parts["q_hat"], parts["a_hat"].reshape(-1),
                            parts["b_hat"].reshape(-1), parts["window"], parts["sign_lut"],
                            *extra])
@@ -127,8 +133,8 @@ def compare(prm, ks, parts, ys, kind=O.NTT, nthreads=0, want_steps=False):
     mu_poly = parts["sign_lut"]
     mu = int(mu_poly[0])
 
-    def pbs(cts, v):
-        return O.pbs(prm, cts, ks.bsk, ks.ksk, v, kind, nthreads)
+    def pbs(cts, v, want_big=False):
+        return O.pbs(prm, cts, ks.bsk, ks.ksk, v, kind, nthreads, want_big=want_big)
 
     steps = {}
     if k == 0:
@@ -138,8 +144,8 @@ def compare(prm, ks, parts, ys, kind=O.NTT, nthreads=0, want_steps=False):
         yp = ys.copy()
         yp[:, n] = (yp[:, n].astype(object) + h) % P
         z = lwe_scale(yp, 2 ** k)
-        s1p = pbs(z, parts["q4"])
-        s1 = pbs(z, parts["c1"])
+        s1, e = pbs(z, parts["c1"], want_big=True)
+        s1p = np.stack([O.keyswitch(prm, row, ks.ksk) for row in lwe_scale(e, 2 ** k)])
         s2 = pbs(lwe_sub(z, s1p), parts["f"])
         y2 = lwe_add(lwe_sub(ys, s1), s2)
         steps = dict(z=z, s1p=s1p, s1=s1, s2=s2, y2=y2)

@@ -24,8 +24,8 @@ def test_refine_poly_is_minus_phase_over_2k(O, N, k):
     ciphertext of phase r p / 2N) leaves round(-phase / 2^k) in the constant
     term for every phase in the padded half [-p/4, p/4), and, f being
     negacyclic, the value of phase - p/2 negated on the other half."""
-    q4, c1, f = OL.refine_polys(N, k)
-    assert int(q4[0]) == P // 4 and int(c1[0]) == P // 2 ** (k + 2)
+    c1, f = OL.refine_polys(N, k)
+    assert all(int(c) == P // 2 ** (k + 2) for c in c1)
     for r in list(range(0, 2 * N, max(1, N // 64))) + [N // 2 - 1, N // 2, 3 * N // 2 - 1,
                                                          3 * N // 2, 2 * N - 1]:
         const = int(O.monomial_mul(f, (2 * N - r) % (2 * N))[0])
@@ -51,7 +51,7 @@ def _grid_compare(O, refine, n, N, sc_steps, want_steps=False):
     nseg = 4
     parts = {"sign_lut": np.full(N, P // (4 * nseg), np.uint64), "refine": refine}
     if refine:
-        parts["q4"], parts["c1"], parts["f"] = OL.refine_polys(N, refine)
+        parts["c1"], parts["f"] = OL.refine_polys(N, refine)
     ys = np.array([round(s * P / (2 * N)) % P for s in sc_steps], dtype=np.uint64)
     cts = O.lwe_encrypt_plain(77, 0.0, ks.lwe_key, ys)
     c, steps = OL.compare(prm, ks, parts, cts, want_steps=True)

@@ -139,6 +139,9 @@ PY_MUTANTS = {
             "coarse sign of p / 2^(k+1) instead of p / 2^(k+2)",
             "c1 = np.full(N, P // 2 ** (k + 2), np.uint64)",
             "c1 = np.full(N, P // 2 ** (k + 1), np.uint64)"),
+        "refine_fine_sign_unscaled": (
+            "fine sign taken from the extracted ciphertext without the 2^k scale",
+            "lwe_scale(e, 2 ** k)", "lwe_scale(e, 1)"),
         "refine_fine_input": (
             "fine bootstrap on z instead of z - s1' (a quarter-phase off)",
             "s2 = pbs(lwe_sub(z, s1p), parts[\"f\"])", "s2 = pbs(z, parts[\"f\"])"),
