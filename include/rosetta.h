@@ -412,11 +412,14 @@ rosetta_status rosetta_sample_extract(const uint64_t *glwe_in, uint64_t *big_out
  *    else 0 (up to noise; inputs within the bootstrap's resolution of tau_j
  *    may fall on either side).  S = sum_j of them: the segment index at scale
  *    2 mu ~ p / 2 nseg, i.e. a rotation by S N / nseg.
- *    With cmp_refine_log = k > 0 each comparison chains four PBS (the paper's
- *    HomComp chains several for precision), which divides the resolution
- *    by 2^k: with h = floor(p / 2^(k+1)),
+ *    With cmp_refine_log = k > 0 each comparison chains three blind
+ *    rotations (the paper's HomComp chains several PBS for precision), which
+ *    divides the resolution by 2^k: with h = floor(p / 2^(k+1)),
  *      z   = 2^k (y_j + (0, h)),
- *      s1' = PBS(z, floor(p/4)),  s1 = PBS(z, floor(p / 2^(k+2))),
+ *      e   = SE(BlindRot(z, floor(p / 2^(k+2)))),  s1 = KS(e),
+ *      s1' = KS(2^k e) (the sign at the fine scale, within 2^k of p/4; e
+ *            is scaled before the key switch so that 2^k multiplies only
+ *            the blind rotation's noise),
  *      s2  = PBS(z - s1', f),  f_i = -round(min(i, N-i) p / (2^(k+1) N))
  *            (half up; the bootstrap then returns -phase / 2^k on phases
  *            in [-p/4, p/4), where z - s1' lies),
@@ -450,7 +453,7 @@ rosetta_status rosetta_sample_extract(const uint64_t *glwe_in, uint64_t *big_out
  *
  * The plaintext block [(4 + 2 nseg) N] words: p, q, a_0..a_{nseg-1},
  * b_0..b_{nseg-1}, W, the sign test polynomial, then with a refined
- * comparison floor(p/4), floor(p / 2^(k+2)) and f (3 N more); constants [nseg]:
+ * comparison floor(p / 2^(k+2)) and f (2 N more); constants [nseg]:
  * -round(tau_j 2^sc) mod p for j = 1..nseg-1, then (nseg-1) mu. */
 typedef struct rosetta_lookup_params {
   uint32_t nseg;           /* N_seg, a power of two in [2, 16] */
@@ -463,10 +466,11 @@ typedef struct rosetta_lookup_params {
   uint32_t trace_level;    /* automorphism key levels */
   uint32_t trace_base_log; /* automorphism key base log */
   uint32_t cmp_refine_log; /* k: bits of refinement of the comparison (0: one sign
-                              bootstrap per boundary; 1..6: four, see Step 1) */
+                              bootstrap per boundary; 1..6: three blind
+                              rotations and four key switches, see Step 1) */
 } rosetta_lookup_params;
 
-/* Words of the plaintext block: (4 + 2 nseg) N, plus 3 N with a refined
+/* Words of the plaintext block: (4 + 2 nseg) N, plus 2 N with a refined
  * comparison. */
 size_t rosetta_lookup_plain_words(const rosetta_params *params,
                                   const rosetta_lookup_params *lp);
@@ -505,8 +509,9 @@ size_t rosetta_lookup_workspace_offset(const rosetta_params *params,
 /* Steps 1-3 for a batch: x_rlwe [batch][2N], x_cmp [batch][n+1], prepared
  * keys (bootstrapping, key switching, automorphism), the prepared plaintext
  * block and the host constants; out [batch][2N] (device, not overlapping the
- * workspace).  Per input: nseg-1 PBS (Step 1; 4 (nseg-1) with a refined
- * comparison), one blind rotation of an
+ * workspace).  Per input: nseg-1 PBS (Step 1; with a refined comparison
+ * 3 (nseg-1) blind rotations and 4 (nseg-1) key switches), one blind
+ * rotation of an
  * encrypted test polynomial + extraction + key switch (Step 2), nseg + 1
  * blind rotations of encrypted test polynomials and traces (Step 3), and
  * nseg + 2 plaintext products. */

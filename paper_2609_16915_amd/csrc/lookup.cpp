@@ -93,10 +93,9 @@ struct Block {
   size_t window() const { return (2 + 2 * nseg) * N; }
   size_t sign_lut() const { return (3 + 2 * nseg) * N; }
   // the refined comparison's test polynomials (present when refine > 0)
-  size_t quarter() const { return (4 + 2 * nseg) * N; }
-  size_t coarse_sign() const { return (5 + 2 * nseg) * N; }
-  size_t fine_part() const { return (6 + 2 * nseg) * N; }
-  size_t words() const { return (4 + 2 * nseg + (refine ? 3 : 0)) * N; }
+  size_t coarse_sign() const { return (4 + 2 * nseg) * N; }
+  size_t fine_part() const { return (5 + 2 * nseg) * N; }
+  size_t words() const { return (4 + 2 * nseg + (refine ? 2 : 0)) * N; }
 };
 
 struct Scratch {
@@ -131,7 +130,7 @@ size_t lookup_ws_words(const rosetta_params *p, const rosetta_lookup_params *lp,
       batch * 2 * N,         // 9 R
       batch * 2 * N,         // 10 R spread over the windows
       rf * batch * nc * w,   // 11 z = 2^k (y + h)
-      rf * batch * nc * w,   // 12 s1' (sign of z at the fine scale)
+      rf * batch * nc * w,   // 12 s1' (sign of z at the fine scale, 2^k s1 before the KS)
       rf * batch * nc * w,   // 13 s1 (sign of z at the coarse scale)
       rf * batch * nc * w,   // 14 z - s1'
       rf * batch * nc * w,   // 15 s2 (-phase / 2^k)
@@ -202,15 +201,14 @@ rosetta_status rosetta_lookup_encode(const rosetta_params *p, const rosetta_look
     consts[j - 1] = t;
   }
   consts[ns - 1] = gl_mul(mu, (u64)(ns - 1));
-  // the refined comparison: floor(p/4), floor(p / 2^(k+2)) and
+  // the refined comparison: floor(p / 2^(k+2)) and
   // f_i = -round(min(i, N-i) p / (2^(k+1) N)) (half up)
   if (const int k = (int)lp->cmp_refine_log) {
-    const u64 q4 = GL_P / 4, c1 = GL_P >> (k + 2);
+    const u64 c1 = GL_P >> (k + 2);
     const unsigned __int128 den = (unsigned __int128)N << (k + 2);
     for (int j = 0; j < N; ++j) {
       const u64 w = (u64)(j < N - j ? j : N - j);
       const u64 g = (u64)(((unsigned __int128)2 * w * GL_P + (den >> 1)) / den);
-      plain[B.quarter() + j] = q4;
       plain[B.coarse_sign() + j] = c1;
       plain[B.fine_part() + j] = g ? GL_P - g : 0;
     }
@@ -292,8 +290,10 @@ rosetta_status rosetta_lookup_eval(const uint64_t *x_rlwe, const uint64_t *x_cmp
   if ((st = rosetta_lwe_add_consts(x_cmp, consts, ws[0], batch, nc, n, s))) return st;
   const uint64_t *cmp_in = ws[0];
   if (const int k = (int)lp->cmp_refine_log) {
-    // z = 2^k (y + h); s1', s1 its signs at the fine and the coarse scale;
-    // s2 = -(z - s1') / 2^k; the sign bootstrap then takes y - s1 + s2
+    // z = 2^k (y + h); s1, s1' its signs at the coarse and the fine scale
+    // from one blind rotation (the extracted ciphertexts key-switched, then
+    // scaled by 2^k and key-switched again); s2 = -(z - s1') / 2^k; the
+    // sign bootstrap then takes y - s1 + s2
     uint64_t shifted[MAX_MONOMIALS / 4];
     const u64 h = GL_P >> (k + 1);
     for (uint32_t j = 0; j < nc; ++j) shifted[j] = gl_add(consts[j], h);
@@ -301,12 +301,14 @@ rosetta_status rosetta_lookup_eval(const uint64_t *x_rlwe, const uint64_t *x_cmp
     if ((st = rosetta_lwe_combine(ws[11], (u64)1 << k, nullptr, 0, nullptr, 0, ws[11], cmp_words,
                                   s)))
       return st;
-    if ((st = rosetta_pbs_batch_ws(ws[11], bsk_dev, ksk_dev, plain_prep_dev + B.quarter(), ws[12],
-                                   cmp_cts, p, ws[1], pbs_ws, s)))
+    if ((st = rosetta_blind_rotate_extract(ws[11], bsk_dev, plain_prep_dev + B.coarse_sign(),
+                                           ws[1], cmp_cts, p, s)))
       return st;
-    if ((st = rosetta_pbs_batch_ws(ws[11], bsk_dev, ksk_dev, plain_prep_dev + B.coarse_sign(),
-                                   ws[13], cmp_cts, p, ws[1], pbs_ws, s)))
+    if ((st = rosetta_keyswitch(ws[1], ksk_dev, ws[13], cmp_cts, p, s))) return st;
+    if ((st = rosetta_lwe_combine(ws[1], (u64)1 << k, nullptr, 0, nullptr, 0, ws[1],
+                                  cmp_cts * (N + 1), s)))
       return st;
+    if ((st = rosetta_keyswitch(ws[1], ksk_dev, ws[12], cmp_cts, p, s))) return st;
     if ((st = rosetta_lwe_combine(ws[11], 1, ws[12], GL_P - 1, nullptr, 0, ws[14], cmp_words, s)))
       return st;
     if ((st = rosetta_pbs_batch_ws(ws[14], bsk_dev, ksk_dev, plain_prep_dev + B.fine_part(),

@@ -42,7 +42,7 @@ def test_encoder_matches_oracle(N, fn, lo, hi, spacing, refine):
     plain, consts = R.lookup_encode(prm, lp, tau, a, b)
     parts = OL.encode(N, lp.nseg, lp.nbr, lp.margin, lp.x_scale_log, lp.coef_scale_log,
                       lp.val_scale_log, lp.cmp_scale_log, tau, a, b, refine=refine)
-    assert plain.size == (4 + 2 * lp.nseg + (3 if refine else 0)) * N
+    assert plain.size == (4 + 2 * lp.nseg + (2 if refine else 0)) * N
     assert np.array_equal(plain, OL.block(parts))
     assert np.array_equal(consts, parts["consts"])
 
