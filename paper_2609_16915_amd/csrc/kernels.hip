@@ -171,9 +171,9 @@ __device__ __forceinline__ u64 rotated_coef(const u64 *v, int j, int r) {
 //   a6  ACC_c += inverse transform of Y_c
 // The transform-domain key rows are pre-scaled by N^-1 (k_bsk_prepare).
 // RT holds the rounded value before digit extraction: 32 bits suffice when
-// l * beta <= 30.  With PF the two key rows of a digit polynomial are loaded
-// into registers before its forward transform, so their latency overlaps
-// the transform.
+// l * beta <= 30.  WAVES is the register budget (waves per SIMD): with 4
+// the key rows stream a chunk at a time, the first chunk requested before
+// the digit's forward transform so that the transform hides its latency.
 //
 // Dynamic LDS: twiddle area [TW_WORDS], exchange buffers [XCHG_WORDS],
 // then the n+1 rounded rotation amounts (u16).
@@ -199,15 +199,15 @@ size_t br_lds_bytes(int n) {
 #ifndef BR_CHUNK_FENCE
 #define BR_CHUNK_FENCE() __builtin_amdgcn_sched_barrier(0)
 #endif
-template <class S, int L, typename RT, bool PF>
-__global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(br_waves_per_eu<S>())))
+template <class S, int L, typename RT, int WAVES>
+__global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(WAVES)))
 k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
                const u64 *__restrict__ lut, u64 *__restrict__ out, int n, int beta, int mode,
                int tp_glwe, const u64 *__restrict__ zeta) {
   constexpr int N = S::N, E = S::E, T = S::T;
   static_assert(E <= 8, "at most 8 elements per thread");
-  // key rows a chunk at a time at the 128-register budget of N = 4096
-  constexpr bool CHUNKED = S::LOGN >= 12;
+  // key rows a chunk at a time at the 128-register budget of four waves
+  constexpr bool CHUNKED = WAVES >= 4;
   u64 *tw = lds_dyn;
   LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   uint16_t *rot = (uint16_t *)(lds_dyn + S::TW_WORDS + S::XCHG_WORDS);
@@ -288,13 +288,6 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
             h1[k] = G.load(tid * 8, row + (N + k * T) * 8);
           }
         }
-        if constexpr (PF && !CHUNKED) {
-#pragma unroll
-          for (int k = 0; k < E; ++k) {
-            g0[k] = G.load(tid * 8, row + k * T * 8);
-            g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
-          }
-        }
         // a3: digit polynomial of level t;  a4: forward transform (its first
         // two stages in integer arithmetic while the digits are small)
         RT d[E];
@@ -321,12 +314,13 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
         // a5: multiply-accumulate with the two rows of GGSW_i[u][t]
         // (running sums weak until the inverse transform takes them)
         if constexpr (!CHUNKED) {
-          if constexpr (!PF) {
+          // (requested here, after the transform: loading them before it,
+          // with 8 elements per thread and 3 waves, cost more in spills of
+          // its 32 registers than the early loads saved)
 #pragma unroll
-            for (int k = 0; k < E; ++k) {
-              g0[k] = G.load(tid * 8, row + k * T * 8);
-              g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
-            }
+          for (int k = 0; k < E; ++k) {
+            g0[k] = G.load(tid * 8, row + k * T * 8);
+            g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
           }
 #pragma unroll
           for (int k = 0; k < E; ++k) {
@@ -718,13 +712,15 @@ hipError_t launch_bsk_prepare(const uint64_t *bsk_std, uint64_t *bsk_dev,
   return hipGetLastError();
 }
 
-// Key rows loaded before each digit transform (PF): with 8 elements per
-// thread at N <= 2048 the extra 32 registers per thread cost more in spills
-// than the early loads save, and with 16 per thread (N = 4096) the 64 they
-// would take are not there.
-template <class S>
-constexpr bool br_prefetch() {
-  return false;
+// Compute units of the current device (cached per device).
+static int device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (!cus[dev] &&
+      hipDeviceGetAttribute(&cus[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus[dev] = 0;
+  return cus[dev];
 }
 
 template <class S, int L>
@@ -734,12 +730,26 @@ static hipError_t launch_br_levels(const uint64_t *lwe_in, const uint64_t *bsk_d
                                    int tp_glwe, hipStream_t st) {
   const int n = (int)p.n, beta = (int)p.pbs_base_log;
   const size_t lds = br_lds_bytes<S>(n);
-  if (L * beta <= 30)
-    ROSETTA_LAUNCH((k_blind_rotate<S, L, int32_t, br_prefetch<S>()>), dim3(batch), dim3(S::T), lds,
-                   st, lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);
-  else
-    ROSETTA_LAUNCH((k_blind_rotate<S, L, int64_t, br_prefetch<S>()>), dim3(batch), dim3(S::T), lds,
-                   st, lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);
+#define ROSETTA_BR_INST(WV)                                                                    \
+  do {                                                                                         \
+    if (L * beta <= 30)                                                                        \
+      ROSETTA_LAUNCH((k_blind_rotate<S, L, int32_t, WV>), dim3(batch), dim3(S::T), lds, st,    \
+                     lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);              \
+    else                                                                                       \
+      ROSETTA_LAUNCH((k_blind_rotate<S, L, int64_t, WV>), dim3(batch), dim3(S::T), lds, st,    \
+                     lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);              \
+  } while (0)
+  // At N = 4096 a batch that the CUs hold one workgroup each is latency,
+  // not throughput: the instance compiled for two waves per SIMD (256
+  // registers, no spills; same LDS and key layout) runs it
+  if constexpr (S::LOGN >= 12) {
+    if (batch <= (size_t)device_cus()) {
+      ROSETTA_BR_INST(2);
+      return hipSuccess;
+    }
+  }
+  ROSETTA_BR_INST(br_waves_per_eu<S>());
+#undef ROSETTA_BR_INST
   return hipSuccess;
 }
 
