@@ -7,6 +7,7 @@
 // bootstrapping key is streamed from memory; all workgroups walk the key in
 // the same order i = 0..n-1, so a GGSW row fetched by one workgroup is
 // served from L2 / the Infinity Cache to the others.
+#include <atomic>
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -712,15 +713,18 @@ hipError_t launch_bsk_prepare(const uint64_t *bsk_std, uint64_t *bsk_dev,
   return hipGetLastError();
 }
 
-// Compute units of the current device (cached per device).
+// Compute units of the current device (cached per device; 0 if unknown,
+// which keeps every batch on the throughput instance).
 static int device_cus() {
-  static int cus[64] = {};
+  static std::atomic<int> cus[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  if (!cus[dev] &&
-      hipDeviceGetAttribute(&cus[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-    cus[dev] = 0;
-  return cus[dev];
+  int c = cus[dev].load(std::memory_order_relaxed);
+  if (!c) {
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) c = 0;
+    cus[dev].store(c, std::memory_order_relaxed);
+  }
+  return c;
 }
 
 template <class S, int L>
