@@ -341,7 +341,7 @@ CORNERS = {
     # the largest LWE dimension
     "n2048_N2048": dict(n=2048, N=2048, pbs_level=3, pbs_base_log=8, ks_level=2, ks_base_log=8,
                         msg_bits=3),
-    # the largest ring, general first stage, 4 waves per SIMD
+    # the largest ring, general first stage (a batch of 3: the two-wave instance)
     "l4_b15_N4096": dict(n=24, N=4096, pbs_level=4, pbs_base_log=15, ks_level=3, ks_base_log=6,
                          msg_bits=3),
     # small-digit first stages (integer stages 0-1) at the rings no workload uses
@@ -387,6 +387,39 @@ def test_parameter_corners_bit_exact(O, torch_dev, name):
     ref_out, ref_big = O.pbs(op, cts, ks.bsk, ks.ksk, v, O.NTT, 0, want_big=True)
     assert np.array_equal(big, ref_big)
     assert np.array_equal(out, ref_out)
+
+
+@pytest.mark.parametrize("beta", [8, 15])
+def test_n4096_two_instances_agree(O, torch_dev, beta):
+    """N = 4096 runs a batch that the CUs hold one workgroup each on the
+    blind-rotation instance compiled for two waves per SIMD, a larger one on
+    the four-wave instance: the first CU-count ciphertexts of a batch one
+    larger equal the same ciphertexts run alone, bit for bit (both kernels,
+    extracted and key-switched), and both ends equal the oracle (32- and
+    64-bit rounded values)."""
+    torch = torch_dev
+    prm = dict(n=32, N=4096, pbs_level=3, pbs_base_log=beta, ks_level=3, ks_base_log=6,
+               msg_bits=3, k=1)
+    op = O.Params.make(**{k: v for k, v in prm.items() if k != "k"})
+    ks = O.KeySet(op, 23 + beta, 2.0 ** -40, 2.0 ** -40)
+    bsk = R.bsk_prepare(R.to_device(ks.bsk), prm)
+    ksk = R.ksk_prepare(R.to_device(ks.ksk), prm)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    rng = np.random.default_rng(beta)
+    cts = rng.integers(0, P, (cus + 1, prm["n"] + 1), dtype=np.uint64)
+    v = rng.integers(0, P, prm["N"], dtype=np.uint64)
+    d_v = R.to_device(v)
+    say(f"[two instances beta={beta}] {cus + 1} and {cus} ciphertexts")
+    big_all = R.to_host(R.blind_rotate_extract(R.to_device(cts), bsk, d_v, prm))
+    out_all = R.to_host(R.pbs_batch(R.to_device(cts), bsk, ksk, d_v, prm))
+    big_cu = R.to_host(R.blind_rotate_extract(R.to_device(cts[:cus]), bsk, d_v, prm))
+    out_cu = R.to_host(R.pbs_batch(R.to_device(cts[:cus]), bsk, ksk, d_v, prm))
+    assert np.array_equal(big_all[:cus], big_cu)
+    assert np.array_equal(out_all[:cus], out_cu)
+    pick = [0, cus - 1, cus]
+    ref_out, ref_big = O.pbs(op, cts[pick], ks.bsk, ks.ksk, v, O.NTT, 0, want_big=True)
+    assert np.array_equal(big_all[pick], ref_big)
+    assert np.array_equal(out_all[pick], ref_out)
 
 
 def test_streams(O, torch_dev):
