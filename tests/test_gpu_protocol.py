@@ -105,7 +105,7 @@ def test_lwe_combine_exact(torch_dev):
 
 
 def test_pipeline_small_ring_refined_bit_exact(O, torch_dev):
-    """The refined comparison (2 bits, four PBS per boundary) inside the
+    """The refined comparison (2 bits, three blind rotations per boundary) inside the
     whole pipeline at the small ring, inputs on both sides of every
     boundary at 1.2 coarse steps and in the segments: GPU output = oracle
     output bit for bit (the segment index S too), within 2e-3 of f~(x)
@@ -138,6 +138,40 @@ def test_pipeline_small_ring_refined_bit_exact(O, torch_dev):
         v = centred(O.glwe_phase(ks.glwe_key, got[q])[0]) / scale
         near = np.min(np.abs(xs[q] - tau[1:-1])) < 0.2
         assert abs(v - want[q]) < (0.05 if near else 2e-3), (xs[q], v, want[q])
+
+
+@pytest.mark.parametrize("nseg,refine", [(2, 0), (8, 0), (16, 0), (8, 3)])
+def test_pipeline_small_ring_segment_counts(O, torch_dev, nseg, refine):
+    """The other segment counts the header allows (2, 8 and 16; 8 with a
+    3-bit refined comparison) at the small ring, SiLU on [-8, 8] with
+    uniform segments and one input inside each segment: GPU output = oracle
+    output bit for bit, the segment index S too, and S decrypts to the
+    input's segment."""
+    op = O.Params.make(**{k: v for k, v in SMALL.items() if k != "k"})
+    sigma = 2.0 ** -40
+    ks = O.KeySet(op, 5, sigma, sigma)
+    lp = lparams(256, sx=44, sv=16, sc=58, margin=64, nseg=nseg, refine=refine)
+    tau, A, B, parts, autk, prep, autk_dev, consts = setup(O, op, ks, lp, "silu", -8.0, 8.0,
+                                                           "uniform", sigma, 6)
+    bsk = R.bsk_prepare(R.to_device(ks.bsk), SMALL)
+    ksk = R.ksk_prepare(R.to_device(ks.ksk), SMALL)
+    rng = np.random.default_rng(nseg + refine)
+    xs = np.array([rng.uniform(tau[s] + 0.3 * (tau[s + 1] - tau[s]),
+                               tau[s] + 0.7 * (tau[s + 1] - tau[s])) for s in range(nseg)])
+    x_rlwe, x_cmp = inputs(O, ks, lp, xs, sigma, 60 + nseg, 256)
+    say(f"[protocol] small ring, {nseg} segments, refine {refine}, {len(xs)} inputs")
+    ws = R.empty(R.lookup_workspace_bytes(SMALL, lp, len(xs)) // 8)
+    got = R.to_host(R.lookup_eval(R.to_device(x_rlwe), R.to_device(x_cmp), bsk, ksk, autk_dev,
+                                  prep, consts, SMALL, lp, workspace=ws))
+    ref, st = OL.evaluate(op, ks, autk, lp.trace_level, lp.trace_base_log, parts, lp.nseg,
+                          x_rlwe, x_cmp, want_steps=True)
+    assert np.array_equal(got, ref)
+    wsh = R.to_host(ws)
+    oS = R.lookup_workspace_offset(SMALL, lp, len(xs), R.LOOKUP_PART_S)
+    assert np.array_equal(wsh[oS:oS + len(xs) * (op.n + 1)].reshape(len(xs), -1), st["S"])
+    for q, x in enumerate(xs):
+        s_phase = centred(O.lwe_phase(ks.lwe_key, st["S"][q:q + 1])[0])
+        assert round(s_phase / (P / (2 * nseg))) == int(G.segment_index(x, tau))
 
 
 def test_pipeline_small_ring_bit_exact(O, torch_dev):
