@@ -268,8 +268,8 @@ def lookup_protocol(R, W, stream, steps, batch):
             "batch": batch, "lookups_per_s": round(batch / wall, 2),
             "ms_per_step": round(wall * 1e3, 3),
             "events_ms_per_step": round(e0.elapsed_time(e1) / steps, 3),
-            "per_lookup": {"blind_rotations_step1": 3 * (nseg - 1),
-                           "key_switches_step1": 4 * (nseg - 1),
+            "per_lookup": {"blind_rotations_step1": (3 if refine else 1) * (nseg - 1),
+                           "key_switches_step1": (4 if refine else 1) * (nseg - 1),
                            "blind_rotations_encrypted_tp": nseg + 2,
                            "traces": nseg + 1, "plaintext_products": nseg + 2},
             "decrypt_check": {"sample": int(sample.size), "median_abs_err": float(np.median(err)),

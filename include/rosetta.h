@@ -182,7 +182,8 @@ rosetta_status rosetta_pbs_batch_ws(const uint64_t *lwe_in, const uint64_t *bsk_
  * twiddle tables are static device memory too.  Nothing is allocated: not
  * on the first call on a device (which looks up that device's address of
  * the array and uploads the twiddle table of N with hipMemcpy if no earlier
- * call did), not later.  A batch whose scratch exceeds the array,
+ * call did: a caller that captures a graph makes one call at that N before
+ * it starts capturing), not later.  A batch whose scratch exceeds the array,
  * batch * (N+1) * 8 > ROSETTA_NOALLOC_SCRATCH_BYTES (at most 4094
  * ciphertexts at N = 2048, 2047 at N = 4096), is rejected with
  * ROSETTA_ERR_SIZE before anything is enqueued.  All calls on one device
