@@ -21,7 +21,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "oracle.c")
-PINS = ["tests/test_oracle_field.py", "tests/test_oracle_pbs.py", "tests/test_oracle_mini.py"]
+PINS = ["tests/test_oracle_field.py", "tests/test_oracle_pbs.py", "tests/test_oracle_lookup.py",
+        "tests/test_oracle_mini.py"]
 LOOKUP_PINS = ["tests/test_oracle_lookup.py", "tests/test_oracle_homcomp.py"]
 MINI_PINS = ["tests/test_oracle_mini.py"]
 
@@ -113,6 +114,39 @@ MUTANTS = {
         "subtraction without the added p (wraps modulo 2^128 instead)",
         "u64 or_sub(u64 a, u64 b) { return (u64)(((u128)a + OR_P - b) % OR_P); }",
         "u64 or_sub(u64 a, u64 b) { return (u64)(((u128)a - b) % OR_P); }"),
+    "automorphism_sign": (
+        "automorphism without the sign of exponents past N",
+        "      out[e - N] = or_sub(out[e - N], a[j]);", "      out[e - N] = or_add(out[e - N], a[j]);"),
+    "automorphism_power": (
+        "automorphism X^j -> X^(j (d+2)) instead of X^(j d)",
+        "u64 e = ((u64)j * (u64)d) % (2 * (u64)N);", "u64 e = ((u64)j * (u64)(d + 2)) % (2 * (u64)N);"),
+    "glwe_ks_sign": (
+        "GLWE key switching adding the digit-weighted rows",
+        "res[(size_t)c * N + x] = or_sub(res[(size_t)c * N + x], prod[x]);",
+        "res[(size_t)c * N + x] = or_add(res[(size_t)c * N + x], prod[x]);"),
+    "glwe_ks_body_dropped": (
+        "GLWE key switching starting from a zero body",
+        "    res[N + x] = ct[N + x];", "    res[N + x] = 0;"),
+    "autk_key_power": (
+        "automorphism key of tau_(2^k - 1) instead of tau_(2^k + 1)",
+        "      int d = (1 << k) + 1;\n      u64 *A = autk", "      int d = (1 << k) - 1;\n      u64 *A = autk"),
+    "trace_scale_last": (
+        "trace without the factor N^-1",
+        "for (int j = 0; j < 2 * N; ++j) c[j] = or_mul(ct[j], ninv);",
+        "for (int j = 0; j < 2 * N; ++j) c[j] = ct[j];"),
+    "trace_round_key": (
+        "trace round k keyed with the automorphism key of round k+1",
+        "autk + (size_t)(k - 1) * levels * 2 * N, ks, kind);",
+        "autk + (size_t)(k % rounds) * levels * 2 * N, ks, kind);"),
+    "mul_plain_offset_dropped": (
+        "plaintext product without the offset polynomial",
+        "tmp[N + x] = or_add(prod[x], pb ? pb[x] : 0);", "tmp[N + x] = prod[x];"),
+    "recombine_exponent": (
+        "recombination placing r_s at X^(e_s + 1)",
+        "exps ? (int)exps[s] : s, tmp, N);", "exps ? (int)exps[s] + 1 : s + 1, tmp, N);"),
+    "br_glwe_init_one_side": (
+        "encrypted test polynomial with only its body rotated by X^(-b~)",
+        "  or_poly_monomial_mul(tp, r0, acc, N);", "  memcpy(acc, tp, (size_t)N * sizeof(u64));"),
     "delta_no_padding": (
         "plaintext scale p/M instead of p/2M (no padding bit)",
         "static u64 or_delta(const or_params *P) { return OR_P / (2ULL << P->msg_bits); }",
