@@ -84,3 +84,119 @@ def test_addresses_are_linear_in_the_element():
             for t in range(0, L.T, max(1, L.T // 64)):
                 for k in range(L.E):
                     assert swz(L.idx(q, t, k)) == swz(L.idx(q, t, 0)) ^ swz(k << lo)
+
+
+# ------------------------------------------------- barrier placement model ---
+
+def _wave_block(L, q):
+    return L.T <= 64 or L.lo(q) <= 6
+
+
+def _sequence(logn, kernel, levels=3, spread_barrier=True):
+    """The LDS accesses of one CMux step of the blind rotation (or one round of
+    the trace) and of the start of the next, as the kernel issues them, split
+    into segments by workgroup barriers: a list of {wave: (reads, writes)}.
+    Cross-wave exchanges take a barrier before the writes and one before the
+    reads; exchanges inside each wave take none, except the first one after
+    a read that may leave a wave's block when the two share a buffer (the
+    rule the kernel's LDS buffer object applies)."""
+    L = Layout(logn)
+    N, T = 1 << logn, L.T
+    shared = logn >= 12
+    local_base = 0 if shared else N
+    waves = range((T + 63) // 64)
+    segs = [{}]
+    state = {"spread": False}
+
+    def barrier():
+        segs.append({})
+
+    def access(w, reads=(), writes=()):
+        r, wr = segs[-1].setdefault(w, (set(), set()))
+        r.update(reads)
+        wr.update(writes)
+
+    def own(q, w, base):
+        return {base + swz(L.idx(q, t, k)) for t in range(64 * w, min(64 * w + 64, T))
+                for k in range(L.E)}
+
+    def natural(w):
+        return {t + T * k for t in range(64 * w, min(64 * w + 64, T)) for k in range(L.E)}
+
+    def cross_gather():
+        # write the natural layout, barrier, then read anywhere (rotation or
+        # automorphism: the source index depends on the data)
+        state["spread"] = True
+        barrier()
+        for w in waves:
+            access(w, writes=natural(w))
+        barrier()
+        for w in waves:
+            access(w, reads=set(range(N)))
+
+    def exchange(qa, qb):
+        if _wave_block(L, qa) and _wave_block(L, qb):
+            if shared and state["spread"] and spread_barrier:
+                barrier()
+                state["spread"] = False
+            for w in waves:
+                access(w, writes=own(qa, w, local_base), reads=own(qb, w, local_base))
+        else:
+            state["spread"] = True
+            barrier()
+            for w in waves:
+                access(w, writes=own(qa, w, 0))
+            barrier()
+            for w in waves:
+                access(w, reads=own(qb, w, 0))
+            if _wave_block(L, qb):
+                state["spread"] = False
+
+    def forward():
+        for q in range(L.passes - 1):
+            exchange(q, q + 1)
+
+    def inverse():
+        for q in range(L.passes - 1, 0, -1):
+            exchange(q, q - 1)
+
+    for step in range(2):
+        if kernel == "blind_rotate":
+            for _u in range(2):
+                cross_gather()
+                for _t in range(levels):
+                    forward()
+        else:
+            cross_gather()
+            cross_gather()
+            for _t in range(levels):
+                forward()
+        inverse()
+        inverse()
+    return segs
+
+
+def _hazards(segs):
+    found = []
+    for i, seg in enumerate(segs):
+        for a, (ra, wa) in seg.items():
+            for b, (rb, wb) in seg.items():
+                if a != b and wa & (rb | wb):
+                    found.append((i, a, b))
+    return found
+
+
+@pytest.mark.parametrize("logn", [8, 11, 12])
+@pytest.mark.parametrize("kernel", ["blind_rotate", "trace"])
+def test_no_two_waves_touch_a_word_without_a_barrier(logn, kernel):
+    """Every pair of accesses by two waves to one LDS word, one of them a
+    write, is separated by a workgroup barrier (the tiny ring is one wave)."""
+    assert _hazards(_sequence(logn, kernel)) == []
+
+
+@pytest.mark.parametrize("kernel", ["blind_rotate", "trace"])
+def test_the_model_sees_the_race_the_spread_barrier_removes(kernel):
+    """Without the barrier that follows a read outside the waves' blocks,
+    the shared buffer of N = 4096 has hazards (the second inverse transform
+    of a step writing while the first one's last exchange is still read)."""
+    assert _hazards(_sequence(12, kernel, spread_barrier=False))
