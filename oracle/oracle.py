@@ -336,15 +336,16 @@ def bsk_transform(params: Params, bsk, nthreads=0) -> np.ndarray:
     return out
 
 
-def pbs_prepared(params: Params, lwe_in, fbsk, ksk, v, nthreads=0) -> np.ndarray:
+def pbs_prepared(params: Params, lwe_in, fbsk, ksk, v, nthreads=0, want_big=False):
     """Tier-2 PBS of a batch with the key transform already done
-    (bsk_transform): returns lwe_out."""
+    (bsk_transform): returns lwe_out (and the extracted [count][N+1])."""
     lwe_in = _u64(lwe_in).reshape(-1, params.n + 1)
     fbsk, ksk, v = _u64(fbsk), _u64(ksk), _u64(v)
     out = np.zeros((lwe_in.shape[0], params.n + 1), dtype=np.uint64)
+    big = np.zeros((lwe_in.shape[0], params.N + 1), dtype=np.uint64) if want_big else None
     lib().or_pbs_prepared(C.byref(params), _ptr(lwe_in), None, _ptr(fbsk), _ptr(ksk), _ptr(v),
-                          _ptr(out), None, None, lwe_in.shape[0], NTT, nthreads)
-    return out
+                          _ptr(out), _ptr(big), None, lwe_in.shape[0], NTT, nthreads)
+    return (out, big) if want_big else out
 
 
 # --------------------------------------------------------------------------
