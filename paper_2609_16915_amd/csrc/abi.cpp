@@ -20,6 +20,7 @@
 using namespace rosetta;
 
 static __device__ __align__(256) uint64_t twiddle_store[256 + 512 + 1024 + 2048 + 4096];
+static __device__ __align__(256) uint64_t psi_store[256 + 512 + 1024 + 2048 + 4096];
 
 namespace {
 
@@ -99,6 +100,7 @@ bool any_overlap(const void *a, size_t na, const void *b, size_t nb) {
 
 // Twiddle tables of every supported N live in one static device array (N
 // words each, at offset N - 256: 256 -> 0, 512 -> 256, .., 4096 -> 3840),
+// and the powers psi^0 .. psi^(N-1) in a second one laid out alike, both
 // uploaded per device on first use of an N, so that no entry point ever
 // allocates memory for them.  Host code reaches the array only through the
 // address hipGetSymbolAddress returns on each device.
@@ -106,6 +108,7 @@ constexpr size_t TWIDDLE_STORE_WORDS = 256 + 512 + 1024 + 2048 + 4096;
 
 struct DeviceState {
   uint64_t *twiddle_base = nullptr;  // this device's copy of twiddle_store
+  uint64_t *psi_base = nullptr;      // this device's copy of psi_store
   std::map<uint32_t, uint64_t> ninv;  // N -> N^-1, present once uploaded
   void *workspace = nullptr;
   size_t workspace_bytes = 0;
@@ -134,6 +137,13 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
     if (e != hipSuccess) {
       ds.twiddle_base = nullptr;
       return hip_fail(e, "hipGetSymbolAddress(twiddle_store)");
+    }
+  }
+  if (!ds.psi_base) {
+    e = hipGetSymbolAddress((void **)&ds.psi_base, HIP_SYMBOL(psi_store));
+    if (e != hipSuccess) {
+      ds.psi_base = nullptr;
+      return hip_fail(e, "hipGetSymbolAddress(psi_store)");
     }
   }
   uint64_t *dst = ds.twiddle_base + (N - 256);
@@ -184,9 +194,17 @@ rosetta_status get_tables(uint32_t N, Tables &out) {
     static_assert(256 + 512 + 1024 + 2048 + 4096 == TWIDDLE_STORE_WORDS, "table offsets");
     e = hipMemcpy(dst, z.data(), z.size() * sizeof(u64), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpy(twiddles)");
+    // psi^e, e < N, for the transform-domain rotation (Tables::psi)
+    std::vector<u64> pw(N);
+    pw[0] = 1;
+    for (uint32_t i = 1; i < N; ++i) pw[i] = gl_mul(pw[i - 1], psi);
+    e = hipMemcpy(ds.psi_base + (N - 256), pw.data(), pw.size() * sizeof(u64),
+                  hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(psi powers)");
     it = ds.ninv.emplace(N, gl_inv(N)).first;
   }
   out.zeta = dst;
+  out.psi = ds.psi_base + (N - 256);
   out.ninv = it->second;
   return ROSETTA_OK;
 }

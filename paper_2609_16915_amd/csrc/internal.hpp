@@ -28,6 +28,9 @@ struct Tables {
   // twisted passes holding their block powers and the stages of a last
   // pass that is not twisted stored slot-major (see ntt.hpp)
   const uint64_t *zeta;
+  // N words: psi^e for e = 0 .. N-1 (psi^N = -1 gives the rest), read by the
+  // blind rotation that keeps its accumulator in the transform domain
+  const uint64_t *psi;
   uint64_t ninv;
 };
 

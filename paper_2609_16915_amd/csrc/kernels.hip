@@ -2,8 +2,9 @@
 //
 // One workgroup owns one ciphertext for the whole blind rotation: the GLWE
 // accumulator stays in registers (E coefficients of each component per
-// thread) for all n CMux steps, and every transform is done by the
-// workgroup in registers with LDS transposes (ntt.hpp).  Only the
+// thread, or E transform slots where it is kept in the transform domain) for
+// all n CMux steps, and every transform is done by the workgroup in
+// registers with LDS transposes (ntt.hpp).  Only the
 // bootstrapping key is streamed from memory; all workgroups walk the key in
 // the same order i = 0..n-1, so a GGSW row fetched by one workgroup is
 // served from L2 / the Infinity Cache to the others.
@@ -126,11 +127,13 @@ k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta, u64
 // below, spilled 107 and ran 1010 instead of 902 ms per headline launch).
 // At N = 4096 a workgroup is 512 threads of 8 elements whose exchanges
 // share one LDS buffer (66 KiB): two workgroups share a CU, two waves of
-// each per SIMD, with 128 registers each.  The spills (about 100 registers
-// of the accumulator and the running sums) cost less than the waits that
-// two waves per SIMD leave exposed: 1297 ms per 8192 ciphertexts, against
-// 1426 ms for 16 elements per thread in 256-thread workgroups at 2 waves
-// (radix-16 passes, 5 % fewer instructions).
+// each per SIMD, with 128 registers each.  That instance keeps its
+// accumulator in the transform domain (no separate running sums, see
+// br_transform_domain), which halves the spill traffic that the
+// coefficient-domain loop had at this budget: 1150 ms per 8192
+// ciphertexts, against 1300 ms for the coefficient-domain loop at four
+// waves and 1426 ms for 16 elements per thread in 256-thread workgroups at
+// 2 waves (radix-16 passes, 5 % fewer instructions).
 #ifndef BR_WAVES_PER_EU
 #define BR_WAVES_PER_EU 3
 #endif
@@ -164,12 +167,213 @@ __device__ __forceinline__ u64 rotated_coef(const u64 *v, int j, int r) {
   return neg ? gl_neg(x) : x;
 }
 
+// Key rows per chunk at the four-wave budget, and the scheduling fence
+// between chunks (see br_levels).
+#ifndef BR_KEY_CHUNK
+#define BR_KEY_CHUNK 1
+#endif
+#ifndef BR_CHUNK_FENCE
+#define BR_CHUNK_FENCE() __builtin_amdgcn_sched_barrier(0)
+#endif
+
+// a3-a5 for one component u of the rotated difference, whose rounded
+// coefficients R it consumes: levels from the least significant (t = L-1)
+// up, each pass taking the balanced low digit of R and shifting it out, the
+// last level what remains (the sums over t are exact, so their order is
+// free).  Each digit polynomial is transformed and multiplied into the
+// running sums Y0, Y1 with the two rows of GGSW_i[u][t] (running sums weak,
+// below 2^64 and congruent).
+template <class S, int L, typename RT, bool CHUNKED>
+__device__ __forceinline__ void br_levels(RT (&R)[S::E], u64 (&Y0)[S::E], u64 (&Y1)[S::E],
+                                          const KeyRows &G, int u, int beta, LdsBufs<S> &lds,
+                                          int tid, const u64 *tw) {
+  constexpr int N = S::N, E = S::E, T = S::T;
+  const RT half = (RT)1 << (beta - 1);
+#pragma unroll 1
+  for (int t = L - 1; t >= 0; --t) {
+    const int row = (u * L + t) * 2 * N * 8;  // byte offset of GGSW_i[u][t][0]
+    u64 g0[CHUNKED ? 1 : E], g1[CHUNKED ? 1 : E];
+    // chunked: the first chunk of the two key rows is requested before
+    // the digit transform, so that the transform hides its latency (the
+    // later chunks overlap the chunk before them)
+    u64 h0[BR_KEY_CHUNK], h1[BR_KEY_CHUNK];
+    if constexpr (CHUNKED) {
+#pragma unroll
+      for (int k = 0; k < BR_KEY_CHUNK; ++k) {
+        h0[k] = G.load(tid * 8, row + k * T * 8);
+        h1[k] = G.load(tid * 8, row + (N + k * T) * 8);
+      }
+    }
+    // a3: digit polynomial of level t;  a4: forward transform (its first
+    // two stages in integer arithmetic while the digits are small)
+    RT d[E];
+    if (t == 0) {
+#pragma unroll
+      for (int k = 0; k < E; ++k) d[k] = R[k];
+    } else {
+      // the low beta bits sign-extended, the rest carried up
+      const int dsh = (int)(8 * sizeof(RT)) - beta;
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        d[k] = (RT)((std::make_unsigned_t<RT>)R[k] << dsh) >> dsh;
+        R[k] = (R[k] + half) >> beta;
+      }
+    }
+    u64 x[E];
+    if (beta <= 14) {
+      ntt_forward_small<S, RT>(d, x, lds, tid, tw);
+    } else {
+#pragma unroll
+      for (int k = 0; k < E; ++k) x[k] = gl_from_i64((i64)d[k]);
+      ntt_forward<S>(x, lds, tid, tw);
+    }
+    // a5: multiply-accumulate with the two rows of GGSW_i[u][t]
+    // (running sums weak until the inverse transform takes them)
+    if constexpr (!CHUNKED) {
+      // (requested here, after the transform: loading them before it,
+      // with 8 elements per thread and 3 waves, cost more in spills of
+      // its 32 registers than the early loads saved)
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        g0[k] = G.load(tid * 8, row + k * T * 8);
+        g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
+      }
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        Y0[k] = gl_mul_add_weak(x[k], g0[k], Y0[k]);
+        Y1[k] = gl_mul_add_weak(x[k], g1[k], Y1[k]);
+      }
+    } else {
+      // the key rows a chunk at a time (BR_KEY_CHUNK elements, 4
+      // registers each), the next chunk requested before the products
+      // of the current one, so that 2 chunks rather than 32 registers
+      // hold them (N = 4096, ms per 8192 ciphertexts on one box: chunks
+      // of 1 1322 and 1329 against 1346 and 1349 for chunks of 2; on
+      // another, chunks of 2 with a scheduling fence between chunks
+      // 1297, without it 1327, chunks of 4 1489, all rows after the
+      // transform 1321; at N = 2048, 3 waves, chunks of 2 ran 908
+      // against 902 ms unchunked)
+#pragma unroll
+      for (int k0 = 0; k0 < E; k0 += BR_KEY_CHUNK) {
+        u64 n0[BR_KEY_CHUNK], n1[BR_KEY_CHUNK];
+        if (k0 + BR_KEY_CHUNK < E) {
+#pragma unroll
+          for (int k = 0; k < BR_KEY_CHUNK; ++k) {
+            n0[k] = G.load(tid * 8, row + (k0 + BR_KEY_CHUNK + k) * T * 8);
+            n1[k] = G.load(tid * 8, row + (N + (k0 + BR_KEY_CHUNK + k) * T) * 8);
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < BR_KEY_CHUNK; ++k) {
+          Y0[k0 + k] = gl_mul_add_weak(x[k0 + k], h0[k], Y0[k0 + k]);
+          Y1[k0 + k] = gl_mul_add_weak(x[k0 + k], h1[k], Y1[k0 + k]);
+        }
+        if (k0 + BR_KEY_CHUNK < E) {
+#pragma unroll
+          for (int k = 0; k < BR_KEY_CHUNK; ++k) {
+            h0[k] = n0[k];
+            h1[k] = n1[k];
+          }
+        }
+        BR_CHUNK_FENCE();
+      }
+    }
+  }
+}
+
+// The accumulator in the transform domain (used at N = 4096, four waves per
+// SIMD, where registers are scarcest): H_c = N^-1 NTT(ACC_c).  The key rows
+// are scaled by N^-1 as well, so the step's products add into H directly
+// and no separate running sums are live across the digit transforms; the
+// rotate-subtract becomes a product by the transform of X^a - 1, and the
+// inverse transform of (W^a - 1) H_c is exactly X^a ACC_c - ACC_c (the
+// inverse transform leaves the factor N that cancels N^-1).  Every step is
+// the same arithmetic mod p as the coefficient-domain loop, so the outputs
+// are the same bits.
+//
+// The transform's slot of in-place index j holds the evaluation at
+// psi^(2 rev(j) + 1), so the slot's factor is psi^((2 rev(j) + 1) a) - 1.
+// In the last pass (lo = 0, E = 8) thread tid holds j = 8 tid + k, and
+// 2 rev(j) + 1 = c0 + rev3(k) N/4 with c0 = 2 rev(tid) + 1 (the (LOGN-3)-bit
+// reversal), so the factor is g w8^(rev3(k) a) - 1 with g = psi^(c0 a) and
+// w8 = psi^(N/4) = 7^((p-1)/8) = 2^120: one table read of g per step and
+// shifts for the rest.
+template <class S>
+constexpr bool td_layout_ok() {
+  return S::E == 8 && S::lo(S::PASSES - 1) == 0;
+}
+
+// The table read of g = psi^e (e < 2N) from psi^0 .. psi^(N-1): the raw
+// word and whether it is negated (psi^N = -1), applied where g is used so
+// that the read can be issued a step ahead.
+struct PsiPow {
+  u64 v;
+  bool neg;
+};
+template <int N>
+__device__ __forceinline__ PsiPow psi_read(const u64 *__restrict__ tab, int e) {
+  return PsiPow{tab[e & (N - 1)], (e & N) != 0};
+}
+
+// w[k] = g 2^(120 ((rev3(k) R) mod 8)) - 1 for the eight slots of a thread.
+template <int R>
+__device__ __forceinline__ void spectrum_minus_one_r(u64 g, u64 (&w)[8]) {
+  static_for<0, 8>([&](auto kc) {
+    constexpr int k = decltype(kc)::value;
+    constexpr int e = (120 * ((rev3(k) * R) & 7)) % 192;
+    const u64 m = mul_pow2_mag<e>(g);
+    // -m - 1 = (p - 1) - m
+    w[k] = sign_pow2(e) > 0 ? gl_sub(m, 1) : gl_sub(GL_P - 1, m);
+  });
+}
+__device__ __forceinline__ void spectrum_minus_one(PsiPow gp, int a, u64 (&w)[8]) {
+  const u64 g = gp.neg ? GL_P - gp.v : gp.v;  // a root of unity: never 0
+  switch (__builtin_amdgcn_readfirstlane(a) & 7) {
+    case 0: spectrum_minus_one_r<0>(g, w); break;
+    case 1: spectrum_minus_one_r<1>(g, w); break;
+    case 2: spectrum_minus_one_r<2>(g, w); break;
+    case 3: spectrum_minus_one_r<3>(g, w); break;
+    case 4: spectrum_minus_one_r<4>(g, w); break;
+    case 5: spectrum_minus_one_r<5>(g, w); break;
+    case 6: spectrum_minus_one_r<6>(g, w); break;
+    default: spectrum_minus_one_r<7>(g, w); break;
+  }
+}
+
+// One component's rotated difference X^a ACC - ACC = inverse((W^a - 1) H),
+// rounded to its top l beta bits (natural layout, as the digits need it).
+template <class S, typename RT>
+__device__ __forceinline__ void td_difference(const u64 (&H)[S::E], const u64 (&w)[S::E],
+                                              RT (&R)[S::E], int s, LdsBufs<S> &lds, int tid,
+                                              const u64 *tw) {
+  u64 y[S::E];
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) y[k] = gl_mul(w[k], H[k]);
+  ntt_inverse<S>(y, lds, tid, tw);
+#pragma unroll
+  for (int k = 0; k < S::E; ++k) {
+    if constexpr (sizeof(RT) == 4)
+      R[k] = gl_round_top32(y[k], s);
+    else
+      R[k] = gl_round_top(y[k], s);
+  }
+}
+
+// Whether an instance keeps its accumulator in the transform domain.
+template <class S, int WAVES>
+constexpr bool br_transform_domain() {
+  return S::LOGN >= 12 && WAVES >= 4 && td_layout_ok<S>();
+}
+
 // One workgroup per ciphertext.  Per CMux step i:
 //   a2  D_u = X^(a~_i) ACC_u - ACC_u           (rotation through LDS)
 //   a3  digits of D_u, level t                 (registers)
 //   a4  forward transform of each digit poly   (registers + LDS)
 //   a5  Y_c += digits^ . GGSW_i[u][t][c]^      (key streamed, pre-transformed)
 //   a6  ACC_c += inverse transform of Y_c
+// or, with the accumulator in the transform domain (H_c = N^-1 NTT(ACC_c)):
+//   a2  D_u = inverse transform of (W^a - 1) H_u, both u first
+//   a3-a5 as above, the products added into H_c directly (a6 folded in)
 // The transform-domain key rows are pre-scaled by N^-1 (k_bsk_prepare).
 // RT holds the rounded value before digit extraction: 32 bits suffice when
 // l * beta <= 30.  WAVES is the register budget (waves per SIMD): with 4
@@ -194,21 +398,17 @@ size_t br_lds_bytes(int n) {
 // tp_glwe = g > 1 pairs each LWE selector with g consecutive test-polynomial
 // ciphertexts (workgroup b uses selector b / g), so that one encrypted
 // index selects in several ciphertexts at once.
-#ifndef BR_KEY_CHUNK
-#define BR_KEY_CHUNK 1
-#endif
-#ifndef BR_CHUNK_FENCE
-#define BR_CHUNK_FENCE() __builtin_amdgcn_sched_barrier(0)
-#endif
 template <class S, int L, typename RT, int WAVES>
 __global__ void __launch_bounds__(S::T) __attribute__((amdgpu_waves_per_eu(WAVES)))
 k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
                const u64 *__restrict__ lut, u64 *__restrict__ out, int n, int beta, int mode,
-               int tp_glwe, const u64 *__restrict__ zeta) {
+               int tp_glwe, const u64 *__restrict__ zeta, const u64 *__restrict__ psi_pow,
+               u64 ninv) {
   constexpr int N = S::N, E = S::E, T = S::T;
   static_assert(E <= 8, "at most 8 elements per thread");
   // key rows a chunk at a time at the 128-register budget of four waves
   constexpr bool CHUNKED = WAVES >= 4;
+  constexpr bool TD = br_transform_domain<S, WAVES>();
   u64 *tw = lds_dyn;
   LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   uint16_t *rot = (uint16_t *)(lds_dyn + S::TW_WORDS + S::XCHG_WORDS);
@@ -235,150 +435,118 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
 
   const int s = 64 - L * beta;
   constexpr size_t ggsw_words = (size_t)2 * L * 2 * N;
-  for (int i = 0; i < n; ++i) {
-    const int a = rot[i];
-    const int ar = a & (N - 1);
-    const bool flip = a >= N;
-    u64 Y0[E], Y1[E];
+  if constexpr (TD) {
+    // H_c = N^-1 NTT(ACC_c)
+    const int c0 = 2 * (int)(__builtin_bitreverse32((unsigned)tid) >> (32 - (S::LOGN - 3))) + 1;
+    // (once per ciphertext, so the two components share one copy of the
+    // transform's code; a zero mask needs no transform)
+    u64 HA[E], HB[E];
 #pragma unroll
-    for (int k = 0; k < E; ++k) Y0[k] = Y1[k] = 0;
-    const KeyRows G(bsk + (size_t)i * ggsw_words);
-
+    for (int k = 0; k < E; ++k) HA[k] = 0;
 #pragma unroll 1
-    for (int u = 0; u < 2; ++u) {
-      // a2: rotate-subtract (natural layout), then round away the s low bits
-      RT R[E];
-      {
-        u64 cur[E];
+    for (int c = tp_glwe ? 0 : 1; c < 2; ++c) {
+      u64 x[E];
 #pragma unroll
-        for (int k = 0; k < E; ++k) cur[k] = u ? accB[k] : accA[k];
-        u64 *buf = lds.cross();
+      for (int k = 0; k < E; ++k) x[k] = c ? accB[k] : accA[k];
+      ntt_forward<S>(x, lds, tid, tw);
 #pragma unroll
-        for (int k = 0; k < E; ++k) buf[tid + T * k] = cur[k];
-        __syncthreads();
-#pragma unroll
-        for (int k = 0; k < E; ++k) {
-          const int j = tid + T * k;
-          const bool neg = (j < ar) != flip;
-          const u64 v = buf[(j - ar) & (N - 1)];
-          // -v as p - v: p itself for v = 0 is a valid minuend of gl_sub,
-          // and the rounding maps it to 0 as it does 0
-          const u64 d = gl_sub(neg ? GL_P - v : v, cur[k]);
-          if constexpr (sizeof(RT) == 4)
-            R[k] = gl_round_top32(d, s);  // s = 64 - l beta >= 34 here
-          else
-            R[k] = gl_round_top(d, s);
-        }
-      }
-      // levels from the least significant (t = L-1) up: each pass takes
-      // the balanced low digit of R and shifts it out, the last level is
-      // what remains (the sums over t are exact, so their order is free)
-      const RT half = (RT)1 << (beta - 1);
-#pragma unroll 1
-      for (int t = L - 1; t >= 0; --t) {
-        const int row = (u * L + t) * 2 * N * 8;  // byte offset of GGSW_i[u][t][0]
-        u64 g0[CHUNKED ? 1 : E], g1[CHUNKED ? 1 : E];
-        // chunked: the first chunk of the two key rows is requested before
-        // the digit transform, so that the transform hides its latency (the
-        // later chunks overlap the chunk before them)
-        u64 h0[BR_KEY_CHUNK], h1[BR_KEY_CHUNK];
-        if constexpr (CHUNKED) {
-#pragma unroll
-          for (int k = 0; k < BR_KEY_CHUNK; ++k) {
-            h0[k] = G.load(tid * 8, row + k * T * 8);
-            h1[k] = G.load(tid * 8, row + (N + k * T) * 8);
-          }
-        }
-        // a3: digit polynomial of level t;  a4: forward transform (its first
-        // two stages in integer arithmetic while the digits are small)
-        RT d[E];
-        if (t == 0) {
-#pragma unroll
-          for (int k = 0; k < E; ++k) d[k] = R[k];
-        } else {
-          // the low beta bits sign-extended, the rest carried up
-          const int dsh = (int)(8 * sizeof(RT)) - beta;
-#pragma unroll
-          for (int k = 0; k < E; ++k) {
-            d[k] = (RT)((std::make_unsigned_t<RT>)R[k] << dsh) >> dsh;
-            R[k] = (R[k] + half) >> beta;
-          }
-        }
-        u64 x[E];
-        if (beta <= 14) {
-          ntt_forward_small<S, RT>(d, x, lds, tid, tw);
-        } else {
-#pragma unroll
-          for (int k = 0; k < E; ++k) x[k] = gl_from_i64((i64)d[k]);
-          ntt_forward<S>(x, lds, tid, tw);
-        }
-        // a5: multiply-accumulate with the two rows of GGSW_i[u][t]
-        // (running sums weak until the inverse transform takes them)
-        if constexpr (!CHUNKED) {
-          // (requested here, after the transform: loading them before it,
-          // with 8 elements per thread and 3 waves, cost more in spills of
-          // its 32 registers than the early loads saved)
-#pragma unroll
-          for (int k = 0; k < E; ++k) {
-            g0[k] = G.load(tid * 8, row + k * T * 8);
-            g1[k] = G.load(tid * 8, row + (N + k * T) * 8);
-          }
-#pragma unroll
-          for (int k = 0; k < E; ++k) {
-            Y0[k] = gl_mul_add_weak(x[k], g0[k], Y0[k]);
-            Y1[k] = gl_mul_add_weak(x[k], g1[k], Y1[k]);
-          }
-        } else {
-          // the key rows a chunk at a time (BR_KEY_CHUNK elements, 4
-          // registers each), the next chunk requested before the products
-          // of the current one, so that 2 chunks rather than 32 registers
-          // hold them (N = 4096, ms per 8192 ciphertexts on one box: chunks
-          // of 1 1322 and 1329 against 1346 and 1349 for chunks of 2; on
-          // another, chunks of 2 with a scheduling fence between chunks
-          // 1297, without it 1327, chunks of 4 1489, all rows after the
-          // transform 1321; at N = 2048, 3 waves, chunks of 2 ran 908
-          // against 902 ms unchunked)
-#pragma unroll
-          for (int k0 = 0; k0 < E; k0 += BR_KEY_CHUNK) {
-            u64 n0[BR_KEY_CHUNK], n1[BR_KEY_CHUNK];
-            if (k0 + BR_KEY_CHUNK < E) {
-#pragma unroll
-              for (int k = 0; k < BR_KEY_CHUNK; ++k) {
-                n0[k] = G.load(tid * 8, row + (k0 + BR_KEY_CHUNK + k) * T * 8);
-                n1[k] = G.load(tid * 8, row + (N + (k0 + BR_KEY_CHUNK + k) * T) * 8);
-              }
-            }
-#pragma unroll
-            for (int k = 0; k < BR_KEY_CHUNK; ++k) {
-              Y0[k0 + k] = gl_mul_add_weak(x[k0 + k], h0[k], Y0[k0 + k]);
-              Y1[k0 + k] = gl_mul_add_weak(x[k0 + k], h1[k], Y1[k0 + k]);
-            }
-            if (k0 + BR_KEY_CHUNK < E) {
-#pragma unroll
-              for (int k = 0; k < BR_KEY_CHUNK; ++k) {
-                h0[k] = n0[k];
-                h1[k] = n1[k];
-              }
-            }
-            BR_CHUNK_FENCE();
-          }
-        }
+      for (int k = 0; k < E; ++k) {
+        const u64 h = gl_mul(x[k], ninv);
+        if (c)
+          HB[k] = h;
+        else
+          HA[k] = h;
       }
     }
-    // a6: back to coefficients, accumulate (unrolled: with c a compile-time
-    // index the accumulator updates need no per-element selection)
+    PsiPow g = psi_read<N>(psi_pow, c0 * (int)rot[0]);
+    for (int i = 0; i < n; ++i) {
+      const int a = rot[i];
+      u64 w[E];
+      spectrum_minus_one(g, a, w);
+      if (i + 1 < n) g = psi_read<N>(psi_pow, c0 * (int)rot[i + 1]);
+      // a2 (both components before the products change H), then a3-a5
+      RT RA[E], RB[E];
+      td_difference<S, RT>(HA, w, RA, s, lds, tid, tw);
+      td_difference<S, RT>(HB, w, RB, s, lds, tid, tw);
+      const KeyRows G(bsk + (size_t)i * ggsw_words);
+      RT R[E];
 #pragma unroll
+      for (int k = 0; k < E; ++k) R[k] = RA[k];
+#pragma unroll 1
+      for (int u = 0; u < 2; ++u) {
+        br_levels<S, L, RT, CHUNKED>(R, HA, HB, G, u, beta, lds, tid, tw);
+#pragma unroll
+        for (int k = 0; k < E; ++k) R[k] = RB[k];
+      }
+    }
+    // back to coefficients: the inverse transform of H_c is N N^-1 ACC_c
+#pragma unroll 1
     for (int c = 0; c < 2; ++c) {
       u64 y[E];
 #pragma unroll
-      for (int k = 0; k < E; ++k) y[k] = gl_canon(c ? Y1[k] : Y0[k]);
+      for (int k = 0; k < E; ++k) y[k] = gl_canon(c ? HB[k] : HA[k]);
       ntt_inverse<S>(y, lds, tid, tw);
 #pragma unroll
       for (int k = 0; k < E; ++k) {
         if (c)
-          accB[k] = gl_add(accB[k], y[k]);
+          accB[k] = y[k];
         else
-          accA[k] = gl_add(accA[k], y[k]);
+          accA[k] = y[k];
+      }
+    }
+  } else {
+    for (int i = 0; i < n; ++i) {
+      const int a = rot[i];
+      const int ar = a & (N - 1);
+      const bool flip = a >= N;
+      u64 Y0[E], Y1[E];
+#pragma unroll
+      for (int k = 0; k < E; ++k) Y0[k] = Y1[k] = 0;
+      const KeyRows G(bsk + (size_t)i * ggsw_words);
+
+#pragma unroll 1
+      for (int u = 0; u < 2; ++u) {
+        // a2: rotate-subtract (natural layout), then round away the s low bits
+        RT R[E];
+        {
+          u64 cur[E];
+#pragma unroll
+          for (int k = 0; k < E; ++k) cur[k] = u ? accB[k] : accA[k];
+          u64 *buf = lds.cross();
+#pragma unroll
+          for (int k = 0; k < E; ++k) buf[tid + T * k] = cur[k];
+          __syncthreads();
+#pragma unroll
+          for (int k = 0; k < E; ++k) {
+            const int j = tid + T * k;
+            const bool neg = (j < ar) != flip;
+            const u64 v = buf[(j - ar) & (N - 1)];
+            // -v as p - v: p itself for v = 0 is a valid minuend of gl_sub,
+            // and the rounding maps it to 0 as it does 0
+            const u64 d = gl_sub(neg ? GL_P - v : v, cur[k]);
+            if constexpr (sizeof(RT) == 4)
+              R[k] = gl_round_top32(d, s);  // s = 64 - l beta >= 34 here
+            else
+              R[k] = gl_round_top(d, s);
+          }
+        }
+        br_levels<S, L, RT, CHUNKED>(R, Y0, Y1, G, u, beta, lds, tid, tw);
+      }
+      // a6: back to coefficients, accumulate (unrolled: with c a compile-time
+      // index the accumulator updates need no per-element selection)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        u64 y[E];
+#pragma unroll
+        for (int k = 0; k < E; ++k) y[k] = gl_canon(c ? Y1[k] : Y0[k]);
+        ntt_inverse<S>(y, lds, tid, tw);
+#pragma unroll
+        for (int k = 0; k < E; ++k) {
+          if (c)
+            accB[k] = gl_add(accB[k], y[k]);
+          else
+            accA[k] = gl_add(accA[k], y[k]);
+        }
       }
     }
   }
@@ -738,10 +906,12 @@ static hipError_t launch_br_levels(const uint64_t *lwe_in, const uint64_t *bsk_d
   do {                                                                                         \
     if (L * beta <= 30)                                                                        \
       ROSETTA_LAUNCH((k_blind_rotate<S, L, int32_t, WV>), dim3(batch), dim3(S::T), lds, st,    \
-                     lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);              \
+                     lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta,  \
+                     tb.psi, tb.ninv);              \
     else                                                                                       \
       ROSETTA_LAUNCH((k_blind_rotate<S, L, int64_t, WV>), dim3(batch), dim3(S::T), lds, st,    \
-                     lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta);              \
+                     lwe_in, bsk_dev, lut, out, n, beta, mode, tp_glwe, tb.zeta,  \
+                     tb.psi, tb.ninv);              \
   } while (0)
   // At N = 4096 a batch that the CUs hold one workgroup each is latency,
   // not throughput: the instance compiled for two waves per SIMD (256

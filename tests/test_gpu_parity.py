@@ -389,19 +389,21 @@ def test_parameter_corners_bit_exact(O, torch_dev, name):
     assert np.array_equal(out, ref_out)
 
 
-@pytest.mark.parametrize("beta", [8, 15])
-def test_n4096_two_instances_agree(O, torch_dev, beta):
+@pytest.mark.parametrize("level,beta", [(3, 8), (3, 15), (1, 20), (2, 16), (4, 7)])
+def test_n4096_two_instances_agree(O, torch_dev, level, beta):
     """N = 4096 runs a batch that the CUs hold one workgroup each on the
-    blind-rotation instance compiled for two waves per SIMD, a larger one on
-    the four-wave instance: the first CU-count ciphertexts of a batch one
+    blind-rotation instance compiled for two waves per SIMD (accumulator in
+    coefficients), a larger one on the four-wave instance (accumulator in
+    the transform domain): the first CU-count ciphertexts of a batch one
     larger equal the same ciphertexts run alone, bit for bit (both kernels,
-    extracted and key-switched), and both ends equal the oracle (32- and
-    64-bit rounded values)."""
+    extracted and key-switched), and both ends equal the oracle, for every
+    level count (32- and 64-bit rounded values, digits through the small
+    and the general forward transform)."""
     torch = torch_dev
-    prm = dict(n=32, N=4096, pbs_level=3, pbs_base_log=beta, ks_level=3, ks_base_log=6,
+    prm = dict(n=32, N=4096, pbs_level=level, pbs_base_log=beta, ks_level=3, ks_base_log=6,
                msg_bits=3, k=1)
     op = O.Params.make(**{k: v for k, v in prm.items() if k != "k"})
-    ks = O.KeySet(op, 23 + beta, 2.0 ** -40, 2.0 ** -40)
+    ks = O.KeySet(op, 23 + beta + 100 * level, 2.0 ** -40, 2.0 ** -40)
     bsk = R.bsk_prepare(R.to_device(ks.bsk), prm)
     ksk = R.ksk_prepare(R.to_device(ks.ksk), prm)
     cus = torch.cuda.get_device_properties(0).multi_processor_count
@@ -409,7 +411,7 @@ def test_n4096_two_instances_agree(O, torch_dev, beta):
     cts = rng.integers(0, P, (cus + 1, prm["n"] + 1), dtype=np.uint64)
     v = rng.integers(0, P, prm["N"], dtype=np.uint64)
     d_v = R.to_device(v)
-    say(f"[two instances beta={beta}] {cus + 1} and {cus} ciphertexts")
+    say(f"[two instances level={level} beta={beta}] {cus + 1} and {cus} ciphertexts")
     big_all = R.to_host(R.blind_rotate_extract(R.to_device(cts), bsk, d_v, prm))
     out_all = R.to_host(R.pbs_batch(R.to_device(cts), bsk, ksk, d_v, prm))
     big_cu = R.to_host(R.blind_rotate_extract(R.to_device(cts[:cus]), bsk, d_v, prm))

@@ -160,6 +160,22 @@ def _sequence(logn, kernel, levels=3, spread_barrier=True):
         for q in range(L.passes - 1, 0, -1):
             exchange(q, q - 1)
 
+    if kernel == "blind_rotate_td":
+        # accumulator in the transform domain: two forward transforms first,
+        # then per step the two inverse transforms of the rotated
+        # differences before the digit transforms (no rotation exchange),
+        # and two inverse transforms at the end
+        forward()
+        forward()
+        for step in range(2):
+            inverse()
+            inverse()
+            for _u in range(2):
+                for _t in range(levels):
+                    forward()
+        inverse()
+        inverse()
+        return segs
     for step in range(2):
         if kernel == "blind_rotate":
             for _u in range(2):
@@ -187,16 +203,17 @@ def _hazards(segs):
 
 
 @pytest.mark.parametrize("logn", [8, 11, 12])
-@pytest.mark.parametrize("kernel", ["blind_rotate", "trace"])
+@pytest.mark.parametrize("kernel", ["blind_rotate", "blind_rotate_td", "trace"])
 def test_no_two_waves_touch_a_word_without_a_barrier(logn, kernel):
     """Every pair of accesses by two waves to one LDS word, one of them a
     write, is separated by a workgroup barrier (the tiny ring is one wave)."""
     assert _hazards(_sequence(logn, kernel)) == []
 
 
-@pytest.mark.parametrize("kernel", ["blind_rotate", "trace"])
+@pytest.mark.parametrize("kernel", ["blind_rotate", "blind_rotate_td", "trace"])
 def test_the_model_sees_the_race_the_spread_barrier_removes(kernel):
     """Without the barrier that follows a read outside the waves' blocks,
     the shared buffer of N = 4096 has hazards (the second inverse transform
-    of a step writing while the first one's last exchange is still read)."""
+    of a step writing while the first one's last exchange is still read;
+    in the transform-domain loop the same pair opens every step)."""
     assert _hazards(_sequence(12, kernel, spread_barrier=False))
