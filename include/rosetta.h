@@ -179,11 +179,11 @@ rosetta_status rosetta_pbs_batch_ws(const uint64_t *lwe_in, const uint64_t *bsk_
  * between them (the extracted ciphertexts, rosetta_pbs_workspace_bytes
  * bytes) is a static device array of ROSETTA_NOALLOC_SCRATCH_BYTES that
  * each GPU the library runs on holds until the process ends, and the
- * twiddle tables are static device memory too.  Nothing is allocated: not
- * on the first call on a device (which looks up that device's address of
- * the array and uploads the twiddle table of N with hipMemcpy if no earlier
- * call did: a caller that captures a graph makes one call at that N before
- * it starts capturing), not later.  A batch whose scratch exceeds the array,
+ * transform tables (the twiddles and the powers of psi) are static device
+ * memory too.  Nothing is allocated: not on the first call on a device
+ * (which looks up that device's addresses of the arrays and uploads the
+ * tables of N with hipMemcpy if no earlier call did: a caller that captures
+ * a graph makes one call at that N before it starts capturing), not later.  A batch whose scratch exceeds the array,
  * batch * (N+1) * 8 > ROSETTA_NOALLOC_SCRATCH_BYTES (at most 4094
  * ciphertexts at N = 2048, 2047 at N = 4096), is rejected with
  * ROSETTA_ERR_SIZE before anything is enqueued.  All calls on one device
@@ -646,8 +646,9 @@ rosetta_status rosetta_autk_keygen(uint64_t seed, const rosetta_params *params, 
                                    uint32_t base_log, double sigma, const uint64_t *glwe_key,
                                    uint64_t *autk_std);
 
-/* Release the library's device state on every device it touched (twiddle
- * tables, workspaces).  The library re-initialises lazily afterwards. */
+/* Release the library's device state on every device it touched (the
+ * workspaces; the transform tables live in static device memory and stay).
+ * The library re-initialises lazily afterwards. */
 rosetta_status rosetta_shutdown(void);
 
 #ifdef __cplusplus

@@ -727,7 +727,7 @@ rosetta_status rosetta_shutdown(void) {
   for (auto &kv : g_dev) {
     (void)hipSetDevice(kv.first);
     (void)hipDeviceSynchronize();
-    // the twiddle tables stay: they live in static device memory
+    // the transform tables stay: they live in static device memory
     if (kv.second.workspace) (void)hipFree(kv.second.workspace);
     kv.second.workspace = nullptr;
     kv.second.workspace_bytes = 0;
