@@ -122,16 +122,15 @@ k_poly_mul(const u64 *a, const u64 *b, u64 *c, const u64 *__restrict__ zeta, u64
 
 // Waves per SIMD the blind-rotation kernel is compiled for.  Up to N = 2048
 // three workgroups fit a CU's LDS, so the kernel targets 3 waves per SIMD
-// (<= 168 registers; the few spills touch only the accumulator, read twice
-// per step; 4 waves at 128 registers, with the LDS of the N = 4096 layout
-// below, spilled 107 and ran 1010 instead of 902 ms per headline launch).
+// (<= 168 registers, a few of them spilled; 4 waves at 128 registers, with
+// the LDS of the N = 4096 layout below, spilled 107 and ran 1010 instead of
+// 902 ms per headline launch with the coefficient-domain loop).
 // At N = 4096 a workgroup is 512 threads of 8 elements whose exchanges
 // share one LDS buffer (66 KiB): two workgroups share a CU, two waves of
-// each per SIMD, with 128 registers each.  That instance keeps its
-// accumulator in the transform domain (no separate running sums, see
-// br_transform_domain), which halves the spill traffic that the
-// coefficient-domain loop had at this budget: 1150 ms per 8192
-// ciphertexts, against 1300 ms for the coefficient-domain loop at four
+// each per SIMD, with 128 registers each.  With the accumulator in the
+// transform domain (no separate running sums, see br_transform_domain) the
+// spill traffic of that budget stays in the L2: 1159 ms per 8192
+// ciphertexts, against 1301 ms for the coefficient-domain loop at four
 // waves and 1426 ms for 16 elements per thread in 256-thread workgroups at
 // 2 waves (radix-16 passes, 5 % fewer instructions).
 #ifndef BR_WAVES_PER_EU
@@ -281,8 +280,8 @@ __device__ __forceinline__ void br_levels(RT (&R)[S::E], u64 (&Y0)[S::E], u64 (&
   }
 }
 
-// The accumulator in the transform domain (used at N = 4096, four waves per
-// SIMD, where registers are scarcest): H_c = N^-1 NTT(ACC_c).  The key rows
+// The accumulator in the transform domain (br_transform_domain): H_c =
+// N^-1 NTT(ACC_c).  The key rows
 // are scaled by N^-1 as well, so the step's products add into H directly
 // and no separate running sums are live across the digit transforms; the
 // rotate-subtract becomes a product by the transform of X^a - 1, and the
@@ -359,10 +358,16 @@ __device__ __forceinline__ void td_difference(const u64 (&H)[S::E], const u64 (&
   }
 }
 
-// Whether an instance keeps its accumulator in the transform domain.
-template <class S, int WAVES>
+// Whether an instance keeps its accumulator in the transform domain: every
+// instance at N >= 2048 (the rings of the workloads).  Measured against the
+// coefficient-domain loop on one box: N = 4096 at four waves 1301 -> 1159 ms
+// per 8192 ciphertexts (its spill traffic had gone beyond the L2), the 32
+// reciprocals at two waves 47.5 -> 46.9 ms, at N = 2048 the 64-bit-rounding
+// lookup key set 923 -> 911 ms and the headline and GPT-2 shapes 0.4 and
+// 0.8 % faster.  Smaller rings keep the coefficient-domain loop.
+template <class S>
 constexpr bool br_transform_domain() {
-  return S::LOGN >= 12 && WAVES >= 4 && td_layout_ok<S>();
+  return S::LOGN >= 11 && td_layout_ok<S>();
 }
 
 // One workgroup per ciphertext.  Per CMux step i:
@@ -408,7 +413,7 @@ k_blind_rotate(const u64 *__restrict__ lwe_in, const u64 *__restrict__ bsk,
   static_assert(E <= 8, "at most 8 elements per thread");
   // key rows a chunk at a time at the 128-register budget of four waves
   constexpr bool CHUNKED = WAVES >= 4;
-  constexpr bool TD = br_transform_domain<S, WAVES>();
+  constexpr bool TD = br_transform_domain<S>();
   u64 *tw = lds_dyn;
   LdsBufs<S> lds(lds_dyn + S::TW_WORDS);
   uint16_t *rot = (uint16_t *)(lds_dyn + S::TW_WORDS + S::XCHG_WORDS);

@@ -392,13 +392,13 @@ def test_parameter_corners_bit_exact(O, torch_dev, name):
 @pytest.mark.parametrize("level,beta", [(3, 8), (3, 15), (1, 20), (2, 16), (4, 7)])
 def test_n4096_two_instances_agree(O, torch_dev, level, beta):
     """N = 4096 runs a batch that the CUs hold one workgroup each on the
-    blind-rotation instance compiled for two waves per SIMD (accumulator in
-    coefficients), a larger one on the four-wave instance (accumulator in
-    the transform domain): the first CU-count ciphertexts of a batch one
-    larger equal the same ciphertexts run alone, bit for bit (both kernels,
-    extracted and key-switched), and both ends equal the oracle, for every
-    level count (32- and 64-bit rounded values, digits through the small
-    and the general forward transform)."""
+    blind-rotation instance compiled for two waves per SIMD, a larger one on
+    the four-wave instance (both with the accumulator in the transform
+    domain, at different register budgets): the first CU-count ciphertexts
+    of a batch one larger equal the same ciphertexts run alone, bit for bit
+    (both kernels, extracted and key-switched), and both ends equal the
+    oracle, for every level count (32- and 64-bit rounded values, digits
+    through the small and the general forward transform)."""
     torch = torch_dev
     prm = dict(n=32, N=4096, pbs_level=level, pbs_base_log=beta, ks_level=3, ks_base_log=6,
                msg_bits=3, k=1)
