@@ -180,8 +180,9 @@ __device__ __forceinline__ u64 rotated_coef(const u64 *v, int j, int r) {
 // up, each pass taking the balanced low digit of R and shifting it out, the
 // last level what remains (the sums over t are exact, so their order is
 // free).  Each digit polynomial is transformed and multiplied into the
-// running sums Y0, Y1 with the two rows of GGSW_i[u][t] (running sums weak,
-// below 2^64 and congruent).
+// running sums Y0, Y1 (the transform-domain accumulator itself, where the
+// kernel keeps one) with the two rows of GGSW_i[u][t] (sums weak, below
+// 2^64 and congruent).
 template <class S, int L, typename RT, bool CHUNKED>
 __device__ __forceinline__ void br_levels(RT (&R)[S::E], u64 (&Y0)[S::E], u64 (&Y1)[S::E],
                                           const KeyRows &G, int u, int beta, LdsBufs<S> &lds,
@@ -280,15 +281,14 @@ __device__ __forceinline__ void br_levels(RT (&R)[S::E], u64 (&Y0)[S::E], u64 (&
   }
 }
 
-// The accumulator in the transform domain (br_transform_domain): H_c =
-// N^-1 NTT(ACC_c).  The key rows
-// are scaled by N^-1 as well, so the step's products add into H directly
-// and no separate running sums are live across the digit transforms; the
-// rotate-subtract becomes a product by the transform of X^a - 1, and the
-// inverse transform of (W^a - 1) H_c is exactly X^a ACC_c - ACC_c (the
-// inverse transform leaves the factor N that cancels N^-1).  Every step is
-// the same arithmetic mod p as the coefficient-domain loop, so the outputs
-// are the same bits.
+// The accumulator in the transform domain (br_transform_domain):
+// H_c = N^-1 NTT(ACC_c).  The key rows are scaled by N^-1 as well, so the
+// step's products add into H directly and no separate running sums are
+// live across the digit transforms; the rotate-subtract becomes a product
+// by the transform of X^a - 1, and the inverse transform of (W^a - 1) H_c
+// is exactly X^a ACC_c - ACC_c (the inverse transform leaves the factor N
+// that cancels N^-1).  Every step is the same arithmetic mod p as the
+// coefficient-domain loop, so the outputs are the same bits.
 //
 // The transform's slot of in-place index j holds the evaluation at
 // psi^(2 rev(j) + 1), so the slot's factor is psi^((2 rev(j) + 1) a) - 1.
